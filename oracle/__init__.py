@@ -1,0 +1,155 @@
+"""ctypes shim over the plain-C CPU oracle (kmeans_oracle.c).
+
+TEST INFRASTRUCTURE ONLY: the oracle is the slow, obviously correct statement
+of Algorithm 1's Lloyd iteration (assign by Eq. (2), centres of gravity by
+Eq. (1), stop on congruent centres) that the GPU library is checked against.
+Only the tests, the smoke check and the benchmark's CPU-baseline leg use it;
+the GPU library never imports, links or calls it.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(_HERE, "kmeans_oracle.c")
+LIB = os.path.join(_HERE, "libkmeans_oracle.so")
+CFLAGS = ["-std=c99", "-O2", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared"]
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (no fused multiply-add, no fast-math)."""
+    if force or not os.path.exists(LIB):
+        tmp = LIB + ".tmp"
+        subprocess.check_call(["gcc", *CFLAGS, "-o", tmp, SRC, "-lm"])
+        os.replace(tmp, LIB)
+    return LIB
+
+
+def _bind(path: str):
+    lib = ctypes.CDLL(path)
+    p = ctypes.c_void_p
+    i64, i32 = ctypes.c_int64, ctypes.c_int32
+    lib.oracle_assign.argtypes = [p, i64, i32, p, i32, p, p, p]
+    lib.oracle_assign.restype = ctypes.c_int
+    lib.oracle_update.argtypes = [p, i64, i32, p, i32, p, p, p]
+    lib.oracle_update.restype = ctypes.c_int
+    lib.oracle_run.argtypes = [p, i64, i32, i32, p, i32, i32, p, p, p, p, p, p]
+    lib.oracle_run.restype = ctypes.c_int
+    lib.oracle_sse.argtypes = [p, i64, i32, p, p, i32]
+    lib.oracle_sse.restype = ctypes.c_double
+    return lib
+
+
+_default = None
+
+
+def _load():
+    global _default
+    if _default is None:
+        # KMEANS_ORACLE_LIB points the shim at another build of the oracle; the
+        # tests that plant mistakes in a copy of the oracle source use it.
+        path = os.environ.get("KMEANS_ORACLE_LIB")
+        if not path:
+            path = LIB
+            if not os.path.exists(path):
+                build(force=False)
+        _default = _bind(path)
+    return _default
+
+
+def _f32(a):
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    if a.ndim != 2:
+        raise ValueError("expected a 2-D array")
+    return a
+
+
+def _ptr(a):
+    return ctypes.c_void_p(a.ctypes.data) if a is not None else None
+
+
+def assign(X, C, with_dist: bool = False):
+    """Algorithm 1 steps 2/4: nearest centre per object (lowest index on ties).
+
+    Returns labels (int32 [n]); with_dist also returns the best and second-best
+    squared distances (fp64 [n]); second-best is +inf when K == 1.
+    """
+    X, C = _f32(X), _f32(C)
+    n, M = X.shape
+    K = C.shape[0]
+    if C.shape[1] != M:
+        raise ValueError("feature count mismatch")
+    labels = np.empty(n, np.int32)
+    d1 = np.empty(n, np.float64) if with_dist else None
+    d2 = np.empty(n, np.float64) if with_dist else None
+    rc = _load().oracle_assign(_ptr(X), n, M, _ptr(C), K, _ptr(labels), _ptr(d1), _ptr(d2))
+    if rc:
+        raise ValueError(f"oracle_assign failed ({rc})")
+    return (labels, d1, d2) if with_dist else labels
+
+
+def update(X, labels, K: int, prev):
+    """Eq. (1): centres of gravity of the labelled objects; empty clusters keep
+    prev. Returns (centers fp32 [K,M], counts int32 [K])."""
+    X, prev = _f32(X), _f32(prev)
+    n, M = X.shape
+    labels = np.ascontiguousarray(labels, dtype=np.int32)
+    if labels.shape != (n,) or prev.shape != (K, M):
+        raise ValueError("shape mismatch")
+    centers = np.empty((K, M), np.float32)
+    counts = np.empty(K, np.int32)
+    rc = _load().oracle_update(_ptr(X), n, M, _ptr(labels), K, _ptr(prev),
+                               _ptr(centers), _ptr(counts))
+    if rc:
+        raise ValueError(f"oracle_update failed ({rc})")
+    return centers, counts
+
+
+def run(X, K: int, init, max_iter: int, fixed: bool = False, with_dist: bool = False):
+    """Algorithm 1 steps 2-7 from the given initial centres.
+
+    Returns (labels, centers, counts, iterations) and, with with_dist, the last
+    assignment's best / second-best squared distances.
+    """
+    X, init = _f32(X), _f32(init)
+    n, M = X.shape
+    if init.shape != (K, M):
+        raise ValueError("init shape mismatch")
+    labels = np.empty(n, np.int32)
+    centers = np.empty((K, M), np.float32)
+    counts = np.empty(K, np.int32)
+    iters = ctypes.c_int32(0)
+    d1 = np.empty(n, np.float64) if with_dist else None
+    d2 = np.empty(n, np.float64) if with_dist else None
+    rc = _load().oracle_run(_ptr(X), n, M, K, _ptr(init), int(max_iter), int(bool(fixed)),
+                            _ptr(labels), _ptr(centers), _ptr(counts),
+                            ctypes.byref(iters), _ptr(d1), _ptr(d2))
+    if rc:
+        raise ValueError(f"oracle_run failed ({rc})")
+    out = (labels, centers, counts, int(iters.value))
+    return out + (d1, d2) if with_dist else out
+
+
+def sse(X, labels, C) -> float:
+    """Objective: sum of squared distances of objects to their centres (fp64)."""
+    X, C = _f32(X), _f32(C)
+    labels = np.ascontiguousarray(labels, dtype=np.int32)
+    return float(_load().oracle_sse(_ptr(X), X.shape[0], X.shape[1], _ptr(labels),
+                                    _ptr(C), C.shape[0]))
+
+
+def gap_rel(d1, d2):
+    """(d2 - d1) / d2 per object: 0 at an exact tie, 1 when there is no
+    competing centre (K == 1); 0 when d2 == 0."""
+    d1 = np.asarray(d1, np.float64)
+    d2 = np.asarray(d2, np.float64)
+    g = np.ones_like(d1)
+    fin = np.isfinite(d2)
+    pos = fin & (d2 > 0)
+    g[pos] = (d2[pos] - d1[pos]) / d2[pos]
+    g[fin & (d2 <= 0)] = 0.0
+    return g

@@ -1,0 +1,201 @@
+/*
+ * CPU oracle for the Lloyd iteration of K-means (Algorithm 1 of Litvinenko,
+ * "Using of GPUs for cluster analysis of large data by K-means method").
+ *
+ * TEST INFRASTRUCTURE ONLY. This file is the plain, slow, single-threaded
+ * statement of what the GPU library must compute; only the test suite, the
+ * smoke check and the benchmark's CPU-baseline leg may load it. It shares no
+ * code, header or constant with the GPU library.
+ *
+ * It follows the single-threaded regime (Algorithm 2, steps 4-8, which is
+ * Algorithm 1 steps 2-7 with given initial centres):
+ *   assign   : every object goes to the cluster whose centre is closest
+ *              (Algorithm 1 steps 2 and 4, distance of Eq. (2));
+ *   update   : each cluster's centre of gravity, Eq. (1)
+ *              (Algorithm 1 steps 3 and 5);
+ *   compare  : stop when the centres of the last two iterations are congruent
+ *              (Algorithm 1 steps 6 and 7).
+ *
+ * Readings where the paper is silent (each is listed with its reason in the
+ * design notes of the repository):
+ *   - distances are compared squared (same argmin as Eq. (2), no sqrt);
+ *   - arithmetic is fp64; inputs and stored centres are fp32; for every
+ *     object and centre the squared distance is accumulated as
+ *         e = (double)x_j - (double)c_j ;  d = d + e*e
+ *     for j ascending, each operation rounded separately (no fused
+ *     multiply-add; build with -ffp-contract=off);
+ *   - ties go to the lowest cluster index (strict '<' while scanning k up);
+ *   - a cluster with no members keeps its previous centre, count 0;
+ *   - "congruent" means bitwise-identical fp32 centres; the first comparison
+ *     is after the second update (t = 2), so the earliest stop is t = 2;
+ *   - iterations = number of assignment passes executed; the returned labels
+ *     are those of the last pass and the returned centres are the centres of
+ *     gravity of those labels.
+ *
+ * Build: gcc -std=c99 -O2 -ffp-contract=off -fPIC -shared
+ * All pointers are host pointers; arrays are row-major; return 0 or -1.
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <math.h>
+
+#define ORACLE_EINVAL (-1)
+#define ORACLE_ENOMEM (-2)
+
+/* Squared distance of Eq. (2) between object x and centre c, in the
+ * normative operation order described above. */
+static double sqdist(const float *x, const float *c, int32_t M)
+{
+    double d = 0.0;
+    for (int32_t j = 0; j < M; ++j) {
+        double e = (double)x[j] - (double)c[j];
+        double sq = e * e;
+        d = d + sq;
+    }
+    return d;
+}
+
+/*
+ * Assignment, Algorithm 1 steps 2 and 4: labels[i] = argmin_k |x_i - c_k|^2,
+ * lowest k on ties. Optionally reports, per object, the best squared distance
+ * d1[i] and the smallest squared distance to any other centre d2[i]
+ * (+infinity when K == 1); both may be NULL.
+ */
+int oracle_assign(const float *X, int64_t n, int32_t M, const float *C, int32_t K,
+                  int32_t *labels, double *d1, double *d2)
+{
+    if (!X || !C || !labels || n < 0 || M < 1 || K < 1)
+        return ORACLE_EINVAL;
+    for (int64_t i = 0; i < n; ++i) {
+        const float *x = X + i * (int64_t)M;
+        double best = INFINITY, second = INFINITY;
+        int32_t lab = 0;
+        for (int32_t k = 0; k < K; ++k) {
+            double d = sqdist(x, C + (int64_t)k * M, M);
+            if (d < best) {
+                second = best;
+                best = d;
+                lab = k;
+            } else if (d < second) {
+                second = d;
+            }
+        }
+        labels[i] = lab;
+        if (d1) d1[i] = best;
+        if (d2) d2[i] = second;
+    }
+    return 0;
+}
+
+/*
+ * Centres of gravity, Eq. (1) (Algorithm 1 steps 3 and 5):
+ *   counts[k]  = n_k = number of objects with label k,
+ *   centers[k] = fp32( (sum over those objects of x, in fp64, i ascending) / n_k )
+ * and a cluster with n_k = 0 keeps prev[k]. centers may alias prev.
+ * Labels outside [0, K) are an error.
+ */
+int oracle_update(const float *X, int64_t n, int32_t M, const int32_t *labels,
+                  int32_t K, const float *prev, float *centers, int32_t *counts)
+{
+    if (!X || !labels || !prev || !centers || !counts || n < 0 || M < 1 || K < 1)
+        return ORACLE_EINVAL;
+    double *S = (double *)calloc((size_t)K * (size_t)M, sizeof(double));
+    int64_t *cnt = (int64_t *)calloc((size_t)K, sizeof(int64_t));
+    if (!S || !cnt) {
+        free(S);
+        free(cnt);
+        return ORACLE_ENOMEM;
+    }
+    for (int64_t i = 0; i < n; ++i) {
+        int32_t l = labels[i];
+        if (l < 0 || l >= K) {
+            free(S);
+            free(cnt);
+            return ORACLE_EINVAL;
+        }
+        const float *x = X + i * (int64_t)M;
+        double *s = S + (int64_t)l * M;
+        for (int32_t j = 0; j < M; ++j)
+            s[j] = s[j] + (double)x[j];
+        cnt[l] += 1;
+    }
+    for (int32_t k = 0; k < K; ++k) {
+        for (int32_t j = 0; j < M; ++j) {
+            int64_t o = (int64_t)k * M + j;
+            if (cnt[k] > 0)
+                centers[o] = (float)(S[o] / (double)cnt[k]);
+            else
+                centers[o] = prev[o];
+        }
+        counts[k] = (int32_t)cnt[k];
+    }
+    free(S);
+    free(cnt);
+    return 0;
+}
+
+/* Steps 6-7: are two sets of K*M fp32 centres congruent (bitwise equal)? */
+static int congruent(const float *a, const float *b, int64_t count)
+{
+    return memcmp(a, b, (size_t)count * sizeof(float)) == 0;
+}
+
+/*
+ * The whole loop, Algorithm 1 steps 2-7 from the given initial centres:
+ *   for t = 1 .. max_iter:
+ *     labels_t = assign(C_{t-1});  C_t = update(labels_t, C_{t-1});
+ *     if !fixed and t >= 2 and C_t congruent to C_{t-1}: stop.
+ * Outputs the last labels, the last centres, their counts, and the number of
+ * assignment passes executed. d1/d2 (nullable) receive the final pass's best
+ * and second-best squared distances per object.
+ */
+int oracle_run(const float *X, int64_t n, int32_t M, int32_t K, const float *init,
+               int32_t max_iter, int32_t fixed, int32_t *labels, float *centers,
+               int32_t *counts, int32_t *iterations, double *d1, double *d2)
+{
+    if (!X || !init || !labels || !centers || !counts || !iterations || n < 0 ||
+        M < 1 || K < 1 || max_iter < 1)
+        return ORACLE_EINVAL;
+    int64_t km = (int64_t)K * M;
+    float *prev = (float *)malloc((size_t)km * sizeof(float));
+    float *cur = (float *)malloc((size_t)km * sizeof(float));
+    if (!prev || !cur) {
+        free(prev);
+        free(cur);
+        return ORACLE_ENOMEM;
+    }
+    memcpy(prev, init, (size_t)km * sizeof(float));
+    int32_t t = 0;
+    int rc = 0;
+    for (t = 1; t <= max_iter; ++t) {
+        rc = oracle_assign(X, n, M, prev, K, labels, d1, d2);
+        if (rc) break;
+        rc = oracle_update(X, n, M, labels, K, prev, cur, counts);
+        if (rc) break;
+        int stop = !fixed && t >= 2 && congruent(cur, prev, km);
+        memcpy(prev, cur, (size_t)km * sizeof(float));
+        if (stop) break;
+    }
+    if (t > max_iter) t = max_iter;
+    if (!rc) {
+        memcpy(centers, prev, (size_t)km * sizeof(float));
+        *iterations = t;
+    }
+    free(prev);
+    free(cur);
+    return rc;
+}
+
+/* Objective sum_i |x_i - c_{label_i}|^2 in fp64 (used by the invariant tests). */
+double oracle_sse(const float *X, int64_t n, int32_t M, const int32_t *labels,
+                  const float *C, int32_t K)
+{
+    double s = 0.0;
+    for (int64_t i = 0; i < n; ++i) {
+        int32_t l = labels[i];
+        if (l < 0 || l >= K) return NAN;
+        s = s + sqdist(X + i * (int64_t)M, C + (int64_t)l * M, M);
+    }
+    return s;
+}

@@ -1,0 +1,62 @@
+"""Plant plausible mistakes in a copy of the oracle source and check that the
+oracle's pins (tests/test_oracle.py) catch every one of them.
+
+Each mutant is a textual edit of oracle/kmeans_oracle.c compiled into a
+temporary library; the pin suite then runs against it in a subprocess (through
+KMEANS_ORACLE_LIB) and must fail. Everything here runs on the CPU.
+"""
+import os
+import subprocess
+import sys
+
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+MUTANTS = {
+    "drop_last_feature": ("for (int32_t j = 0; j < M; ++j) {\n        double e",
+                          "for (int32_t j = 0; j < M - 1; ++j) {\n        double e"),
+    "drop_first_feature": ("for (int32_t j = 0; j < M; ++j) {\n        double e",
+                           "for (int32_t j = 1; j < M; ++j) {\n        double e"),
+    "wrong_sign": ("double e = (double)x[j] - (double)c[j];",
+                   "double e = (double)x[j] + (double)c[j];"),
+    "ties_to_highest_index": ("if (d < best) {", "if (d <= best) {"),
+    "wrong_centre_stride": ("sqdist(x, C + (int64_t)k * M, M)",
+                            "sqdist(x, C + (int64_t)k * (M > 1 ? M - 1 : 1), M)"),
+    "transposed_object_index": ("const float *x = X + i * (int64_t)M;\n        double best",
+                                "const float *x = X + (i % M) * (int64_t)M;\n        double best"),
+    "empty_cluster_to_zero": ("centers[o] = prev[o];", "centers[o] = 0.0f;"),
+    "sum_not_mean": ("centers[o] = (float)(S[o] / (double)cnt[k]);",
+                     "centers[o] = (float)(S[o] / (double)(cnt[k] + 1));"),
+    "skip_first_object_in_sum": ("int32_t l = labels[i];\n        if (l < 0 || l >= K) {",
+                                 "int32_t l = labels[i];\n        if (i == 0) continue;\n        if (l < 0 || l >= K) {"),
+    "compare_from_first_iteration": ("t >= 2 && congruent", "t >= 1 && congruent"),
+    "never_stop": ("if (stop) break;", "if (0 && stop) break;"),
+    "fp32_difference": ("double e = (double)x[j] - (double)c[j];\n        double sq = e * e;",
+                        "float e = x[j] - c[j];\n        double sq = e * e;"),
+    "count_off_by_one": ("cnt[l] += 1;", "cnt[l] += (i > 0);"),
+}
+
+
+@pytest.fixture(scope="module")
+def source():
+    with open(oracle.SRC) as f:
+        return f.read()
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_planted_mistake(name, source, tmp_path):
+    old, new = MUTANTS[name]
+    assert source.count(old) == 1, f"mutant {name} does not apply"
+    src = tmp_path / "mutant.c"
+    src.write_text(source.replace(old, new))
+    lib = tmp_path / "libmutant.so"
+    subprocess.check_call(["gcc", *oracle.CFLAGS, "-o", str(lib), str(src), "-lm"])
+    env = dict(os.environ, KMEANS_ORACLE_LIB=str(lib))
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        os.path.join(ROOT, "tests", "test_oracle.py")],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    assert r.returncode != 0, f"mutant {name} survived the oracle pins:\n{r.stdout[-2000:]}"
