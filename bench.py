@@ -1,0 +1,218 @@
+"""Benchmark: Lloyd iterations per second on one MI355X.
+
+A step is one Lloyd iteration of Algorithm 1 over the whole point set: the
+fused assign+accumulate launch (steps 2/4 and the sums of Eq. (1)) and the
+finalise launch (centres of Eq. (1), congruence test of steps 6/7). The default
+workload is the paper's largest size: n = 2,000,000 objects, M = 25 features,
+K = 16 clusters (anisotropic Gaussian blobs, seed 2, farthest-point initial
+centres). Iterations run in fixed-count mode so every timed step does the full
+work (this workload converges after 2 passes; the passes after that repeat the
+same labels and centres).
+
+python bench.py [--gpus 1] [--steps 1000] [--warmup 20] [--workload 3]
+                [--no-cpu-baseline] [--no-control] [--path direct|mfma]
+python bench.py --calibrate-copy   # plain device copy of known size (PMC scaling)
+
+Prints ONE JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, vendor peak
+PROFILES = os.path.join(ROOT, "profiles")
+KERNEL_SOURCES = {
+    "direct": os.path.join(ROOT, "paper_1402_3788_amd", "csrc", "lloyd_valu.hip"),
+}
+
+
+def _parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1000)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="3")
+    ap.add_argument("--path", default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-control", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true")
+    return ap.parse_args()
+
+
+def _sha(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def _traffic(kernel_key: str, workload: str, n_launch_bytes: float):
+    """HBM traffic per launch from the committed PMC summary, if it was taken on
+    the current kernel source; else None."""
+    path = os.path.join(PROFILES, f"pmc_{kernel_key}_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    m = re.search(r"```json\n(.*?)\n```", open(path).read(), re.S)
+    if not m:
+        return None
+    d = json.loads(m.group(1))
+    if d.get("kernel_src_sha256") != _sha(KERNEL_SOURCES[kernel_key]):
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+def calibrate_copy():
+    import torch
+    n = 1 << 28                                   # 2^28 fp32 = 1 GiB
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(10):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n, "launches": 10}))
+
+
+def copy_bandwidth(torch, nbytes=1 << 30, reps=20):
+    n = nbytes // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    s.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e.record()
+    torch.cuda.synchronize()
+    sec = s.elapsed_time(e) / 1e3 / reps
+    del src, dst
+    return 2 * nbytes / sec / 1e9
+
+
+def main():
+    args = _parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (got --gpus {args.gpus}); "
+              "the multi-GPU sharding of the Lloyd iteration is described in DESIGN.md "
+              "but not built", file=sys.stderr)
+        sys.exit(2)
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
+
+    import numpy as np
+    import torch
+
+    import paper_1402_3788_amd as km
+    import workloads
+
+    w = workloads.get(args.workload)
+    X, _, _, init = workloads.load(args.workload)
+    dev = torch.device("cuda:0")
+    Xg = torch.from_numpy(X).to(dev)
+    Cg = torch.from_numpy(init).to(dev)
+    n, M, K = w.n, w.M, w.K
+    out = (torch.empty(n, dtype=torch.int32, device=dev),
+           torch.empty((K, M), dtype=torch.float32, device=dev),
+           torch.empty(K, dtype=torch.int32, device=dev))
+    ws = km.workspace(n, M, K, dev)
+
+    # warmup
+    km.kmeans_run(Xg, K, Cg, max(1, args.warmup), fixed_iters=True, path=args.path, out=out, ws=ws)
+    torch.cuda.synchronize()
+
+    # timed region: exactly `steps` Lloyd iterations in one fixed-count run
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    _, _, _, iters, tm = km.kmeans_run(Xg, K, Cg, args.steps, fixed_iters=True, path=args.path,
+                                       timing=True, out=out, ws=ws)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    assert iters == args.steps
+    sec = t1 - t0
+    iters_per_s = args.steps / sec
+    bytes_per_point = 4 * M + 4                    # read the object once, write its label
+    launch_bytes = n * bytes_per_point
+    assign_avg_s = tm.assign_ms / 1e3 / tm.assign_launches
+    finalize_avg_s = tm.finalize_ms / 1e3 / tm.finalize_launches
+    achieved = launch_bytes / assign_avg_s / 1e9
+    kernel_key = "direct"
+    traffic = _traffic(kernel_key, w.name, launch_bytes)
+
+    result = {
+        "metric": "Lloyd iters/sec at n=2e6,M=25,K=16 (also points*iters/sec, % of HBM peak)",
+        "value": round(iters_per_s, 2),
+        "unit": "iters/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(sec * 1e3 / args.steps, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "n": n, "M": M, "K": K, "mode": "fixed iterations",
+                   "accumulation": "f64", "path": args.path or "auto"},
+        "points_iters_per_s": round(iters_per_s * n, 1),
+        "algorithmic_GBps_whole_step": round(launch_bytes * iters_per_s / 1e9, 1),
+        "pct_hbm_peak_whole_step": round(100 * launch_bytes * iters_per_s / 1e9 / HBM_PEAK_GBPS, 2),
+        "kernel_avg_us": {"assign_accumulate": round(assign_avg_s * 1e6, 3),
+                          "finalize": round(finalize_avg_s * 1e6, 3)},
+        "roofline": {
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": traffic,
+            "kernel": "lloyd_valu_kernel<25, assign+accumulate>",
+            "bytes_per_launch": launch_bytes,
+        },
+    }
+
+    if not args.no_control:
+        # same kernel on a point set larger than the 256 MB Infinity Cache
+        rng = np.random.default_rng(123)
+        nc = 8_000_000
+        Xc = torch.from_numpy(rng.uniform(-50, 50, (nc, M)).astype(np.float32)).to(dev)
+        Cc = Xc[:K].clone()
+        km.kmeans_run(Xc, K, Cc, 5, fixed_iters=True, path=args.path)
+        _, _, _, _, tmc = km.kmeans_run(Xc, K, Cc, 50, fixed_iters=True, path=args.path,
+                                        timing=True)
+        avg = tmc.assign_ms / 1e3 / tmc.assign_launches
+        result["control_n8m_uniform"] = {
+            "assign_accumulate_avg_us": round(avg * 1e6, 2),
+            "achieved_GBps": round(nc * bytes_per_point / avg / 1e9, 1),
+        }
+        del Xc
+        result["copy_GBps_torch_1GiB"] = round(copy_bandwidth(torch), 1)
+
+    if not args.no_cpu_baseline:
+        import oracle
+        t = time.perf_counter()
+        oracle.run(X, K, init, 1, fixed=True)
+        one = time.perf_counter() - t
+        T = int(max(1, min(20, 15.0 // max(one, 1e-3))))
+        t = time.perf_counter()
+        oracle.run(X, K, init, T, fixed=True)
+        cpu_s = time.perf_counter() - t
+        result["cpu_baseline"] = {
+            "value": round(T / cpu_s, 4),
+            "unit": "iters/s",
+            "cores": 1,
+            "kind": "oracle",
+            "sample": f"{T} fixed Lloyd iterations over all {n} objects (single-threaded C, fp64)",
+        }
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,119 @@
+/*
+ * kmeans.h -- C ABI of the MI355X (gfx950) Lloyd-iteration library.
+ *
+ * The library runs the data-parallel part of K-means as described in
+ * Algorithm 1 of Litvinenko, "Using of GPUs for cluster analysis of large data
+ * by K-means method": assign every object to the nearest centre (steps 2 and
+ * 4, Euclidean distance of Eq. (2)), recompute each cluster's centre of gravity
+ * (steps 3 and 5, Eq. (1)), and stop when the centres of the last two
+ * iterations are congruent (steps 6 and 7).
+ *
+ * Conventions shared by every entry point
+ *   - Array arguments are DEVICE pointers (hipMalloc'd or equivalent), owned by
+ *     the caller; the library never allocates, frees or retains device memory
+ *     beyond a call. Row-major layouts: X is [n][M] fp32 (object-major, each
+ *     object's M features contiguous), centres are [K][M] fp32.
+ *   - X must be 16-byte aligned (every hipMalloc'd buffer is).
+ *   - `stream` is a hipStream_t (NULL = the default stream). Work is enqueued on
+ *     it; kmeans_assign and kmeans_update return without waiting, kmeans_run
+ *     waits for its own work before returning.
+ *   - The return value is KMEANS_OK (0) or a negative KMEANS_E* code. Arguments
+ *     are validated on the host before anything is enqueued: on a validation
+ *     error nothing is enqueued and no output is touched. kmeans_strerror()
+ *     names a code. No C++ exception crosses this interface.
+ *   - Envelope: 1 <= n <= 2^31-1, 1 <= M <= 64, 1 <= K <= 1024, K*M <= 16384.
+ *     Shapes outside it return KMEANS_EUNSUPPORTED.
+ *   - Results are deterministic: the same inputs on the same device give
+ *     bitwise-identical labels, centres, counts and iteration counts (sums are
+ *     formed in fp64 in a fixed order; no floating-point atomics).
+ *   - Arithmetic (the readings taken where the paper is silent): distances are
+ *     compared squared; ties go to the lowest centre index; centres are the
+ *     fp64 mean of the members rounded once to fp32; a cluster with no members
+ *     keeps its previous centre and has count 0. A label is the exact-arithmetic
+ *     argmin: points whose fp32 distances are too close to call are re-decided
+ *     with fp64 distances. Inputs containing NaN or Inf give unspecified labels.
+ */
+#ifndef KMEANS_MI355X_H
+#define KMEANS_MI355X_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define KMEANS_OK             0
+#define KMEANS_EINVAL        -1   /* NULL pointer, non-positive size, misaligned X, bad flags */
+#define KMEANS_EUNSUPPORTED  -2   /* shape outside the envelope above                        */
+#define KMEANS_EWORKSPACE    -3   /* workspace missing or smaller than kmeans_workspace_bytes */
+#define KMEANS_EHIP          -4   /* a HIP runtime call or kernel launch failed              */
+
+/* Flags (bitwise OR). */
+#define KMEANS_FIXED_ITERS  (1u << 0) /* kmeans_run: run exactly max_iter iterations, no early stop */
+#define KMEANS_PATH_DIRECT  (1u << 1) /* force the vector-ALU distance path                          */
+#define KMEANS_PATH_MFMA    (1u << 2) /* force the matrix-core (expanded-form) distance path          */
+
+/* Optional per-call timing, filled by kmeans_run when a non-NULL pointer is
+ * passed: device time of the fused assign/accumulate launches and of the
+ * finalise launches, measured with HIP events recorded on `stream` around every
+ * launch. Timing adds one event record per launch. */
+typedef struct kmeans_timing {
+    double  assign_ms;        /* summed duration of the assign/accumulate launches */
+    double  finalize_ms;      /* summed duration of the finalise/compare launches  */
+    int32_t assign_launches;
+    int32_t finalize_launches;
+} kmeans_timing_t;
+
+/* Bytes of device workspace that kmeans_update and kmeans_run need for a problem
+ * of this shape (per-workgroup fp64 partial sums and counts plus a small
+ * control block). kmeans_assign needs none. Returns 0 for shapes outside the
+ * envelope. Pure host computation. */
+size_t kmeans_workspace_bytes(int64_t n, int32_t M, int32_t K, uint32_t flags);
+
+/* Human-readable name of a status code (static storage). */
+const char *kmeans_strerror(int status);
+
+/*
+ * Assignment, Algorithm 1 steps 2 and 4, distance of Eq. (2):
+ *   labels[i] = argmin_k |X_i - centers_k|^2  (lowest k on ties), int32 [n].
+ * min_d2 (may be NULL) receives fp32 [n] squared distances to the chosen centre.
+ * flags: KMEANS_PATH_* only. Asynchronous on `stream`.
+ */
+int kmeans_assign(const float *X, int64_t n, int32_t M, const float *centers, int32_t K,
+                  int32_t *labels, float *min_d2, uint32_t flags, void *stream);
+
+/*
+ * Centres of gravity, Eq. (1) (Algorithm 1 steps 3 and 5):
+ *   counts[k]  = number of objects with labels[i] == k                 (int32 [K]),
+ *   centers[k] = fp32(fp64 mean of those objects), or prev_centers[k] when the
+ *                cluster has no member                                 (fp32 [K][M]).
+ * labels must lie in [0, K); objects with other labels are not counted.
+ * centers may alias prev_centers. Asynchronous on `stream`.
+ */
+int kmeans_update(const float *X, int64_t n, int32_t M, const int32_t *labels, int32_t K,
+                  const float *prev_centers, float *centers, int32_t *counts,
+                  void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * The Lloyd loop, Algorithm 1 steps 2-7, from the given initial centres:
+ *   for t = 1..max_iter: labels_t = assign(C_{t-1}); C_t = update(labels_t);
+ *                        stop when t >= 2 and C_t is bitwise equal to C_{t-1}
+ *                        (unless KMEANS_FIXED_ITERS).
+ * Outputs: labels of the last assignment pass (int32 [n]), the centres of
+ * gravity of those labels (fp32 [K][M]), their counts (int32 [K]), and in
+ * *iterations (a HOST int32) the number of assignment passes executed.
+ * init_centers may alias centers. Synchronous: returns once the work is done.
+ * timing may be NULL.
+ */
+int kmeans_run(const float *X, int64_t n, int32_t M, int32_t K, const float *init_centers,
+               int32_t max_iter, uint32_t flags, int32_t *labels, float *centers,
+               int32_t *counts, int32_t *iterations, void *workspace,
+               size_t workspace_bytes, void *stream, kmeans_timing_t *timing);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KMEANS_MI355X_H */

@@ -1,0 +1,183 @@
+"""MI355X (gfx950) Lloyd-iteration library: Python binding.
+
+Thin ctypes marshalling over libkmeans_mi355x.so (C ABI in include/kmeans.h).
+Tensors are PyTorch device tensors; every step of the computation runs in the
+library's HIP kernels. Importing this module fails loudly if the library has
+not been built (python -m paper_1402_3788_amd.build).
+
+Entry points (same names as the C ABI):
+    kmeans_assign(X, centers, with_min_d2=False, path=None) -> labels [, min_d2]
+    kmeans_update(X, labels, K, prev_centers, out=None) -> (centers, counts)
+    kmeans_run(X, K, init_centers, max_iter, fixed_iters=False, path=None,
+               timing=False) -> (labels, centers, counts, iterations[, timing])
+    kmeans_workspace_bytes(n, M, K, flags=0), kmeans_strerror(code)
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch  # loads the HIP runtime this library binds to
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libkmeans_mi355x.so")
+
+KMEANS_OK = 0
+KMEANS_EINVAL = -1
+KMEANS_EUNSUPPORTED = -2
+KMEANS_EWORKSPACE = -3
+KMEANS_EHIP = -4
+
+KMEANS_FIXED_ITERS = 1 << 0
+KMEANS_PATH_DIRECT = 1 << 1
+KMEANS_PATH_MFMA = 1 << 2
+
+EXPORTED = ("kmeans_workspace_bytes", "kmeans_strerror", "kmeans_assign", "kmeans_update",
+            "kmeans_run")
+
+
+class KmeansTiming(ctypes.Structure):
+    _fields_ = [("assign_ms", ctypes.c_double), ("finalize_ms", ctypes.c_double),
+                ("assign_launches", ctypes.c_int32), ("finalize_launches", ctypes.c_int32)]
+
+
+class KmeansError(RuntimeError):
+    def __init__(self, fn: str, code: int):
+        super().__init__(f"{fn}: {strerror(code)} ({code})")
+        self.code = code
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_1402_3788_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    p, i64, i32, u32, sz = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32,
+                            ctypes.c_size_t)
+    lib.kmeans_workspace_bytes.argtypes = [i64, i32, i32, u32]
+    lib.kmeans_workspace_bytes.restype = sz
+    lib.kmeans_strerror.argtypes = [ctypes.c_int]
+    lib.kmeans_strerror.restype = ctypes.c_char_p
+    lib.kmeans_assign.argtypes = [p, i64, i32, p, i32, p, p, u32, p]
+    lib.kmeans_assign.restype = ctypes.c_int
+    lib.kmeans_update.argtypes = [p, i64, i32, p, i32, p, p, p, p, sz, p]
+    lib.kmeans_update.restype = ctypes.c_int
+    lib.kmeans_run.argtypes = [p, i64, i32, i32, p, i32, u32, p, p, p, p, p, sz, p,
+                               ctypes.POINTER(KmeansTiming)]
+    lib.kmeans_run.restype = ctypes.c_int
+    return lib
+
+
+_lib = _load()
+
+
+def strerror(code: int) -> str:
+    return _lib.kmeans_strerror(int(code)).decode()
+
+
+kmeans_strerror = strerror
+
+
+def kmeans_workspace_bytes(n: int, M: int, K: int, flags: int = 0) -> int:
+    return int(_lib.kmeans_workspace_bytes(int(n), int(M), int(K), int(flags)))
+
+
+def _stream_ptr(device) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _check_x(X: torch.Tensor):
+    if not (isinstance(X, torch.Tensor) and X.is_cuda and X.dtype == torch.float32
+            and X.dim() == 2 and X.is_contiguous()):
+        raise ValueError("X must be a contiguous float32 [n, M] tensor on a GPU")
+
+
+def _dev_ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def _flags(path):
+    if path is None or path == "auto":
+        return 0
+    if path == "direct":
+        return KMEANS_PATH_DIRECT
+    if path == "mfma":
+        return KMEANS_PATH_MFMA
+    raise ValueError(f"unknown path {path!r}")
+
+
+def workspace(n: int, M: int, K: int, device, flags: int = 0) -> torch.Tensor:
+    nbytes = kmeans_workspace_bytes(n, M, K, flags)
+    if nbytes == 0:
+        raise KmeansError("kmeans_workspace_bytes", KMEANS_EUNSUPPORTED)
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+def kmeans_assign(X: torch.Tensor, centers: torch.Tensor, with_min_d2: bool = False, path=None):
+    """Algorithm 1 steps 2/4: labels[i] = nearest centre (lowest index on ties)."""
+    _check_x(X)
+    n, M = X.shape
+    C = centers.contiguous()
+    K = C.shape[0]
+    labels = torch.empty(n, dtype=torch.int32, device=X.device)
+    d2 = torch.empty(n, dtype=torch.float32, device=X.device) if with_min_d2 else None
+    rc = _lib.kmeans_assign(_dev_ptr(X), n, M, _dev_ptr(C), K, _dev_ptr(labels), _dev_ptr(d2),
+                            _flags(path), _stream_ptr(X.device))
+    if rc:
+        raise KmeansError("kmeans_assign", rc)
+    return (labels, d2) if with_min_d2 else labels
+
+
+def kmeans_update(X: torch.Tensor, labels: torch.Tensor, K: int, prev_centers: torch.Tensor,
+                  out: torch.Tensor | None = None, ws: torch.Tensor | None = None):
+    """Eq. (1): centres of gravity of the labelled objects (empty keeps prev)."""
+    _check_x(X)
+    n, M = X.shape
+    prev = prev_centers.contiguous()
+    centers = out if out is not None else torch.empty((K, M), dtype=torch.float32, device=X.device)
+    counts = torch.empty(K, dtype=torch.int32, device=X.device)
+    if ws is None:
+        ws = workspace(n, M, K, X.device)
+    rc = _lib.kmeans_update(_dev_ptr(X), n, M, _dev_ptr(labels.contiguous()), int(K),
+                            _dev_ptr(prev), _dev_ptr(centers), _dev_ptr(counts), _dev_ptr(ws),
+                            ws.numel(), _stream_ptr(X.device))
+    if rc:
+        raise KmeansError("kmeans_update", rc)
+    return centers, counts
+
+
+def kmeans_run(X: torch.Tensor, K: int, init_centers: torch.Tensor, max_iter: int,
+               fixed_iters: bool = False, path=None, timing: bool = False,
+               out=None, ws: torch.Tensor | None = None):
+    """Algorithm 1 steps 2-7 from init_centers (synchronous).
+
+    Returns (labels, centers, counts, iterations), plus a KmeansTiming when
+    timing=True. `out` may supply (labels, centers, counts) tensors to reuse.
+    """
+    _check_x(X)
+    n, M = X.shape
+    init = init_centers.contiguous()
+    if out is None:
+        labels = torch.empty(n, dtype=torch.int32, device=X.device)
+        centers = torch.empty((K, M), dtype=torch.float32, device=X.device)
+        counts = torch.empty(K, dtype=torch.int32, device=X.device)
+    else:
+        labels, centers, counts = out
+    flags = _flags(path) | (KMEANS_FIXED_ITERS if fixed_iters else 0)
+    if ws is None:
+        ws = workspace(n, M, K, X.device, flags)
+    iters = ctypes.c_int32(0)
+    tm = KmeansTiming() if timing else None
+    rc = _lib.kmeans_run(_dev_ptr(X), n, M, int(K), _dev_ptr(init), int(max_iter), flags,
+                         _dev_ptr(labels), _dev_ptr(centers), _dev_ptr(counts),
+                         ctypes.byref(iters), _dev_ptr(ws), ws.numel(), _stream_ptr(X.device),
+                         ctypes.byref(tm) if tm is not None else None)
+    if rc:
+        raise KmeansError("kmeans_run", rc)
+    res = (labels, centers, counts, int(iters.value))
+    return res + (tm,) if timing else res
+
+
+def ctl_fallbacks(ws: torch.Tensor) -> int:
+    """Objects re-decided in fp64 during the last kmeans_run that used `ws`
+    (read from the control block at the start of the workspace)."""
+    return int(ws[12:16].view(torch.int32).item())

@@ -1,0 +1,223 @@
+// C ABI of the Lloyd-iteration library: argument validation, workspace layout,
+// and the iteration control of Algorithm 1 (steps 2-7). See include/kmeans.h.
+#include "../../include/kmeans.h"
+#include "lloyd.h"
+
+#include <vector>
+
+using namespace lloyd;
+
+namespace {
+
+constexpr uint32_t kKnownFlags = KMEANS_FIXED_ITERS | KMEANS_PATH_DIRECT | KMEANS_PATH_MFMA;
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+int check_shape(int64_t n, int32_t M, int32_t K)
+{
+    if (n < 1 || M < 1 || K < 1) return KMEANS_EINVAL;
+    if (n > INT32_MAX) return KMEANS_EUNSUPPORTED;
+    if (M > kMaxM || K > kMaxK || (int64_t)K * M > kMaxKM) return KMEANS_EUNSUPPORTED;
+    return KMEANS_OK;
+}
+
+int check_flags(uint32_t flags)
+{
+    if (flags & ~kKnownFlags) return KMEANS_EINVAL;
+    if ((flags & KMEANS_PATH_DIRECT) && (flags & KMEANS_PATH_MFMA)) return KMEANS_EINVAL;
+    if (flags & KMEANS_PATH_MFMA) return KMEANS_EUNSUPPORTED;   // no matrix-core path yet
+    return KMEANS_OK;
+}
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Workspace: [Ctl (256 B)] [fp64 partial sums: G*K*M] [int32 partial counts: G*K]
+struct Layout {
+    AccumPlan plan;
+    size_t sums_off, counts_off, total;
+};
+
+Layout layout(int64_t n, int32_t M, int32_t K)
+{
+    Layout L{};
+    L.plan = plan_valu(n, M, K, kAssignAccum);
+    L.sums_off = align_up(sizeof(Ctl), 256);
+    L.counts_off = align_up(L.sums_off + (size_t)L.plan.groups * K * M * sizeof(double), 256);
+    L.total = align_up(L.counts_off + (size_t)L.plan.groups * K * sizeof(int32_t), 256);
+    return L;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? KMEANS_OK : KMEANS_EHIP; }
+
+hipError_t allow_lds(const AccumPlan &)
+{
+    // gfx950 serves up to 160 KB of LDS per workgroup without an opt-in; nothing
+    // to configure, kept as the single place to add one.
+    return hipSuccess;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *kmeans_strerror(int status)
+{
+    switch (status) {
+    case KMEANS_OK: return "ok";
+    case KMEANS_EINVAL: return "invalid argument";
+    case KMEANS_EUNSUPPORTED: return "shape or option outside the supported envelope";
+    case KMEANS_EWORKSPACE: return "workspace missing or too small";
+    case KMEANS_EHIP: return "HIP runtime or kernel launch failure";
+    default: return "unknown status";
+    }
+}
+
+size_t kmeans_workspace_bytes(int64_t n, int32_t M, int32_t K, uint32_t flags)
+{
+    if (check_shape(n, M, K) != KMEANS_OK || (flags & ~kKnownFlags)) return 0;
+    return layout(n, M, K).total;
+}
+
+int kmeans_assign(const float *X, int64_t n, int32_t M, const float *centers, int32_t K,
+                  int32_t *labels, float *min_d2, uint32_t flags, void *stream)
+{
+    if (!X || !centers || !labels) return KMEANS_EINVAL;
+    int rc = check_shape(n, M, K);
+    if (rc) return rc;
+    if ((rc = check_flags(flags & ~KMEANS_FIXED_ITERS))) return rc;
+    if (!aligned16(X)) return KMEANS_EINVAL;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const AccumPlan plan = plan_valu(n, M, K, kAssign);
+    StepArgs a{};
+    a.X = X; a.n = n; a.M = M; a.C = centers; a.K = K;
+    a.labels = labels; a.min_d2 = min_d2;
+    return hip_status(launch_valu(a, kAssign, plan, s));
+}
+
+int kmeans_update(const float *X, int64_t n, int32_t M, const int32_t *labels, int32_t K,
+                  const float *prev_centers, float *centers, int32_t *counts, void *workspace,
+                  size_t workspace_bytes, void *stream)
+{
+    if (!X || !labels || !prev_centers || !centers || !counts) return KMEANS_EINVAL;
+    int rc = check_shape(n, M, K);
+    if (rc) return rc;
+    if (!aligned16(X)) return KMEANS_EINVAL;
+    const Layout L = layout(n, M, K);
+    if (!workspace || workspace_bytes < L.total) return KMEANS_EWORKSPACE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    char *ws = static_cast<char *>(workspace);
+    StepArgs a{};
+    a.X = X; a.n = n; a.M = M; a.C = prev_centers; a.K = K;
+    a.labels_in = labels;
+    a.part_sums = reinterpret_cast<double *>(ws + L.sums_off);
+    a.part_counts = reinterpret_cast<int32_t *>(ws + L.counts_off);
+    AccumPlan plan = plan_valu(n, M, K, kAccumLabels);
+    if ((rc = hip_status(allow_lds(plan)))) return rc;
+    if ((rc = hip_status(launch_valu(a, kAccumLabels, plan, s)))) return rc;
+    return hip_status(launch_finalize(a.part_sums, a.part_counts, plan.groups, K, M, prev_centers,
+                                      centers, counts, nullptr, 0, 1, 0, s));
+}
+
+int kmeans_run(const float *X, int64_t n, int32_t M, int32_t K, const float *init_centers,
+               int32_t max_iter, uint32_t flags, int32_t *labels, float *centers, int32_t *counts,
+               int32_t *iterations, void *workspace, size_t workspace_bytes, void *stream,
+               kmeans_timing_t *timing)
+{
+    if (!X || !init_centers || !labels || !centers || !counts || !iterations) return KMEANS_EINVAL;
+    int rc = check_shape(n, M, K);
+    if (rc) return rc;
+    if (max_iter < 1) return KMEANS_EINVAL;
+    if ((rc = check_flags(flags))) return rc;
+    if (!aligned16(X)) return KMEANS_EINVAL;
+    const Layout L = layout(n, M, K);
+    if (!workspace || workspace_bytes < L.total) return KMEANS_EWORKSPACE;
+
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    char *ws = static_cast<char *>(workspace);
+    Ctl *ctl = reinterpret_cast<Ctl *>(ws);
+    const int fixed = (flags & KMEANS_FIXED_ITERS) ? 1 : 0;
+
+    StepArgs a{};
+    a.X = X; a.n = n; a.M = M; a.C = centers; a.K = K;
+    a.labels = labels;
+    a.part_sums = reinterpret_cast<double *>(ws + L.sums_off);
+    a.part_counts = reinterpret_cast<int32_t *>(ws + L.counts_off);
+    a.ctl = ctl;
+    a.fixed = fixed;
+
+    if ((rc = hip_status(allow_lds(L.plan)))) return rc;
+    if ((rc = hip_status(launch_ctl_reset(ctl, s)))) return rc;
+    if (init_centers != centers) {
+        rc = hip_status(hipMemcpyAsync(centers, init_centers, sizeof(float) * (size_t)K * M,
+                                       hipMemcpyDeviceToDevice, s));
+        if (rc) return rc;
+    }
+
+    std::vector<hipEvent_t> ev;
+    auto mark = [&]() -> int {
+        if (!timing) return KMEANS_OK;
+        hipEvent_t e;
+        if (hipEventCreate(&e) != hipSuccess) return KMEANS_EHIP;
+        ev.push_back(e);
+        return hip_status(hipEventRecord(e, s));
+    };
+    auto cleanup = [&]() {
+        for (hipEvent_t e : ev) (void)hipEventDestroy(e);
+    };
+
+    // Enqueue iterations in chunks; between chunks (early-stop mode only) read
+    // the control block to learn whether the centres have become congruent.
+    // Launches past convergence return at their first instruction.
+    int t = 1, chunk = 3;
+    Ctl host{};
+    rc = mark();
+    while (!rc && t <= max_iter) {
+        // fixed-count runs enqueue everything at once; otherwise chunks grow 3, 6, 12, ...
+        const int end = (fixed || t + chunk - 1 >= max_iter) ? max_iter : t + chunk - 1;
+        for (int tt = t; tt <= end && !rc; ++tt) {
+            a.t = tt;
+            rc = hip_status(launch_valu(a, kAssignAccum, L.plan, s));
+            if (!rc) rc = mark();
+            if (!rc)
+                rc = hip_status(launch_finalize(a.part_sums, a.part_counts, L.plan.groups, K, M,
+                                                centers, centers, counts, ctl, tt, fixed, 1, s));
+            if (!rc) rc = mark();
+        }
+        t = end + 1;
+        if (rc || t > max_iter) break;
+        rc = hip_status(hipMemcpyAsync(&host, ctl, sizeof(Ctl), hipMemcpyDeviceToHost, s));
+        if (!rc) rc = hip_status(hipStreamSynchronize(s));
+        if (rc || host.converged_at != 0) break;
+        chunk = chunk * 2 < 64 ? chunk * 2 : 64;
+    }
+    if (!rc) rc = hip_status(hipMemcpyAsync(&host, ctl, sizeof(Ctl), hipMemcpyDeviceToHost, s));
+    if (!rc) rc = hip_status(hipStreamSynchronize(s));
+    if (rc) {
+        cleanup();
+        return rc;
+    }
+    *iterations = host.converged_at != 0 ? host.converged_at : max_iter;
+
+    if (timing) {
+        timing->assign_ms = timing->finalize_ms = 0.0;
+        timing->assign_launches = timing->finalize_launches = 0;
+        for (size_t e = 0; e + 1 < ev.size(); ++e) {
+            float ms = 0.f;
+            if (hipEventElapsedTime(&ms, ev[e], ev[e + 1]) != hipSuccess) {
+                rc = KMEANS_EHIP;
+                break;
+            }
+            if (e % 2 == 0) {
+                timing->assign_ms += ms;
+                timing->assign_launches++;
+            } else {
+                timing->finalize_ms += ms;
+                timing->finalize_launches++;
+            }
+        }
+    }
+    cleanup();
+    return rc;
+}
+
+}  // extern "C"

@@ -1,0 +1,229 @@
+"""GPU parity: the HIP library (through the C ABI) against the CPU oracle on the
+same seeded inputs and the same initial centres.
+
+Bar (from the parity contract): labels identical for every object whose
+oracle best-vs-second-best squared-distance gap is at least 1e-5 relative;
+centres within 1e-5 of the oracle's, relative to each centre's largest
+coordinate magnitude; counts equal up to the number of exempt label
+mismatches; iteration counts equal. The library re-decides close calls in fp64
+and sums in fp64, so in practice labels and counts are identical everywhere and
+centres agree bit for bit; the tests report both.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_1402_3788_amd as km
+import workloads
+
+pytestmark = pytest.mark.gpu
+
+DEV = torch.device("cuda:0") if torch.cuda.is_available() else None
+GAP_EXEMPT = 1e-5
+CENTER_RTOL = 1e-5
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+def _gpu(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def check_centers(C, oC, rtol=CENTER_RTOL):
+    scale = np.maximum(np.abs(oC).max(axis=1, keepdims=True), 1e-30)
+    err = np.abs(C.astype(np.float64) - oC.astype(np.float64))
+    assert (err <= rtol * scale).all(), f"max centre error {(err / scale).max():.3g} (relative)"
+    return int((C.view(np.uint32) != oC.view(np.uint32)).sum())
+
+
+def check_labels(lab, olab, gap):
+    mism = lab != olab
+    hard = mism & (gap >= GAP_EXEMPT)
+    assert not hard.any(), f"{int(hard.sum())} label mismatches outside the near-tie band"
+    return int(mism.sum())
+
+
+def run_parity(X, init, K, max_iter, fixed=False, path=None, name=""):
+    _say(f"[parity] {name} n={X.shape[0]} M={X.shape[1]} K={K} max_iter={max_iter} "
+         f"fixed={fixed} path={path}")
+    lab, C, cnt, it = km.kmeans_run(_gpu(X), K, _gpu(init), max_iter, fixed_iters=fixed,
+                                    path=path)
+    lab, C, cnt = lab.cpu().numpy(), C.cpu().numpy(), cnt.cpu().numpy()
+    olab, oC, ocnt, oit, d1, d2 = oracle.run(X, K, init, max_iter, fixed=fixed, with_dist=True)
+    gap = oracle.gap_rel(d1, d2)
+    assert it == oit, f"iterations {it} vs oracle {oit}"
+    nmis = check_labels(lab, olab, gap)
+    assert np.abs(cnt.astype(np.int64) - ocnt).sum() <= 2 * nmis
+    nbits = check_centers(C, oC)
+    _say(f"[parity] {name}: iterations {it}, exempt label mismatches {nmis}, "
+         f"centre coordinates not bit-identical {nbits}")
+    return lab, C, cnt, it
+
+
+# ------------------------------------------------------------ small and ragged shapes
+
+SHAPES = [
+    # n, M, K, kind, init
+    (1, 3, 1, "uniform", "farthest"),
+    (63, 2, 4, "blobs", "farthest"),
+    (64, 5, 7, "blobs", "farthest"),
+    (65, 25, 16, "blobs", "farthest"),
+    (1000, 1, 5, "line", "farthest"),
+    (4097, 3, 2, "uniform", "farthest"),
+    (4099, 25, 16, "blobs", "farthest"),
+    (10_001, 7, 33, "uniform", "farthest"),
+    (50_003, 25, 16, "blobs", "farthest"),
+    (20_011, 32, 64, "blobs", "farthest"),
+    (20_013, 33, 8, "blobs", "farthest"),
+    (9_999, 64, 100, "uniform", "farthest"),
+    (30_001, 25, 256, "blobs", "farthest"),
+    (5_000, 16, 1024, "uniform", "farthest"),
+    (3_001, 4, 12, "dups", "random"),       # exact ties, duplicate centres, empty clusters
+    (10, 3, 16, "uniform", "random"),       # K > n: empty clusters keep their centres
+]
+
+
+@pytest.mark.parametrize("n,M,K,kind,init", SHAPES)
+def test_run_parity_shapes(n, M, K, kind, init):
+    X, C0 = workloads.random_case(n, M, K, seed=n + M + K, kind=kind, init=init)
+    run_parity(X, C0, K, 40, name=f"{kind}/{init}")
+
+
+@pytest.mark.parametrize("n,M,K", [(4099, 25, 16), (1000, 3, 5), (20_011, 32, 64)])
+def test_run_parity_fixed_iterations(n, M, K):
+    X, C0 = workloads.random_case(n, M, K, seed=7, kind="uniform")
+    _, _, _, it = run_parity(X, C0, K, 13, fixed=True, name="fixed")
+    assert it == 13
+
+
+def test_run_max_iter_one_and_alias():
+    X, C0 = workloads.random_case(5000, 6, 9, seed=3, kind="blobs")
+    run_parity(X, C0, 9, 1, name="max_iter=1")
+    # init_centers may alias centers
+    Cg = _gpu(C0)
+    lab, C, cnt, it = km.kmeans_run(_gpu(X), 9, Cg, 50, out=(
+        torch.empty(5000, dtype=torch.int32, device=DEV), Cg,
+        torch.empty(9, dtype=torch.int32, device=DEV)))
+    olab, oC, ocnt, oit = oracle.run(X, 9, C0, 50)
+    assert it == oit and np.array_equal(lab.cpu().numpy(), olab)
+    check_centers(C.cpu().numpy(), oC)
+
+
+# ------------------------------------------------------------ single steps
+
+@pytest.mark.parametrize("n,M,K", [(1, 1, 1), (777, 2, 3), (65_537, 25, 16), (10_000, 64, 200),
+                                   (4_000, 16, 1024), (3_000, 25, 655)])
+def test_assign_parity(n, M, K):
+    _say(f"[assign] n={n} M={M} K={K}")
+    rng = np.random.default_rng(n + K)
+    X = rng.standard_normal((n, M)).astype(np.float32)
+    C = rng.standard_normal((K, M)).astype(np.float32)
+    lab, d2 = km.kmeans_assign(_gpu(X), _gpu(C), with_min_d2=True)
+    olab, d1, od2 = oracle.assign(X, C, with_dist=True)
+    assert np.array_equal(lab.cpu().numpy(), olab)
+    np.testing.assert_allclose(d2.cpu().numpy(), d1, rtol=(M + 2) * 2.0**-22, atol=1e-30)
+
+
+def test_assign_near_ties_are_exact():
+    # objects placed on bisector hyperplanes between pairs of centres, so the
+    # fp32 distances cannot call them; the fp64 re-check must reproduce the
+    # oracle, including the lowest-index rule on exact ties
+    rng = np.random.default_rng(12)
+    M, K = 25, 16
+    C = rng.uniform(-50, 50, (K, M)).astype(np.float32)
+    a, b = rng.integers(0, K, 4000), rng.integers(0, K, 4000)
+    t = rng.uniform(0.49999, 0.50001, (4000, 1))
+    X = (C[a] * t + C[b] * (1 - t)).astype(np.float32)
+    X[:200] = C[rng.integers(0, K, 200)]                   # exactly on a centre
+    Cd = C.copy()
+    Cd[5] = Cd[2]                                          # duplicate centres: ties
+    for CC in (C, Cd):
+        lab = km.kmeans_assign(_gpu(X), _gpu(CC)).cpu().numpy()
+        assert np.array_equal(lab, oracle.assign(X, CC))
+
+
+@pytest.mark.parametrize("n,M,K", [(1, 2, 1), (1000, 3, 7), (65_537, 25, 16), (33_333, 64, 100),
+                                   (10_000, 10, 1024)])
+def test_update_parity(n, M, K):
+    _say(f"[update] n={n} M={M} K={K}")
+    rng = np.random.default_rng(n * 3 + K)
+    X = rng.uniform(-60, 60, (n, M)).astype(np.float32)
+    labels = rng.integers(0, K, n).astype(np.int32)
+    if K > 2:
+        labels[labels == 1] = 0                            # cluster 1 empty
+    prev = rng.standard_normal((K, M)).astype(np.float32)
+    C, cnt = km.kmeans_update(_gpu(X), _gpu(labels), K, _gpu(prev))
+    oC, ocnt = oracle.update(X, labels, K, prev)
+    assert np.array_equal(cnt.cpu().numpy(), ocnt)
+    check_centers(C.cpu().numpy(), oC)
+    # in place: centers aliasing prev_centers
+    P = _gpu(prev)
+    km.kmeans_update(_gpu(X), _gpu(labels), K, P, out=P)
+    check_centers(P.cpu().numpy(), oC)
+
+
+def test_determinism():
+    X, C0 = workloads.random_case(200_003, 25, 64, seed=1, kind="uniform")
+    Xg, Cg = _gpu(X), _gpu(C0)
+    a = km.kmeans_run(Xg, 64, Cg, 12, fixed_iters=True)
+    b = km.kmeans_run(Xg, 64, Cg, 12, fixed_iters=True)
+    for u, v in zip(a[:3], b[:3]):
+        assert torch.equal(u, v)
+    assert a[3] == b[3] == 12
+
+
+# ------------------------------------------------------------ the named workloads
+
+@pytest.mark.parametrize("name", ["1", "2", "3"])
+def test_workload_full_parity(name):
+    w = workloads.get(name)
+    X, _, _, init = workloads.load(name)
+    run_parity(X, init, w.K, w.max_iter, fixed=w.fixed, name=w.name)
+
+
+def test_workload3_fixed_mode_as_benchmarked():
+    # the benchmark runs this workload for a fixed 100 iterations; it converges
+    # at t = 2, after which every pass reproduces the same labels and centres
+    w = workloads.get("3")
+    X, _, _, init = workloads.load("3")
+    _say("[parity] aniso25d fixed 100")
+    lab, C, cnt, it = km.kmeans_run(_gpu(X), w.K, _gpu(init), 100, fixed_iters=True)
+    olab, oC, ocnt, oit = oracle.run(X, w.K, init, 100)
+    assert it == 100 and oit < 100
+    assert np.array_equal(lab.cpu().numpy(), olab)
+    assert np.array_equal(cnt.cpu().numpy(), ocnt)
+    check_centers(C.cpu().numpy(), oC)
+
+
+def _stepwise_at_scale(name, T, sample=20_000):
+    """Full-size check without the full oracle trajectory: the GPU's labels of
+    pass T are compared with the oracle's assignment (to the GPU's own centres
+    of pass T-1) on a seeded sample of objects, and the GPU's centres of pass T
+    with the oracle's Eq. (1) over all objects with the GPU's labels."""
+    w = workloads.get(name)
+    X, _, _, init = workloads.load(name)
+    Xg, Cg = _gpu(X), _gpu(init)
+    _say(f"[scale] {w.name}: GPU {T - 1} and {T} fixed iterations")
+    _, Cprev, _, _ = km.kmeans_run(Xg, w.K, Cg, T - 1, fixed_iters=True)
+    lab, C, cnt, it = km.kmeans_run(Xg, w.K, Cg, T, fixed_iters=True)
+    assert it == T
+    Cprev, lab, C, cnt = Cprev.cpu().numpy(), lab.cpu().numpy(), C.cpu().numpy(), cnt.cpu().numpy()
+    idx = np.random.default_rng(99).choice(X.shape[0], sample, replace=False)
+    olab, d1, d2 = oracle.assign(X[idx], Cprev, with_dist=True)
+    check_labels(lab[idx], olab, oracle.gap_rel(d1, d2))
+    oC, ocnt = oracle.update(X, lab, w.K, Cprev)
+    assert np.array_equal(cnt, ocnt)
+    nbits = check_centers(C, oC)
+    _say(f"[scale] {w.name}: sampled labels match; centres differ in {nbits} coordinates")
+    del Xg
+
+
+def test_workload4_at_scale():
+    _stepwise_at_scale("4", 30)
+
+
+def test_workload5_at_scale():
+    _stepwise_at_scale("5", 30, sample=10_000)
