@@ -32,6 +32,11 @@ HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, vendor peak
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = {
     "direct": os.path.join(ROOT, "paper_1402_3788_amd", "csrc", "lloyd_valu.hip"),
+    "mfma": os.path.join(ROOT, "paper_1402_3788_amd", "csrc", "lloyd_mfma.hip"),
+}
+KERNEL_NAMES = {
+    "direct": "lloyd_valu_kernel<M, assign+accumulate>",
+    "mfma": "lloyd_mfma_kernel<M, assign+accumulate>",
 }
 
 
@@ -143,7 +148,7 @@ def main():
     assign_avg_s = tm.assign_ms / 1e3 / tm.assign_launches
     finalize_avg_s = tm.finalize_ms / 1e3 / tm.finalize_launches
     achieved = launch_bytes / assign_avg_s / 1e9
-    kernel_key = "direct"
+    kernel_key = args.path or ("mfma" if K >= 16 else "direct")
     traffic = _traffic(kernel_key, w.name, launch_bytes)
 
     result = {
@@ -173,7 +178,7 @@ def main():
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
             "traffic": traffic,
-            "kernel": "lloyd_valu_kernel<25, assign+accumulate>",
+            "kernel": KERNEL_NAMES[kernel_key].replace("<M,", f"<{M},"),
             "bytes_per_launch": launch_bytes,
         },
     }

@@ -53,7 +53,11 @@ extern "C" {
 /* Flags (bitwise OR). */
 #define KMEANS_FIXED_ITERS  (1u << 0) /* kmeans_run: run exactly max_iter iterations, no early stop */
 #define KMEANS_PATH_DIRECT  (1u << 1) /* force the vector-ALU distance path                          */
-#define KMEANS_PATH_MFMA    (1u << 2) /* force the matrix-core (expanded-form) distance path          */
+#define KMEANS_PATH_MFMA    (1u << 2) /* force the matrix-core (expanded-form) distance path;         */
+                                      /* KMEANS_EUNSUPPORTED when its per-workgroup state (centre     */
+                                      /* operands, fp64 sums) does not fit in LDS for this K and M    */
+/* Without a path flag the matrix-core path is used for K >= 16 where it fits,
+ * the vector-ALU path otherwise. Both give the same labels, centres and counts. */
 
 /* Optional per-call timing, filled by kmeans_run when a non-NULL pointer is
  * passed: device time of the fused assign/accumulate launches and of the
@@ -67,9 +71,12 @@ typedef struct kmeans_timing {
 } kmeans_timing_t;
 
 /* Bytes of device workspace that kmeans_update and kmeans_run need for a problem
- * of this shape (per-workgroup fp64 partial sums and counts plus a small
- * control block). kmeans_assign needs none. Returns 0 for shapes outside the
- * envelope. Pure host computation. */
+ * of this shape and these flags (per-workgroup fp64 partial sums and counts,
+ * their totals, and a 256-byte control block at the start). kmeans_assign needs
+ * none. Returns 0 for shapes or flags the library refuses. Pure host
+ * computation. After kmeans_run, bytes 12..15 of the workspace hold (int32)
+ * the number of objects whose label was re-decided with fp64 distances during
+ * the run -- a diagnostic, not part of the result. */
 size_t kmeans_workspace_bytes(int64_t n, int32_t M, int32_t K, uint32_t flags);
 
 /* Human-readable name of a status code (static storage). */

@@ -13,7 +13,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libkmeans_mi355x.so")
-SOURCES = ["kmeans_api.hip", "lloyd_valu.hip", "lloyd_finalize.hip"]
+SOURCES = ["kmeans_api.hip", "lloyd_valu.hip", "lloyd_mfma.hip", "lloyd_finalize.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

@@ -25,36 +25,67 @@ int check_flags(uint32_t flags)
 {
     if (flags & ~kKnownFlags) return KMEANS_EINVAL;
     if ((flags & KMEANS_PATH_DIRECT) && (flags & KMEANS_PATH_MFMA)) return KMEANS_EINVAL;
-    if (flags & KMEANS_PATH_MFMA) return KMEANS_EUNSUPPORTED;   // no matrix-core path yet
     return KMEANS_OK;
 }
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-// Workspace: [Ctl (256 B)] [fp64 partial sums: G*K*M] [int32 partial counts: G*K]
+// Distance path: forced by a flag, else the matrix cores from K >= 16 on (one
+// full 16-centre tile) when their workgroup state fits in LDS, else the vector
+// ALU. Returns -1 when a forced matrix-core path does not fit.
+int select_path(int32_t M, int32_t K, uint32_t flags)
+{
+    if (flags & KMEANS_PATH_DIRECT) return kPathValu;
+    const bool fits = mfma_fits(M, K);
+    if (flags & KMEANS_PATH_MFMA) return fits ? kPathMfma : -1;
+    return (K >= 16 && fits) ? kPathMfma : kPathValu;
+}
+
+AccumPlan plan_for(int p, int64_t n, int32_t M, int32_t K, Mode mode)
+{
+    return p == kPathMfma ? plan_mfma(n, M, K, mode) : plan_valu(n, M, K, mode);
+}
+
+hipError_t launch_step(const StepArgs &a, Mode mode, const AccumPlan &plan, hipStream_t s)
+{
+    return plan.path == kPathMfma ? launch_mfma(a, mode, plan, s) : launch_valu(a, mode, plan, s);
+}
+
+// Workspace: [Ctl (256 B)] [fp64 totals K*M] [int32 totals K]
+//            [fp64 partial sums G*K*M] [int32 partial counts G*K]
 struct Layout {
     AccumPlan plan;
-    size_t sums_off, counts_off, total;
+    size_t tot_sums_off, tot_counts_off, sums_off, counts_off, total;
 };
 
-Layout layout(int64_t n, int32_t M, int32_t K)
+Layout layout(int64_t n, int32_t M, int32_t K, uint32_t flags)
 {
     Layout L{};
-    L.plan = plan_valu(n, M, K, kAssignAccum);
-    L.sums_off = align_up(sizeof(Ctl), 256);
-    L.counts_off = align_up(L.sums_off + (size_t)L.plan.groups * K * M * sizeof(double), 256);
+    L.plan = plan_for(select_path(M, K, flags), n, M, K, kAssignAccum);
+    const size_t km = (size_t)K * M;
+    L.tot_sums_off = align_up(sizeof(Ctl), 256);
+    L.tot_counts_off = align_up(L.tot_sums_off + km * sizeof(double), 256);
+    L.sums_off = align_up(L.tot_counts_off + (size_t)K * sizeof(int32_t), 256);
+    L.counts_off = align_up(L.sums_off + (size_t)L.plan.groups * km * sizeof(double), 256);
     L.total = align_up(L.counts_off + (size_t)L.plan.groups * K * sizeof(int32_t), 256);
     return L;
 }
 
-int hip_status(hipError_t e) { return e == hipSuccess ? KMEANS_OK : KMEANS_EHIP; }
-
-hipError_t allow_lds(const AccumPlan &)
+FinalizeArgs finalize_args(const Layout &L, char *ws, int32_t K, int32_t M)
 {
-    // gfx950 serves up to 160 KB of LDS per workgroup without an opt-in; nothing
-    // to configure, kept as the single place to add one.
-    return hipSuccess;
+    FinalizeArgs f{};
+    f.part_sums = reinterpret_cast<const double *>(ws + L.sums_off);
+    f.part_counts = reinterpret_cast<const int32_t *>(ws + L.counts_off);
+    f.groups = L.plan.groups;
+    f.K = K;
+    f.M = M;
+    f.tot_sums = reinterpret_cast<double *>(ws + L.tot_sums_off);
+    f.tot_counts = reinterpret_cast<int32_t *>(ws + L.tot_counts_off);
+    f.ticket = &reinterpret_cast<Ctl *>(ws)->ticket;
+    return f;
 }
+
+int hip_status(hipError_t e) { return e == hipSuccess ? KMEANS_OK : KMEANS_EHIP; }
 
 }  // namespace
 
@@ -75,7 +106,8 @@ const char *kmeans_strerror(int status)
 size_t kmeans_workspace_bytes(int64_t n, int32_t M, int32_t K, uint32_t flags)
 {
     if (check_shape(n, M, K) != KMEANS_OK || (flags & ~kKnownFlags)) return 0;
-    return layout(n, M, K).total;
+    if (check_flags(flags) != KMEANS_OK || select_path(M, K, flags) < 0) return 0;
+    return layout(n, M, K, flags).total;
 }
 
 int kmeans_assign(const float *X, int64_t n, int32_t M, const float *centers, int32_t K,
@@ -84,14 +116,15 @@ int kmeans_assign(const float *X, int64_t n, int32_t M, const float *centers, in
     if (!X || !centers || !labels) return KMEANS_EINVAL;
     int rc = check_shape(n, M, K);
     if (rc) return rc;
-    if ((rc = check_flags(flags & ~KMEANS_FIXED_ITERS))) return rc;
+    if ((rc = check_flags(flags)) || (flags & KMEANS_FIXED_ITERS)) return rc ? rc : KMEANS_EINVAL;
     if (!aligned16(X)) return KMEANS_EINVAL;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    const AccumPlan plan = plan_valu(n, M, K, kAssign);
+    if (select_path(M, K, flags) < 0) return KMEANS_EUNSUPPORTED;
+    const AccumPlan plan = plan_for(select_path(M, K, flags), n, M, K, kAssign);
     StepArgs a{};
     a.X = X; a.n = n; a.M = M; a.C = centers; a.K = K;
     a.labels = labels; a.min_d2 = min_d2;
-    return hip_status(launch_valu(a, kAssign, plan, s));
+    return hip_status(launch_step(a, kAssign, plan, s));
 }
 
 int kmeans_update(const float *X, int64_t n, int32_t M, const int32_t *labels, int32_t K,
@@ -102,7 +135,7 @@ int kmeans_update(const float *X, int64_t n, int32_t M, const int32_t *labels, i
     int rc = check_shape(n, M, K);
     if (rc) return rc;
     if (!aligned16(X)) return KMEANS_EINVAL;
-    const Layout L = layout(n, M, K);
+    const Layout L = layout(n, M, K, 0);
     if (!workspace || workspace_bytes < L.total) return KMEANS_EWORKSPACE;
     hipStream_t s = static_cast<hipStream_t>(stream);
     char *ws = static_cast<char *>(workspace);
@@ -111,11 +144,10 @@ int kmeans_update(const float *X, int64_t n, int32_t M, const int32_t *labels, i
     a.labels_in = labels;
     a.part_sums = reinterpret_cast<double *>(ws + L.sums_off);
     a.part_counts = reinterpret_cast<int32_t *>(ws + L.counts_off);
-    AccumPlan plan = plan_valu(n, M, K, kAccumLabels);
-    if ((rc = hip_status(allow_lds(plan)))) return rc;
-    if ((rc = hip_status(launch_valu(a, kAccumLabels, plan, s)))) return rc;
-    return hip_status(launch_finalize(a.part_sums, a.part_counts, plan.groups, K, M, prev_centers,
-                                      centers, counts, nullptr, 0, 1, 0, s));
+    const FinalizeArgs f = finalize_args(L, ws, K, M);
+    if ((rc = hip_status(launch_ctl_reset(reinterpret_cast<Ctl *>(ws), s)))) return rc;
+    if ((rc = hip_status(launch_step(a, kAccumLabels, L.plan, s)))) return rc;
+    return hip_status(launch_finalize(f, prev_centers, centers, counts, nullptr, 0, 1, 0, s));
 }
 
 int kmeans_run(const float *X, int64_t n, int32_t M, int32_t K, const float *init_centers,
@@ -129,7 +161,8 @@ int kmeans_run(const float *X, int64_t n, int32_t M, int32_t K, const float *ini
     if (max_iter < 1) return KMEANS_EINVAL;
     if ((rc = check_flags(flags))) return rc;
     if (!aligned16(X)) return KMEANS_EINVAL;
-    const Layout L = layout(n, M, K);
+    if (select_path(M, K, flags) < 0) return KMEANS_EUNSUPPORTED;
+    const Layout L = layout(n, M, K, flags);
     if (!workspace || workspace_bytes < L.total) return KMEANS_EWORKSPACE;
 
     hipStream_t s = static_cast<hipStream_t>(stream);
@@ -145,7 +178,7 @@ int kmeans_run(const float *X, int64_t n, int32_t M, int32_t K, const float *ini
     a.ctl = ctl;
     a.fixed = fixed;
 
-    if ((rc = hip_status(allow_lds(L.plan)))) return rc;
+    const FinalizeArgs f = finalize_args(L, ws, K, M);
     if ((rc = hip_status(launch_ctl_reset(ctl, s)))) return rc;
     if (init_centers != centers) {
         rc = hip_status(hipMemcpyAsync(centers, init_centers, sizeof(float) * (size_t)K * M,
@@ -176,11 +209,10 @@ int kmeans_run(const float *X, int64_t n, int32_t M, int32_t K, const float *ini
         const int end = (fixed || t + chunk - 1 >= max_iter) ? max_iter : t + chunk - 1;
         for (int tt = t; tt <= end && !rc; ++tt) {
             a.t = tt;
-            rc = hip_status(launch_valu(a, kAssignAccum, L.plan, s));
+            rc = hip_status(launch_step(a, kAssignAccum, L.plan, s));
             if (!rc) rc = mark();
             if (!rc)
-                rc = hip_status(launch_finalize(a.part_sums, a.part_counts, L.plan.groups, K, M,
-                                                centers, centers, counts, ctl, tt, fixed, 1, s));
+                rc = hip_status(launch_finalize(f, centers, centers, counts, ctl, tt, fixed, 1, s));
             if (!rc) rc = mark();
         }
         t = end + 1;

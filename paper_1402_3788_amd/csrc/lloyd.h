@@ -7,27 +7,37 @@
 
 namespace lloyd {
 
-constexpr int kWave = 64;          // CDNA wavefront width
-constexpr int kMaxM = 64;          // features supported
-constexpr int kMaxK = 1024;        // clusters supported
-constexpr int kMaxKM = 16384;      // K * M supported
+constexpr int kWave = 64;            // CDNA wavefront width
+constexpr int kMaxM = 64;            // features supported
+constexpr int kMaxK = 1024;          // clusters supported
+constexpr int kMaxKM = 16384;        // K * M supported
 constexpr int kMaxLds = 160 * 1024;  // LDS bytes per workgroup on gfx950
-constexpr int kMaxGroups = 1024;   // persistent workgroups of the accumulating launches
+constexpr int kCUs = 256;            // compute units the launch geometry is sized for
 
-// Iteration control block, kept in the caller's workspace (device memory).
-//   changed[t & 1]  : set (integer OR) by the finalise launch of iteration t when
-//                     any centre coordinate differs bitwise from iteration t-1;
-//                     cleared by iteration t's assign launch before that.
-//   converged_at    : first t >= 2 whose centres were congruent with t-1's
-//                     (0 = not yet); written by the finalise launch of t+1.
-//   fallbacks       : objects whose label was re-decided in fp64 (diagnostic).
+// Iteration control block, kept at the start of the caller's workspace.
+//   changed[t & 1] : set by the finalise launch of iteration t when any centre
+//                    coordinate differs bitwise from iteration t-1; cleared by
+//                    iteration t's assign launch before that.
+//   converged_at   : first t >= 2 whose centres were congruent with t-1's
+//                    (0 = not yet); written by the finalise launch of t+1.
+//   fallbacks      : objects whose label was re-decided in fp64 (diagnostic).
+//   ticket         : arrival counter of the finalise launch's workgroups.
 struct Ctl {
     int32_t changed[2];
     int32_t converged_at;
     int32_t fallbacks;
-    int32_t pad[60];
+    uint32_t ticket;
+    int32_t pad[59];
 };
 static_assert(sizeof(Ctl) == 256, "control block is one 256-byte slot");
+
+// Early exit of a launch that belongs to an iteration after convergence.
+__device__ inline bool stop_before(const Ctl *ctl, int t, int fixed)
+{
+    if (ctl == nullptr || fixed) return false;
+    if (ctl->converged_at != 0) return true;
+    return (t - 1 >= 2) && ctl->changed[(t - 1) & 1] == 0;
+}
 
 // What a launch of the distance kernels does with the assignment.
 enum Mode : int {
@@ -36,38 +46,57 @@ enum Mode : int {
     kAccumLabels = 2,   // partial sums/counts from caller-provided labels
 };
 
+enum Path : int { kPathValu = 0, kPathMfma = 1 };
+
 struct AccumPlan {
+    Path path;
     int waves;          // wavefronts per workgroup
     int groups;         // workgroups (persistent, strided over 64-object tiles)
+    int accum;          // accumulation form of the matrix-core kernel (1 wave, 2 block)
     size_t lds_bytes;   // dynamic LDS per workgroup
 };
 
-// Launch geometry of the vector-ALU kernel for a problem shape (pure host code).
+// Launch geometry for a problem shape (pure host code).
 AccumPlan plan_valu(int64_t n, int M, int K, Mode mode);
+AccumPlan plan_mfma(int64_t n, int M, int K, Mode mode);
+// Whether the matrix-core kernel's per-workgroup state (centre operands and
+// fp64 slab) fits in one workgroup's LDS for this shape.
+bool mfma_fits(int M, int K);
 
 struct StepArgs {
     const float *X;
     int64_t n;
     int M;
-    const float *C;          // centres read by the assignment
+    const float *C;            // centres read by the assignment
     int K;
-    int32_t *labels;         // out (modes 0/1)
+    int32_t *labels;           // out (modes 0/1)
     const int32_t *labels_in;  // in (mode 2)
-    float *min_d2;           // optional out (mode 0)
-    double *part_sums;       // [groups][K][M] (modes 1/2)
-    int32_t *part_counts;    // [groups][K]
-    Ctl *ctl;                // iteration control (mode 1 in a run), else null
-    int t;                   // iteration number (1-based) for the control block
-    int fixed;               // no early stop
+    float *min_d2;             // optional out (mode 0)
+    double *part_sums;         // [groups][K][M] (modes 1/2)
+    int32_t *part_counts;      // [groups][K]
+    Ctl *ctl;                  // iteration control (mode 1 in a run), else null
+    int t;                     // iteration number (1-based) for the control block
+    int fixed;                 // no early stop
 };
 
 hipError_t launch_valu(const StepArgs &a, Mode mode, const AccumPlan &plan, hipStream_t s);
+hipError_t launch_mfma(const StepArgs &a, Mode mode, const AccumPlan &plan, hipStream_t s);
 
-// Reduce the per-workgroup partials in fixed order, form fp32 centres (Eq. (1)),
-// write counts, and (compare != 0) flag a change against prev for iteration t.
-hipError_t launch_finalize(const double *part_sums, const int32_t *part_counts, int groups,
-                           int K, int M, const float *prev, float *centers, int32_t *counts,
-                           Ctl *ctl, int t, int fixed, int compare, hipStream_t s);
+// Finalise: reduce the G per-workgroup partials in a fixed order into totals,
+// then (last workgroup) form the fp32 centres of Eq. (1), the counts, and the
+// change flag of iteration t.
+struct FinalizeArgs {
+    const double *part_sums;
+    const int32_t *part_counts;
+    int groups, K, M;
+    double *tot_sums;     // [K][M] scratch
+    int32_t *tot_counts;  // [K] scratch
+    uint32_t *ticket;     // zero before the launch; left zero after it
+};
+
+int finalize_blocks(int K, int M);
+hipError_t launch_finalize(const FinalizeArgs &f, const float *prev, float *centers,
+                           int32_t *counts, Ctl *ctl, int t, int fixed, int compare, hipStream_t s);
 
 hipError_t launch_ctl_reset(Ctl *ctl, hipStream_t s);
 

@@ -13,13 +13,14 @@
 //      in a fixed operation order and takes the lowest-index minimum, so the
 //      label is the exact-arithmetic argmin;
 //   3. accumulation (the numerator and denominator of Eq. (1)): for each cluster,
-//      a ballot gives the lanes holding its members; lanes then act as feature
-//      columns and add the members' features (read back from the LDS tile) into
-//      an fp64 running sum, two members per step (one per half-wave), and the
-//      sum is added to the wave's private fp64 slab. No atomics are involved.
+//      a ballot gives the lanes holding its members; lanes then act as (slot,
+//      feature) pairs and add the members' features (read back from the LDS
+//      tile) into fp64 running sums, and the sum is added to the wave's private
+//      fp64 slab (wave_accumulate). No atomics are involved.
 //   4. at the end the workgroup adds its waves' slabs in wave order and writes
 //      one fp64 partial per (cluster, feature) plus one count per cluster.
 #include "lloyd.h"
+#include "lloyd_device.h"
 
 #include <math.h>
 
@@ -27,91 +28,8 @@ namespace lloyd {
 
 namespace {
 
-__device__ inline bool stop_before(const Ctl *ctl, int t, int fixed)
-{
-    if (ctl == nullptr || fixed) return false;
-    if (ctl->converged_at != 0) return true;
-    return (t - 1 >= 2) && ctl->changed[(t - 1) & 1] == 0;
-}
-
-template <int M>
-struct TileGeom {
-    static constexpr int kFloats = kWave * M;          // floats per 64-object tile
-    static constexpr int kVec = kFloats / 4;           // float4s per tile (64*M divisible by 4)
-    static constexpr int kVecPerLane = (kVec + kWave - 1) / kWave;
-};
-
-// Issue the loads of tile q (objects 64q .. 64q+63) into registers.
-template <int M>
-__device__ inline void load_tile(const float *__restrict__ X, int64_t n, int64_t q, int lane,
-                                 float4 (&buf)[TileGeom<M>::kVecPerLane])
-{
-    using G = TileGeom<M>;
-    const int64_t f0 = q * (int64_t)G::kFloats;
-    const int64_t total = n * (int64_t)M;
-    const int64_t left = total - f0;
-    const int nf = left < G::kFloats ? (int)left : G::kFloats;   // floats present
-    const float4 *src = reinterpret_cast<const float4 *>(X + f0);
-#pragma unroll
-    for (int v = 0; v < G::kVecPerLane; ++v) {
-        const int idx = lane + kWave * v;
-        if (idx < G::kVec) {
-            if (4 * idx + 3 < nf) {
-                buf[v] = src[idx];
-            } else {
-                const float *s = X + f0 + 4 * idx;
-                float4 r = make_float4(0.f, 0.f, 0.f, 0.f);
-                if (4 * idx + 0 < nf) r.x = s[0];
-                if (4 * idx + 1 < nf) r.y = s[1];
-                if (4 * idx + 2 < nf) r.z = s[2];
-                buf[v] = r;
-            }
-        }
-    }
-}
-
-template <int M>
-__device__ inline void store_tile(float *tile, int lane,
-                                  const float4 (&buf)[TileGeom<M>::kVecPerLane])
-{
-    using G = TileGeom<M>;
-    float4 *dst = reinterpret_cast<float4 *>(tile);
-#pragma unroll
-    for (int v = 0; v < G::kVecPerLane; ++v) {
-        const int idx = lane + kWave * v;
-        if (idx < G::kVec) dst[idx] = buf[v];
-    }
-}
-
-// fp64 squared distance in the reference operation order: for j ascending,
-// e = x_j - c_j, then d = d + e*e, every operation rounded on its own (this file
-// is compiled with -ffp-contract=off, so nothing is fused).
-template <int M>
-__device__ inline int argmin_fp64(const float (&x)[M], const float *__restrict__ C, int K,
-                                  double &best_out)
-{
-    double best = INFINITY;
-    int lab = 0;
-    for (int k = 0; k < K; ++k) {
-        const float *c = C + k * M;
-        double d = 0.0;
-#pragma unroll
-        for (int j = 0; j < M; ++j) {
-            const double e = (double)x[j] - (double)c[j];
-            const double sq = e * e;
-            d = d + sq;
-        }
-        if (d < best) {
-            best = d;
-            lab = k;
-        }
-    }
-    best_out = best;
-    return lab;
-}
-
 template <int M, int MODE>
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(1024)
 lloyd_valu_kernel(const float *__restrict__ X, int64_t n, const float *__restrict__ C, int K,
                   int32_t *__restrict__ labels, const int32_t *__restrict__ labels_in,
                   float *__restrict__ min_d2, double *__restrict__ part_sums,
@@ -128,14 +46,19 @@ lloyd_valu_kernel(const float *__restrict__ X, int64_t n, const float *__restric
         if (ctl != nullptr && blockIdx.x == 0 && threadIdx.x == 0) ctl->changed[t & 1] = 0;
     }
 
-    float *tile = reinterpret_cast<float *>(smem) + wave * G::kFloats;
-    double *slab = reinterpret_cast<double *>(smem + (size_t)W * G::kFloats * 4) +
-                   (size_t)wave * K * M;
-    int32_t *cnt = reinterpret_cast<int32_t *>(smem + (size_t)W * G::kFloats * 4 +
-                                               (size_t)W * K * M * 8) + wave * K;
+    using S = Slots<M>;
+    constexpr int MW = S::MW;
+    // LDS: [ones: 68 floats] [W tiles of kTileFloats] [W slabs of K*(M+1) fp64]
+    float *ones = reinterpret_cast<float *>(smem);
+    float *tile = ones + 68 + wave * S::kTileFloats;
+    double *slab = reinterpret_cast<double *>(smem + (68 + (size_t)W * S::kTileFloats) * 4) +
+                   (size_t)wave * K * MW;
+    for (int i = lane; i < S::kTileFloats - kWave * M; i += kWave) tile[kWave * M + i] = 0.f;
     if (MODE != kAssign) {
-        for (int i = lane; i < K * M; i += kWave) slab[i] = 0.0;
-        for (int i = lane; i < K; i += kWave) cnt[i] = 0;
+        for (int i = lane; i < K * MW; i += kWave) slab[i] = 0.0;
+        if (wave == 0)
+            for (int i = lane; i < 68; i += kWave) ones[i] = i < kWave ? 1.f : 0.f;
+        __syncthreads();
     }
 
     // Bound on the relative error of an fp32 squared distance (M products and
@@ -212,40 +135,7 @@ lloyd_valu_kernel(const float *__restrict__ X, int64_t n, const float *__restric
             if (!valid) lab = -1;
         }
 
-        if (MODE != kAssign) {
-            const bool hi = lane >= 32;
-            const int jl = (M <= 32) ? (lane & 31) : lane;
-            for (int k = 0; k < K; ++k) {
-                uint64_t mask = __ballot(lab == k);
-                if (mask == 0) continue;
-                if (lane == 0) cnt[k] += __popcll(mask);
-                double acc = 0.0;
-                if (M <= 32) {
-                    // two members per step: the lower half-wave takes the
-                    // first, the upper half-wave the second
-                    while (mask) {
-                        const int p0 = __ffsll((unsigned long long)mask) - 1;
-                        mask &= mask - 1;
-                        int p1 = -1;
-                        if (mask) {
-                            p1 = __ffsll((unsigned long long)mask) - 1;
-                            mask &= mask - 1;
-                        }
-                        const int pp = hi ? p1 : p0;
-                        if (jl < M && pp >= 0) acc = acc + (double)tile[pp * M + jl];
-                    }
-                    const double upper = __shfl_down(acc, 32, kWave);
-                    if (lane < M) slab[k * M + lane] = slab[k * M + lane] + (acc + upper);
-                } else {
-                    while (mask) {
-                        const int p0 = __ffsll((unsigned long long)mask) - 1;
-                        mask &= mask - 1;
-                        if (lane < M) acc = acc + (double)tile[p0 * M + lane];
-                    }
-                    if (lane < M) slab[k * M + lane] = slab[k * M + lane] + acc;
-                }
-            }
-        }
+        if (MODE != kAssign) wave_accumulate<M>(lab, tile, ones, slab, K, lane);
         __builtin_amdgcn_wave_barrier();
     }
 
@@ -253,19 +143,19 @@ lloyd_valu_kernel(const float *__restrict__ X, int64_t n, const float *__restric
 
     if (MODE != kAssign) {
         __syncthreads();
-        const double *slabs = reinterpret_cast<const double *>(smem + (size_t)W * G::kFloats * 4);
-        const int32_t *cnts = reinterpret_cast<const int32_t *>(
-            smem + (size_t)W * G::kFloats * 4 + (size_t)W * K * M * 8);
+        const double *slabs =
+            reinterpret_cast<const double *>(smem + (68 + (size_t)W * S::kTileFloats) * 4);
         double *out = part_sums + (int64_t)blockIdx.x * K * M;
-        for (int idx = threadIdx.x; idx < K * M; idx += blockDim.x) {
-            double s = slabs[idx];
-            for (int w = 1; w < W; ++w) s = s + slabs[(size_t)w * K * M + idx];
-            out[idx] = s;
+        for (int e = threadIdx.x; e < K * M; e += blockDim.x) {
+            const int k = e / M, j = e - (e / M) * M;
+            double s = slabs[k * MW + j];
+            for (int w = 1; w < W; ++w) s = s + slabs[(size_t)w * K * MW + k * MW + j];
+            out[e] = s;
         }
         for (int k = threadIdx.x; k < K; k += blockDim.x) {
-            int32_t c = cnts[k];
-            for (int w = 1; w < W; ++w) c += cnts[w * K + k];
-            part_counts[(int64_t)blockIdx.x * K + k] = c;
+            double c = 0.0;
+            for (int w = 0; w < W; ++w) c = c + slabs[(size_t)w * K * MW + k * MW + M];
+            part_counts[(int64_t)blockIdx.x * K + k] = (int32_t)c;
         }
     }
 }
@@ -312,17 +202,19 @@ constexpr auto make_table(std::integer_sequence<int, Is...>)
 AccumPlan plan_valu(int64_t n, int M, int K, Mode mode)
 {
     AccumPlan p{};
-    const size_t tile = (size_t)kWave * M * 4;
-    const size_t per_wave = tile + (mode == kAssign ? 0 : (size_t)K * M * 8 + (size_t)K * 4);
-    int W = 4;
-    while (W > 1 && (size_t)W * per_wave > (size_t)kMaxLds) W /= 2;
+    p.path = kPathValu;
+    const size_t tile = (size_t)((kWave * M + (M > 4 ? M : 4) + 3) / 4 * 4) * 4;
+    const size_t per_wave = tile + (mode == kAssign ? 0 : (size_t)K * (M + 1) * 8);
+    int W = 16;
+    while (W > 1 && 68 * 4 + (size_t)W * per_wave > (size_t)kMaxLds) W /= 2;
     const int64_t nq = (n + kWave - 1) / kWave;
+    while (W > 1 && W / 2 >= nq) W /= 2;
     int64_t groups = (nq + W - 1) / W;
-    const int64_t cap = mode == kAssign ? 8192 : kMaxGroups;
-    if (groups > cap) groups = cap;
+    if (groups > kCUs) groups = kCUs;       // one persistent workgroup per compute unit
     p.waves = W;
     p.groups = (int)groups;
-    p.lds_bytes = (size_t)W * per_wave;
+    p.accum = 1;
+    p.lds_bytes = 68 * 4 + (size_t)W * per_wave;
     return p;
 }
 

@@ -46,9 +46,22 @@ def check_labels(lab, olab, gap):
     return int(mism.sum())
 
 
+def outside_mfma_envelope(n, M, K, path):
+    """A forced matrix-core path is refused (EUNSUPPORTED) exactly when its
+    workgroup state does not fit in LDS; the library reports that as a zero
+    workspace size."""
+    return path == "mfma" and km.kmeans_workspace_bytes(n, M, K, km.KMEANS_PATH_MFMA) == 0
+
+
 def run_parity(X, init, K, max_iter, fixed=False, path=None, name=""):
     _say(f"[parity] {name} n={X.shape[0]} M={X.shape[1]} K={K} max_iter={max_iter} "
          f"fixed={fixed} path={path}")
+    if outside_mfma_envelope(X.shape[0], X.shape[1], K, path):
+        with pytest.raises(km.KmeansError) as e:
+            km.kmeans_run(_gpu(X), K, _gpu(init), max_iter, fixed_iters=fixed, path=path)
+        assert e.value.code == km.KMEANS_EUNSUPPORTED
+        _say("[parity] outside the matrix-core envelope: refused as documented")
+        return None, None, None, max_iter
     lab, C, cnt, it = km.kmeans_run(_gpu(X), K, _gpu(init), max_iter, fixed_iters=fixed,
                                     path=path)
     lab, C, cnt = lab.cpu().numpy(), C.cpu().numpy(), cnt.cpu().numpy()
@@ -86,16 +99,21 @@ SHAPES = [
 ]
 
 
+PATHS = ["direct", "mfma"]
+
+
+@pytest.mark.parametrize("path", PATHS)
 @pytest.mark.parametrize("n,M,K,kind,init", SHAPES)
-def test_run_parity_shapes(n, M, K, kind, init):
+def test_run_parity_shapes(n, M, K, kind, init, path):
     X, C0 = workloads.random_case(n, M, K, seed=n + M + K, kind=kind, init=init)
-    run_parity(X, C0, K, 40, name=f"{kind}/{init}")
+    run_parity(X, C0, K, 40, path=path, name=f"{kind}/{init}")
 
 
+@pytest.mark.parametrize("path", PATHS)
 @pytest.mark.parametrize("n,M,K", [(4099, 25, 16), (1000, 3, 5), (20_011, 32, 64)])
-def test_run_parity_fixed_iterations(n, M, K):
+def test_run_parity_fixed_iterations(n, M, K, path):
     X, C0 = workloads.random_case(n, M, K, seed=7, kind="uniform")
-    _, _, _, it = run_parity(X, C0, K, 13, fixed=True, name="fixed")
+    _, _, _, it = run_parity(X, C0, K, 13, fixed=True, path=path, name="fixed")
     assert it == 13
 
 
@@ -116,12 +134,17 @@ def test_run_max_iter_one_and_alias():
 
 @pytest.mark.parametrize("n,M,K", [(1, 1, 1), (777, 2, 3), (65_537, 25, 16), (10_000, 64, 200),
                                    (4_000, 16, 1024), (3_000, 25, 655)])
-def test_assign_parity(n, M, K):
-    _say(f"[assign] n={n} M={M} K={K}")
+@pytest.mark.parametrize("path", PATHS)
+def test_assign_parity(n, M, K, path):
+    _say(f"[assign] n={n} M={M} K={K} path={path}")
     rng = np.random.default_rng(n + K)
     X = rng.standard_normal((n, M)).astype(np.float32)
     C = rng.standard_normal((K, M)).astype(np.float32)
-    lab, d2 = km.kmeans_assign(_gpu(X), _gpu(C), with_min_d2=True)
+    if outside_mfma_envelope(n, M, K, path):
+        with pytest.raises(km.KmeansError):
+            km.kmeans_assign(_gpu(X), _gpu(C), path=path)
+        return
+    lab, d2 = km.kmeans_assign(_gpu(X), _gpu(C), with_min_d2=True, path=path)
     olab, d1, od2 = oracle.assign(X, C, with_dist=True)
     assert np.array_equal(lab.cpu().numpy(), olab)
     np.testing.assert_allclose(d2.cpu().numpy(), d1, rtol=(M + 2) * 2.0**-22, atol=1e-30)
@@ -141,8 +164,9 @@ def test_assign_near_ties_are_exact():
     Cd = C.copy()
     Cd[5] = Cd[2]                                          # duplicate centres: ties
     for CC in (C, Cd):
-        lab = km.kmeans_assign(_gpu(X), _gpu(CC)).cpu().numpy()
-        assert np.array_equal(lab, oracle.assign(X, CC))
+        for path in PATHS:
+            lab = km.kmeans_assign(_gpu(X), _gpu(CC), path=path).cpu().numpy()
+            assert np.array_equal(lab, oracle.assign(X, CC)), path
 
 
 @pytest.mark.parametrize("n,M,K", [(1, 2, 1), (1000, 3, 7), (65_537, 25, 16), (33_333, 64, 100),
@@ -165,11 +189,12 @@ def test_update_parity(n, M, K):
     check_centers(P.cpu().numpy(), oC)
 
 
-def test_determinism():
+@pytest.mark.parametrize("path", PATHS)
+def test_determinism(path):
     X, C0 = workloads.random_case(200_003, 25, 64, seed=1, kind="uniform")
     Xg, Cg = _gpu(X), _gpu(C0)
-    a = km.kmeans_run(Xg, 64, Cg, 12, fixed_iters=True)
-    b = km.kmeans_run(Xg, 64, Cg, 12, fixed_iters=True)
+    a = km.kmeans_run(Xg, 64, Cg, 12, fixed_iters=True, path=path)
+    b = km.kmeans_run(Xg, 64, Cg, 12, fixed_iters=True, path=path)
     for u, v in zip(a[:3], b[:3]):
         assert torch.equal(u, v)
     assert a[3] == b[3] == 12
@@ -177,11 +202,12 @@ def test_determinism():
 
 # ------------------------------------------------------------ the named workloads
 
+@pytest.mark.parametrize("path", PATHS)
 @pytest.mark.parametrize("name", ["1", "2", "3"])
-def test_workload_full_parity(name):
+def test_workload_full_parity(name, path):
     w = workloads.get(name)
     X, _, _, init = workloads.load(name)
-    run_parity(X, init, w.K, w.max_iter, fixed=w.fixed, name=w.name)
+    run_parity(X, init, w.K, w.max_iter, fixed=w.fixed, path=path, name=w.name)
 
 
 def test_workload3_fixed_mode_as_benchmarked():
