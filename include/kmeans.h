@@ -60,14 +60,15 @@ extern "C" {
  * the vector-ALU path otherwise. Both give the same labels, centres and counts. */
 
 /* Optional per-call timing, filled by kmeans_run when a non-NULL pointer is
- * passed: device time of the fused assign/accumulate launches and of the
- * finalise launches, measured with HIP events recorded on `stream` around every
- * launch. Timing adds one event record per launch. */
+ * passed: device time of the per-iteration launches (each one assigns,
+ * accumulates, forms the centres and compares them), measured with HIP events
+ * recorded on `stream` between consecutive launches. Timing adds one event
+ * record per launch; in early-stop mode the intervals also contain the host's
+ * convergence polls, so it is meant for KMEANS_FIXED_ITERS runs. */
 typedef struct kmeans_timing {
-    double  assign_ms;        /* summed duration of the assign/accumulate launches */
-    double  finalize_ms;      /* summed duration of the finalise/compare launches  */
-    int32_t assign_launches;
-    int32_t finalize_launches;
+    double  step_ms;          /* summed duration of the iteration launches */
+    int32_t step_launches;    /* number of intervals summed                 */
+    int32_t reserved;
 } kmeans_timing_t;
 
 /* Bytes of device workspace that kmeans_update and kmeans_run need for a problem

@@ -37,8 +37,8 @@ EXPORTED = ("kmeans_workspace_bytes", "kmeans_strerror", "kmeans_assign", "kmean
 
 
 class KmeansTiming(ctypes.Structure):
-    _fields_ = [("assign_ms", ctypes.c_double), ("finalize_ms", ctypes.c_double),
-                ("assign_launches", ctypes.c_int32), ("finalize_launches", ctypes.c_int32)]
+    _fields_ = [("step_ms", ctypes.c_double), ("step_launches", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
 
 
 class KmeansError(RuntimeError):

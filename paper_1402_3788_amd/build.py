@@ -13,7 +13,12 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libkmeans_mi355x.so")
-SOURCES = ["kmeans_api.hip", "lloyd_valu.hip", "lloyd_mfma.hip", "lloyd_finalize.hip"]
+# (source, extra flags, object name); the kernel files are compiled once per
+# part of the feature-count range so the template instantiations build in parallel
+PARTS = 4
+SOURCES = ([("kmeans_api.hip", [], "kmeans_api.o"), ("lloyd_ctl.hip", [], "lloyd_ctl.o")]
+           + [(f, [f"-DLLOYD_PART={p}"], f.replace(".hip", f"_part{p}.o"))
+              for f in ("lloyd_mfma.hip", "lloyd_valu.hip") for p in range(PARTS)])
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [
@@ -32,17 +37,17 @@ def hipcc() -> str:
     return os.path.join(rocm, "bin", "hipcc")
 
 
-def build(verbose: bool = True, jobs: int = 4) -> str:
+def build(verbose: bool = True, jobs: int = 8) -> str:
     """Compile every source to an object file (in parallel), then link."""
     objdir = os.path.join(HERE, "_build")
     os.makedirs(objdir, exist_ok=True)
     procs = []
     objs = []
     t0 = time.time()
-    for src in SOURCES:
-        obj = os.path.join(objdir, src.replace(".hip", ".o"))
+    for src, extra, oname in SOURCES:
+        obj = os.path.join(objdir, oname)
         objs.append(obj)
-        cmd = [hipcc(), *HIPCC_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [hipcc(), *HIPCC_FLAGS, *extra, "-c", os.path.join(CSRC, src), "-o", obj]
         procs.append((src, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)))
         while sum(p.poll() is None for _, p in procs) >= jobs:
             time.sleep(0.05)

@@ -2,6 +2,7 @@
 // and the iteration control of Algorithm 1 (steps 2-7). See include/kmeans.h.
 #include "../../include/kmeans.h"
 #include "lloyd.h"
+#include "lloyd_reduce.h"
 
 #include <vector>
 
@@ -51,11 +52,13 @@ hipError_t launch_step(const StepArgs &a, Mode mode, const AccumPlan &plan, hipS
     return plan.path == kPathMfma ? launch_mfma(a, mode, plan, s) : launch_valu(a, mode, plan, s);
 }
 
-// Workspace: [Ctl (256 B)] [fp64 totals K*M] [int32 totals K]
-//            [fp64 partial sums G*K*M] [int32 partial counts G*K]
+// Workspace: [Ctl (256 B)] [fp64 group partials NG*K*M] [int32 group counts NG*K]
+//            [fp64 workgroup partials G*K*M] [int32 workgroup counts G*K]
+// with G the persistent workgroups of the accumulating launch and
+// NG = ceil(G / kGroup) the first-level reduction groups.
 struct Layout {
     AccumPlan plan;
-    size_t tot_sums_off, tot_counts_off, sums_off, counts_off, total;
+    size_t grp_sums_off, grp_counts_off, sums_off, counts_off, total;
 };
 
 Layout layout(int64_t n, int32_t M, int32_t K, uint32_t flags)
@@ -63,26 +66,22 @@ Layout layout(int64_t n, int32_t M, int32_t K, uint32_t flags)
     Layout L{};
     L.plan = plan_for(select_path(M, K, flags), n, M, K, kAssignAccum);
     const size_t km = (size_t)K * M;
-    L.tot_sums_off = align_up(sizeof(Ctl), 256);
-    L.tot_counts_off = align_up(L.tot_sums_off + km * sizeof(double), 256);
-    L.sums_off = align_up(L.tot_counts_off + (size_t)K * sizeof(int32_t), 256);
+    const size_t ng = (size_t)(L.plan.groups + kGroup - 1) / kGroup;
+    L.grp_sums_off = align_up(sizeof(Ctl), 256);
+    L.grp_counts_off = align_up(L.grp_sums_off + ng * km * sizeof(double), 256);
+    L.sums_off = align_up(L.grp_counts_off + ng * K * sizeof(int32_t), 256);
     L.counts_off = align_up(L.sums_off + (size_t)L.plan.groups * km * sizeof(double), 256);
     L.total = align_up(L.counts_off + (size_t)L.plan.groups * K * sizeof(int32_t), 256);
     return L;
 }
 
-FinalizeArgs finalize_args(const Layout &L, char *ws, int32_t K, int32_t M)
+void bind_workspace(StepArgs &a, const Layout &L, char *ws)
 {
-    FinalizeArgs f{};
-    f.part_sums = reinterpret_cast<const double *>(ws + L.sums_off);
-    f.part_counts = reinterpret_cast<const int32_t *>(ws + L.counts_off);
-    f.groups = L.plan.groups;
-    f.K = K;
-    f.M = M;
-    f.tot_sums = reinterpret_cast<double *>(ws + L.tot_sums_off);
-    f.tot_counts = reinterpret_cast<int32_t *>(ws + L.tot_counts_off);
-    f.ticket = &reinterpret_cast<Ctl *>(ws)->ticket;
-    return f;
+    a.part_sums = reinterpret_cast<double *>(ws + L.sums_off);
+    a.part_counts = reinterpret_cast<int32_t *>(ws + L.counts_off);
+    a.grp_sums = reinterpret_cast<double *>(ws + L.grp_sums_off);
+    a.grp_counts = reinterpret_cast<int32_t *>(ws + L.grp_counts_off);
+    a.ctl = reinterpret_cast<Ctl *>(ws);
 }
 
 int hip_status(hipError_t e) { return e == hipSuccess ? KMEANS_OK : KMEANS_EHIP; }
@@ -138,16 +137,16 @@ int kmeans_update(const float *X, int64_t n, int32_t M, const int32_t *labels, i
     const Layout L = layout(n, M, K, 0);
     if (!workspace || workspace_bytes < L.total) return KMEANS_EWORKSPACE;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    char *ws = static_cast<char *>(workspace);
     StepArgs a{};
     a.X = X; a.n = n; a.M = M; a.C = prev_centers; a.K = K;
     a.labels_in = labels;
-    a.part_sums = reinterpret_cast<double *>(ws + L.sums_off);
-    a.part_counts = reinterpret_cast<int32_t *>(ws + L.counts_off);
-    const FinalizeArgs f = finalize_args(L, ws, K, M);
-    if ((rc = hip_status(launch_ctl_reset(reinterpret_cast<Ctl *>(ws), s)))) return rc;
-    if ((rc = hip_status(launch_step(a, kAccumLabels, L.plan, s)))) return rc;
-    return hip_status(launch_finalize(f, prev_centers, centers, counts, nullptr, 0, 1, 0, s));
+    a.centers_out = centers;
+    a.counts_out = counts;
+    bind_workspace(a, L, static_cast<char *>(workspace));
+    a.fixed = 1;
+    a.compare = 0;
+    if ((rc = hip_status(launch_ctl_reset(a.ctl, s)))) return rc;
+    return hip_status(launch_step(a, kAccumLabels, L.plan, s));
 }
 
 int kmeans_run(const float *X, int64_t n, int32_t M, int32_t K, const float *init_centers,
@@ -166,19 +165,18 @@ int kmeans_run(const float *X, int64_t n, int32_t M, int32_t K, const float *ini
     if (!workspace || workspace_bytes < L.total) return KMEANS_EWORKSPACE;
 
     hipStream_t s = static_cast<hipStream_t>(stream);
-    char *ws = static_cast<char *>(workspace);
-    Ctl *ctl = reinterpret_cast<Ctl *>(ws);
     const int fixed = (flags & KMEANS_FIXED_ITERS) ? 1 : 0;
 
     StepArgs a{};
     a.X = X; a.n = n; a.M = M; a.C = centers; a.K = K;
     a.labels = labels;
-    a.part_sums = reinterpret_cast<double *>(ws + L.sums_off);
-    a.part_counts = reinterpret_cast<int32_t *>(ws + L.counts_off);
-    a.ctl = ctl;
+    a.centers_out = centers;     // centres are updated in place, iteration by iteration
+    a.counts_out = counts;
+    bind_workspace(a, L, static_cast<char *>(workspace));
     a.fixed = fixed;
+    a.compare = 1;
+    Ctl *ctl = a.ctl;
 
-    const FinalizeArgs f = finalize_args(L, ws, K, M);
     if ((rc = hip_status(launch_ctl_reset(ctl, s)))) return rc;
     if (init_centers != centers) {
         rc = hip_status(hipMemcpyAsync(centers, init_centers, sizeof(float) * (size_t)K * M,
@@ -198,6 +196,7 @@ int kmeans_run(const float *X, int64_t n, int32_t M, int32_t K, const float *ini
         for (hipEvent_t e : ev) (void)hipEventDestroy(e);
     };
 
+    // One launch per iteration (assign, accumulate, centres and compare fused).
     // Enqueue iterations in chunks; between chunks (early-stop mode only) read
     // the control block to learn whether the centres have become congruent.
     // Launches past convergence return at their first instruction.
@@ -210,9 +209,6 @@ int kmeans_run(const float *X, int64_t n, int32_t M, int32_t K, const float *ini
         for (int tt = t; tt <= end && !rc; ++tt) {
             a.t = tt;
             rc = hip_status(launch_step(a, kAssignAccum, L.plan, s));
-            if (!rc) rc = mark();
-            if (!rc)
-                rc = hip_status(launch_finalize(f, centers, centers, counts, ctl, tt, fixed, 1, s));
             if (!rc) rc = mark();
         }
         t = end + 1;
@@ -231,21 +227,17 @@ int kmeans_run(const float *X, int64_t n, int32_t M, int32_t K, const float *ini
     *iterations = host.converged_at != 0 ? host.converged_at : max_iter;
 
     if (timing) {
-        timing->assign_ms = timing->finalize_ms = 0.0;
-        timing->assign_launches = timing->finalize_launches = 0;
+        timing->step_ms = 0.0;
+        timing->step_launches = 0;
+        timing->reserved = 0;
         for (size_t e = 0; e + 1 < ev.size(); ++e) {
             float ms = 0.f;
             if (hipEventElapsedTime(&ms, ev[e], ev[e + 1]) != hipSuccess) {
                 rc = KMEANS_EHIP;
                 break;
             }
-            if (e % 2 == 0) {
-                timing->assign_ms += ms;
-                timing->assign_launches++;
-            } else {
-                timing->finalize_ms += ms;
-                timing->finalize_launches++;
-            }
+            timing->step_ms += ms;
+            timing->step_launches++;
         }
     }
     cleanup();

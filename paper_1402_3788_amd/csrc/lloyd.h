@@ -15,28 +15,32 @@ constexpr int kMaxLds = 160 * 1024;  // LDS bytes per workgroup on gfx950
 constexpr int kCUs = 256;            // compute units the launch geometry is sized for
 
 // Iteration control block, kept at the start of the caller's workspace.
-//   changed[t & 1] : set by the finalise launch of iteration t when any centre
-//                    coordinate differs bitwise from iteration t-1; cleared by
-//                    iteration t's assign launch before that.
+//   changed[t & 1] : written by the launch of iteration t (its last workgroup):
+//                    1 when any centre coordinate differs bitwise from t-1's.
 //   converged_at   : first t >= 2 whose centres were congruent with t-1's
-//                    (0 = not yet); written by the finalise launch of t+1.
+//                    (0 = not yet); written by the launch of iteration t+1.
 //   fallbacks      : objects whose label was re-decided in fp64 (diagnostic).
-//   ticket         : arrival counter of the finalise launch's workgroups.
+//   tickets        : arrival counters of the cross-workgroup reduction; zero
+//                    between launches.
 struct Ctl {
     int32_t changed[2];
     int32_t converged_at;
     int32_t fallbacks;
-    uint32_t ticket;
-    int32_t pad[59];
+    uint32_t tickets[32];
+    int32_t pad[28];
 };
 static_assert(sizeof(Ctl) == 256, "control block is one 256-byte slot");
 
-// Early exit of a launch that belongs to an iteration after convergence.
-__device__ inline bool stop_before(const Ctl *ctl, int t, int fixed)
+// Early exit of a launch that belongs to an iteration after convergence; the
+// first such launch records the iteration count.
+__device__ inline bool stop_before(Ctl *ctl, int t, int fixed)
 {
     if (ctl == nullptr || fixed) return false;
-    if (ctl->converged_at != 0) return true;
-    return (t - 1 >= 2) && ctl->changed[(t - 1) & 1] == 0;
+    const bool stop =
+        ctl->converged_at != 0 || ((t - 1 >= 2) && ctl->changed[(t - 1) & 1] == 0);
+    if (stop && blockIdx.x == 0 && threadIdx.x == 0 && ctl->converged_at == 0)
+        ctl->converged_at = t - 1;
+    return stop;
 }
 
 // What a launch of the distance kernels does with the assignment.
@@ -67,36 +71,25 @@ struct StepArgs {
     const float *X;
     int64_t n;
     int M;
-    const float *C;            // centres read by the assignment
+    const float *C;            // centres read by the assignment (previous centres)
     int K;
     int32_t *labels;           // out (modes 0/1)
     const int32_t *labels_in;  // in (mode 2)
     float *min_d2;             // optional out (mode 0)
     double *part_sums;         // [groups][K][M] (modes 1/2)
     int32_t *part_counts;      // [groups][K]
-    Ctl *ctl;                  // iteration control (mode 1 in a run), else null
-    int t;                     // iteration number (1-based) for the control block
+    double *grp_sums;          // [ceil(groups/16)][K][M]
+    int32_t *grp_counts;       // [ceil(groups/16)][K]
+    float *centers_out;        // new centres (may alias C)
+    int32_t *counts_out;       // [K]
+    Ctl *ctl;                  // control block (modes 1/2)
+    int t;                     // iteration number (1-based)
     int fixed;                 // no early stop
+    int compare;               // record the change flag of iteration t
 };
 
 hipError_t launch_valu(const StepArgs &a, Mode mode, const AccumPlan &plan, hipStream_t s);
 hipError_t launch_mfma(const StepArgs &a, Mode mode, const AccumPlan &plan, hipStream_t s);
-
-// Finalise: reduce the G per-workgroup partials in a fixed order into totals,
-// then (last workgroup) form the fp32 centres of Eq. (1), the counts, and the
-// change flag of iteration t.
-struct FinalizeArgs {
-    const double *part_sums;
-    const int32_t *part_counts;
-    int groups, K, M;
-    double *tot_sums;     // [K][M] scratch
-    int32_t *tot_counts;  // [K] scratch
-    uint32_t *ticket;     // zero before the launch; left zero after it
-};
-
-int finalize_blocks(int K, int M);
-hipError_t launch_finalize(const FinalizeArgs &f, const float *prev, float *centers,
-                           int32_t *counts, Ctl *ctl, int t, int fixed, int compare, hipStream_t s);
 
 hipError_t launch_ctl_reset(Ctl *ctl, hipStream_t s);
 

@@ -109,13 +109,14 @@ struct Slots {
     static constexpr int kTileFloats = (kWave * M + (M > 4 ? M : 4) + 3) / 4 * 4;
 };
 
+
 // Add the members of one 64-object tile into the wave's private fp64 slab
 // slab[k][0..M] (feature sums and the count of cluster k: the numerator and
 // denominator of Eq. (1)).
 //
 // lab is this lane's object label (-1: no object). tile holds the 64 objects'
-// features, object-major, followed by one row of zeros; ones[0..63] = 1 and
-// ones[64] = 0. For each cluster present in the tile a ballot lists its
+// features, object-major, followed by at least one row of zeros; ones[0..63] = 1
+// and ones[64] = 0. For each cluster present in the tile a ballot lists its
 // members; member m (in ascending lane order) goes to slot m % P, each slot
 // adds its members in order in fp64, the P slot sums are combined in a fixed
 // tree and added once to the slab. Absent members read the zero row, so the
@@ -126,8 +127,17 @@ __device__ inline void wave_accumulate(int lab, const float *tile, const float *
 {
     constexpr int MW = Slots<M>::MW, P = Slots<M>::P;
     const int s = lane / MW, j = lane - (lane / MW) * MW;
-    const float *base = (j < M) ? tile + j : ones;   // value of member p: base[p * stride]
-    const int stride = (j < M) ? M : 1;
+    // Value of member p for this lane: *(base + p * stride) (bytes). Lanes of
+    // slot u take the position p_u of their step; the per-slot strides are zero
+    // for the other slots, so the address is base + sum_u p_u * stride_u with
+    // one multiply-add per slot and no selects. Lanes outside every slot read
+    // row 0 and their sums are never used.
+    const char *base = (j < M) ? reinterpret_cast<const char *>(tile + j)
+                               : reinterpret_cast<const char *>(ones);
+    const uint32_t stride = (j < M) ? M * 4 : 4;
+    uint32_t st[P];
+#pragma unroll
+    for (int u = 0; u < P; ++u) st[u] = (s == u) ? stride : 0u;
     for (int k = 0; k < K; ++k) {
         uint64_t mask = __ballot(lab == k);
         if (mask == 0) continue;
@@ -135,21 +145,21 @@ __device__ inline void wave_accumulate(int lab, const float *tile, const float *
         const double old = (lane < MW) ? slab[k * MW + lane] : 0.0;
         double acc = 0.0;
         do {
-            int pa = kWave, pb = kWave;
+            uint32_t offa = 0, offb = 0;
 #pragma unroll
-            for (int u = 0; u < P; ++u) {
-                const int p = mask ? (int)__builtin_ctzll(mask) : kWave;
-                mask &= mask - 1;
-                pa = (s == u) ? p : pa;
+            for (int u = 0; u < P; ++u) {          // positions off the mask, in order
+                const uint32_t p = mask ? (uint32_t)__builtin_ctzll(mask) : (uint32_t)kWave;
+                mask &= ~(1ull << (p & 63));
+                offa += p * st[u];
             }
 #pragma unroll
             for (int u = 0; u < P; ++u) {
-                const int p = mask ? (int)__builtin_ctzll(mask) : kWave;
-                mask &= mask - 1;
-                pb = (s == u) ? p : pb;
+                const uint32_t p = mask ? (uint32_t)__builtin_ctzll(mask) : (uint32_t)kWave;
+                mask &= ~(1ull << (p & 63));
+                offb += p * st[u];
             }
-            const float va = base[pa * stride];
-            const float vb = base[pb * stride];
+            const float va = *reinterpret_cast<const float *>(base + offa);
+            const float vb = *reinterpret_cast<const float *>(base + offb);
             acc = acc + (double)va;
             acc = acc + (double)vb;
         } while (mask);

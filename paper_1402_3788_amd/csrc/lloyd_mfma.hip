@@ -33,11 +33,14 @@
 //              adds them. Used for large K*M.
 #include "lloyd.h"
 #include "lloyd_device.h"
+#include "lloyd_reduce.h"
 
 #include <math.h>
 
 #include <array>
 #include <utility>
+
+#include "lloyd_parts.h"
 
 namespace lloyd {
 
@@ -87,7 +90,8 @@ __global__ void __launch_bounds__(kMaxWaves * kWave)
 lloyd_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict__ C, int K,
                   int32_t *__restrict__ labels, const int32_t *__restrict__ labels_in,
                   float *__restrict__ min_d2, double *__restrict__ part_sums,
-                  int32_t *__restrict__ part_counts, Ctl *__restrict__ ctl, int t, int fixed)
+                  int32_t *__restrict__ part_counts, Ctl *__restrict__ ctl, int t, int fixed,
+                  TreeArgs tree)
 {
     using TG = TileGeom<M>;
     constexpr int KS = (M + 3) / 4;
@@ -101,10 +105,7 @@ lloyd_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restric
     const int tid = threadIdx.x;
     const int KT = (K + 15) / 16;
 
-    if (MODE == kAssignAccum) {
-        if (stop_before(ctl, t, fixed)) return;
-        if (ctl != nullptr && blockIdx.x == 0 && tid == 0) ctl->changed[t & 1] = 0;
-    }
+    if (MODE == kAssignAccum && stop_before(ctl, t, fixed)) return;
 
     const MfmaLds L = mfma_lds(M, K, W, kAcc);
     float *ones = reinterpret_cast<float *>(smem + L.ones);
@@ -248,7 +249,9 @@ lloyd_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restric
                         lb[c] = lt ? kb + r : lb[c];
                     }
             }
-            // merge the four lanes that hold the same object
+            // merge the four lanes that hold the same object (no branches: the
+            // second best of two (best, second) pairs is the median of
+            // (b1, pb1, min(b2, pb2)) when b1 <= b2 and pb1 <= pb2)
 #pragma unroll
             for (int c = 0; c < kCols; ++c)
 #pragma unroll
@@ -256,8 +259,9 @@ lloyd_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restric
                     const float pb1 = __shfl_xor(b1[c], off, kWave);
                     const float pb2 = __shfl_xor(b2[c], off, kWave);
                     const int pl = __shfl_xor(lb[c], off, kWave);
-                    const float nb2 = fminf(fminf(b2[c], pb2), fmaxf(b1[c], pb1));
-                    const bool take = pb1 < b1[c] || (pb1 == b1[c] && pl < lb[c]);
+                    const float m2 = __builtin_amdgcn_fmed3f(b2[c], pb2, -INFINITY);
+                    const float nb2 = __builtin_amdgcn_fmed3f(b1[c], pb1, m2);
+                    const bool take = (pb1 < b1[c]) | ((pb1 == b1[c]) & (pl < lb[c]));
                     b1[c] = take ? pb1 : b1[c];
                     lb[c] = take ? pl : lb[c];
                     b2[c] = nb2;
@@ -372,16 +376,38 @@ lloyd_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restric
         for (int e = tid; e < K * M; e += blockDim.x) out[e] = slab[e];
         for (int k = tid; k < K; k += blockDim.x) part_counts[(int64_t)blockIdx.x * K + k] = cnt[k];
     }
+    if (kAccum) tree_finalize(tree, reinterpret_cast<uint32_t *>(smem + L.slab));
+}
+
+TreeArgs tree_args(const StepArgs &a, int groups)
+{
+    TreeArgs r{};
+    r.part_sums = a.part_sums;
+    r.part_counts = a.part_counts;
+    r.grp_sums = a.grp_sums;
+    r.grp_counts = a.grp_counts;
+    r.tickets = a.ctl != nullptr ? a.ctl->tickets : nullptr;
+    r.G = groups;
+    r.K = a.K;
+    r.M = a.M;
+    r.prev = a.C;
+    r.centers = a.centers_out;
+    r.counts = a.counts_out;
+    r.ctl = a.ctl;
+    r.t = a.t;
+    r.compare = a.compare;
+    return r;
 }
 
 template <int M>
 hipError_t launch_m(const StepArgs &a, Mode mode, const AccumPlan &p, hipStream_t s)
 {
     const dim3 grid(p.groups), block(p.waves * kWave);
+    const TreeArgs tr = tree_args(a, p.groups);
 #define LLOYD_MFMA_LAUNCH(MD, AC)                                                              \
     hipLaunchKernelGGL((lloyd_mfma_kernel<M, MD, AC>), grid, block, p.lds_bytes, s, a.X, a.n,   \
                        a.C, a.K, a.labels, a.labels_in, a.min_d2, a.part_sums, a.part_counts,  \
-                       a.ctl, a.t, a.fixed)
+                       a.ctl, a.t, a.fixed, tr)
     const bool wave_acc = p.accum == kAccWave;
     switch (mode) {
     case kAssign: LLOYD_MFMA_LAUNCH(kAssign, kAccWave); break;
@@ -400,14 +426,27 @@ hipError_t launch_m(const StepArgs &a, Mode mode, const AccumPlan &p, hipStream_
 
 using LaunchFn = hipError_t (*)(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
 
+// This translation unit instantiates the kernels for the feature counts of
+// one part of [1, kMaxM] (the build compiles it once per part, in parallel).
+constexpr int kPartLo = LLOYD_PART * kMaxM / LLOYD_PARTS + 1;
+constexpr int kPartN = kMaxM / LLOYD_PARTS;
+
 template <int... Is>
 constexpr auto make_table(std::integer_sequence<int, Is...>)
 {
-    return std::array<LaunchFn, sizeof...(Is)>{&launch_m<Is + 1>...};
+    return std::array<LaunchFn, sizeof...(Is)>{&launch_m<kPartLo + Is>...};
 }
 
 }  // namespace
 
+hipError_t LLOYD_PART_FN(launch_mfma_part)(const StepArgs &a, Mode mode, const AccumPlan &plan, hipStream_t s)
+{
+    static constexpr auto table = make_table(std::make_integer_sequence<int, kPartN>{});
+    if (a.M < kPartLo || a.M >= kPartLo + kPartN) return hipErrorInvalidValue;
+    return table[a.M - kPartLo](a, mode, plan, s);
+}
+
+#if LLOYD_PART == 0
 AccumPlan plan_mfma(int64_t n, int M, int K, Mode mode)
 {
     AccumPlan p{};
@@ -420,7 +459,7 @@ AccumPlan plan_mfma(int64_t n, int M, int K, Mode mode)
     } else {
         // private slabs while at least 8 waves fit, else one shared slab
         acc = kAccWave;
-        while (W > 8 && !fits(W, kAccWave)) W /= 2;
+        while (W > 8 && !fits(W, kAccWave)) --W;
         if (!fits(W, kAccWave)) {
             acc = kAccBlock;
             W = kMaxWaves;
@@ -445,9 +484,14 @@ bool mfma_fits(int M, int K)
 
 hipError_t launch_mfma(const StepArgs &a, Mode mode, const AccumPlan &plan, hipStream_t s)
 {
-    static constexpr auto table = make_table(std::make_integer_sequence<int, kMaxM>{});
     if (a.M < 1 || a.M > kMaxM) return hipErrorInvalidValue;
-    return table[a.M - 1](a, mode, plan, s);
+    switch ((a.M - 1) / (kMaxM / LLOYD_PARTS)) {
+#define LLOYD_CASE(P) case P: return launch_mfma_part_##P(a, mode, plan, s);
+        LLOYD_PART_CASES
+#undef LLOYD_CASE
+    }
+    return hipErrorInvalidValue;
 }
+#endif
 
 }  // namespace lloyd

@@ -21,8 +21,14 @@
 //      one fp64 partial per (cluster, feature) plus one count per cluster.
 #include "lloyd.h"
 #include "lloyd_device.h"
+#include "lloyd_reduce.h"
 
 #include <math.h>
+
+#include <array>
+#include <utility>
+
+#include "lloyd_parts.h"
 
 namespace lloyd {
 
@@ -33,7 +39,8 @@ __global__ void __launch_bounds__(1024)
 lloyd_valu_kernel(const float *__restrict__ X, int64_t n, const float *__restrict__ C, int K,
                   int32_t *__restrict__ labels, const int32_t *__restrict__ labels_in,
                   float *__restrict__ min_d2, double *__restrict__ part_sums,
-                  int32_t *__restrict__ part_counts, Ctl *__restrict__ ctl, int t, int fixed)
+                  int32_t *__restrict__ part_counts, Ctl *__restrict__ ctl, int t, int fixed,
+                  TreeArgs tree)
 {
     using G = TileGeom<M>;
     extern __shared__ __align__(16) unsigned char smem[];
@@ -41,18 +48,15 @@ lloyd_valu_kernel(const float *__restrict__ X, int64_t n, const float *__restric
     const int wave = threadIdx.x / kWave;
     const int lane = threadIdx.x % kWave;
 
-    if (MODE == kAssignAccum) {
-        if (stop_before(ctl, t, fixed)) return;
-        if (ctl != nullptr && blockIdx.x == 0 && threadIdx.x == 0) ctl->changed[t & 1] = 0;
-    }
+    if (MODE == kAssignAccum && stop_before(ctl, t, fixed)) return;
 
     using S = Slots<M>;
     constexpr int MW = S::MW;
     // LDS: [ones: 68 floats] [W tiles of kTileFloats] [W slabs of K*(M+1) fp64]
     float *ones = reinterpret_cast<float *>(smem);
     float *tile = ones + 68 + wave * S::kTileFloats;
-    double *slab = reinterpret_cast<double *>(smem + (68 + (size_t)W * S::kTileFloats) * 4) +
-                   (size_t)wave * K * MW;
+    const size_t slab_off = (68 + (size_t)W * S::kTileFloats) * 4;
+    double *slab = reinterpret_cast<double *>(smem + slab_off) + (size_t)wave * K * MW;
     for (int i = lane; i < S::kTileFloats - kWave * M; i += kWave) tile[kWave * M + i] = 0.f;
     if (MODE != kAssign) {
         for (int i = lane; i < K * MW; i += kWave) slab[i] = 0.0;
@@ -143,8 +147,7 @@ lloyd_valu_kernel(const float *__restrict__ X, int64_t n, const float *__restric
 
     if (MODE != kAssign) {
         __syncthreads();
-        const double *slabs =
-            reinterpret_cast<const double *>(smem + (68 + (size_t)W * S::kTileFloats) * 4);
+        const double *slabs = reinterpret_cast<const double *>(smem + slab_off);
         double *out = part_sums + (int64_t)blockIdx.x * K * M;
         for (int e = threadIdx.x; e < K * M; e += blockDim.x) {
             const int k = e / M, j = e - (e / M) * M;
@@ -157,56 +160,81 @@ lloyd_valu_kernel(const float *__restrict__ X, int64_t n, const float *__restric
             for (int w = 0; w < W; ++w) c = c + slabs[(size_t)w * K * MW + k * MW + M];
             part_counts[(int64_t)blockIdx.x * K + k] = (int32_t)c;
         }
+        tree_finalize(tree, reinterpret_cast<uint32_t *>(const_cast<double *>(slabs)));
     }
+}
+
+TreeArgs tree_args(const StepArgs &a, int groups)
+{
+    TreeArgs r{};
+    r.part_sums = a.part_sums;
+    r.part_counts = a.part_counts;
+    r.grp_sums = a.grp_sums;
+    r.grp_counts = a.grp_counts;
+    r.tickets = a.ctl != nullptr ? a.ctl->tickets : nullptr;
+    r.G = groups;
+    r.K = a.K;
+    r.M = a.M;
+    r.prev = a.C;
+    r.centers = a.centers_out;
+    r.counts = a.counts_out;
+    r.ctl = a.ctl;
+    r.t = a.t;
+    r.compare = a.compare;
+    return r;
 }
 
 template <int M>
 hipError_t launch_m(const StepArgs &a, Mode mode, const AccumPlan &p, hipStream_t s)
 {
     const dim3 grid(p.groups), block(p.waves * kWave);
+    const TreeArgs tr = tree_args(a, p.groups);
+#define LLOYD_VALU_LAUNCH(MD)                                                                  \
+    hipLaunchKernelGGL((lloyd_valu_kernel<M, MD>), grid, block, p.lds_bytes, s, a.X, a.n, a.C,  \
+                       a.K, a.labels, a.labels_in, a.min_d2, a.part_sums, a.part_counts, a.ctl, \
+                       a.t, a.fixed, tr)
     switch (mode) {
-    case kAssign:
-        hipLaunchKernelGGL((lloyd_valu_kernel<M, kAssign>), grid, block, p.lds_bytes, s, a.X,
-                           a.n, a.C, a.K, a.labels, a.labels_in, a.min_d2, a.part_sums,
-                           a.part_counts, a.ctl, a.t, a.fixed);
-        break;
-    case kAssignAccum:
-        hipLaunchKernelGGL((lloyd_valu_kernel<M, kAssignAccum>), grid, block, p.lds_bytes, s,
-                           a.X, a.n, a.C, a.K, a.labels, a.labels_in, a.min_d2, a.part_sums,
-                           a.part_counts, a.ctl, a.t, a.fixed);
-        break;
-    case kAccumLabels:
-        hipLaunchKernelGGL((lloyd_valu_kernel<M, kAccumLabels>), grid, block, p.lds_bytes, s,
-                           a.X, a.n, a.C, a.K, a.labels, a.labels_in, a.min_d2, a.part_sums,
-                           a.part_counts, a.ctl, a.t, a.fixed);
-        break;
+    case kAssign: LLOYD_VALU_LAUNCH(kAssign); break;
+    case kAssignAccum: LLOYD_VALU_LAUNCH(kAssignAccum); break;
+    case kAccumLabels: LLOYD_VALU_LAUNCH(kAccumLabels); break;
     }
+#undef LLOYD_VALU_LAUNCH
     return hipGetLastError();
 }
 
 using LaunchFn = hipError_t (*)(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
 
-template <int... Ms>
-struct LaunchTable {
-    static constexpr LaunchFn fns[sizeof...(Ms)] = {&launch_m<Ms + 1>...};
-};
+// This translation unit instantiates the kernels for the feature counts of
+// one part of [1, kMaxM] (the build compiles it once per part, in parallel).
+constexpr int kPartLo = LLOYD_PART * kMaxM / LLOYD_PARTS + 1;
+constexpr int kPartN = kMaxM / LLOYD_PARTS;
 
 template <int... Is>
 constexpr auto make_table(std::integer_sequence<int, Is...>)
 {
-    return LaunchTable<Is...>{};
+    return std::array<LaunchFn, sizeof...(Is)>{&launch_m<kPartLo + Is>...};
 }
 
 }  // namespace
 
+hipError_t LLOYD_PART_FN(launch_valu_part)(const StepArgs &a, Mode mode, const AccumPlan &plan,
+                                           hipStream_t s)
+{
+    static constexpr auto table = make_table(std::make_integer_sequence<int, kPartN>{});
+    if (a.M < kPartLo || a.M >= kPartLo + kPartN) return hipErrorInvalidValue;
+    return table[a.M - kPartLo](a, mode, plan, s);
+}
+
+#if LLOYD_PART == 0
 AccumPlan plan_valu(int64_t n, int M, int K, Mode mode)
 {
     AccumPlan p{};
     p.path = kPathValu;
     const size_t tile = (size_t)((kWave * M + (M > 4 ? M : 4) + 3) / 4 * 4) * 4;
-    const size_t per_wave = tile + (mode == kAssign ? 0 : (size_t)K * (M + 1) * 8);
+    const size_t per_wave =
+        tile + (mode == kAssign ? 0 : (size_t)K * (M + 1) * 8);
     int W = 16;
-    while (W > 1 && 68 * 4 + (size_t)W * per_wave > (size_t)kMaxLds) W /= 2;
+    while (W > 1 && 68 * 4 + (size_t)W * per_wave > (size_t)kMaxLds) W -= (W > 8 ? 1 : W / 2);
     const int64_t nq = (n + kWave - 1) / kWave;
     while (W > 1 && W / 2 >= nq) W /= 2;
     int64_t groups = (nq + W - 1) / W;
@@ -220,9 +248,14 @@ AccumPlan plan_valu(int64_t n, int M, int K, Mode mode)
 
 hipError_t launch_valu(const StepArgs &a, Mode mode, const AccumPlan &plan, hipStream_t s)
 {
-    static constexpr auto table = make_table(std::make_integer_sequence<int, kMaxM>{});
     if (a.M < 1 || a.M > kMaxM) return hipErrorInvalidValue;
-    return decltype(table)::fns[a.M - 1](a, mode, plan, s);
+    switch ((a.M - 1) / (kMaxM / LLOYD_PARTS)) {
+#define LLOYD_CASE(P) case P: return launch_valu_part_##P(a, mode, plan, s);
+        LLOYD_PART_CASES
+#undef LLOYD_CASE
+    }
+    return hipErrorInvalidValue;
 }
+#endif
 
 }  // namespace lloyd
