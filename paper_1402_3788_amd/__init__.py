@@ -3,7 +3,7 @@
 Thin ctypes marshalling over libkmeans_mi355x.so (C ABI in include/kmeans.h).
 Tensors are PyTorch device tensors; every step of the computation runs in the
 library's HIP kernels. Importing this module fails loudly if the library has
-not been built (python -m paper_1402_3788_amd.build).
+not been built (python paper_1402_3788_amd/build.py).
 
 Entry points (same names as the C ABI):
     kmeans_assign(X, centers, with_min_d2=False, path=None) -> labels [, min_d2]
@@ -49,7 +49,7 @@ class KmeansError(RuntimeError):
 
 def _load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_1402_3788_amd.build`")
+        raise ImportError(f"{LIB_PATH} is not built; run `python paper_1402_3788_amd/build.py`")
     lib = ctypes.CDLL(LIB_PATH)
     p, i64, i32, u32, sz = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32,
                             ctypes.c_size_t)

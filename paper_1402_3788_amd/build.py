@@ -1,6 +1,7 @@
 """Build libkmeans_mi355x.so (the HIP library behind include/kmeans.h) in-tree.
 
-Usage: python -m paper_1402_3788_amd.build
+Usage: python paper_1402_3788_amd/build.py
+(run as a script: importing the package needs the library this builds)
 """
 from __future__ import annotations
 
