@@ -3,15 +3,15 @@
 A step is one Lloyd iteration of Algorithm 1 over the whole point set: one
 launch that assigns every object (steps 2/4), accumulates the sums of Eq. (1),
 forms the new centres and compares them with the previous ones (steps 6/7).
-The default
-workload is the paper's largest size: n = 2,000,000 objects, M = 25 features,
-K = 16 clusters (anisotropic Gaussian blobs, seed 2, farthest-point initial
-centres). Iterations run in fixed-count mode so every timed step does the full
-work (this workload converges after 2 passes; the passes after that repeat the
-same labels and centres).
+The default workload is the paper's largest size: n = 2,000,000 objects,
+M = 25 features, K = 16 clusters (anisotropic Gaussian blobs, seed 2,
+farthest-point initial centres). Iterations run in fixed-count mode so every
+timed step does the full work (this workload converges after 2 passes; the
+passes after that repeat the same labels and centres). X is resident in device
+memory before the timed region starts.
 
 python bench.py [--gpus 1] [--steps 1000] [--warmup 20] [--workload 3]
-                [--no-cpu-baseline] [--no-control] [--path direct|mfma]
+                [--path auto|direct|mfma|tiles] [--no-cpu-baseline] [--no-control]
 python bench.py --calibrate-copy   # plain device copy of known size (PMC scaling)
 
 Prints ONE JSON line.
@@ -31,13 +31,18 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, vendor peak
 PROFILES = os.path.join(ROOT, "profiles")
-KERNEL_SOURCES = {
-    "direct": os.path.join(ROOT, "paper_1402_3788_amd", "csrc", "lloyd_valu.hip"),
-    "mfma": os.path.join(ROOT, "paper_1402_3788_amd", "csrc", "lloyd_mfma.hip"),
-}
-KERNEL_NAMES = {
-    "direct": "lloyd_valu_kernel<M, assign+accumulate>",
-    "mfma": "lloyd_mfma_kernel<M, assign+accumulate>",
+CSRC = os.path.join(ROOT, "paper_1402_3788_amd", "csrc")
+METRIC = "Lloyd iters/sec and points·iters/sec at n=2e6,M=25,K=16; % of HBM peak"
+
+# kernel that does the work of a step on each distance path, and the sources
+# it is built from (a committed counter summary is used only while they match)
+KERNELS = {
+    "lane-mfma": ("lloyd_lane_kernel<M, assign+accumulate, dist=mfma 4x4x1>",
+                  ["lloyd_lane.hip", "lloyd_device.h", "lloyd_reduce.h", "lloyd.h"]),
+    "direct": ("lloyd_lane_kernel<M, assign+accumulate, dist=valu>",
+               ["lloyd_lane.hip", "lloyd_device.h", "lloyd_reduce.h", "lloyd.h"]),
+    "tiles": ("lloyd_tile_kernel<M, assign+accumulate, acc>",
+              ["lloyd_tile.hip", "lloyd_device.h", "lloyd_reduce.h", "lloyd.h"]),
 }
 
 
@@ -47,29 +52,46 @@ def _parse():
     ap.add_argument("--steps", type=int, default=1000)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="3")
-    ap.add_argument("--path", default=None)
+    ap.add_argument("--path", default="auto", choices=["auto", "direct", "mfma", "tiles"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-control", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true")
     return ap.parse_args()
 
 
-def _sha(path):
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+def kernel_key(M: int, K: int, path: str) -> str:
+    """Which kernel runs the iteration (mirrors the library's path choice)."""
+    lane_fits = K <= 16 and M <= 27
+    if path == "direct":
+        return "direct"
+    if path == "tiles":
+        return "tiles"
+    if path == "mfma":
+        return "lane-mfma" if lane_fits else "tiles"
+    if K > 16:
+        return "tiles"
+    return "lane-mfma" if (lane_fits and K >= 5) else "direct"
 
 
-def _traffic(kernel_key: str, workload: str, n_launch_bytes: float):
-    """HBM traffic per launch from the committed PMC summary, if it was taken on
-    the current kernel source; else None."""
-    path = os.path.join(PROFILES, f"pmc_{kernel_key}_{workload}.md")
+def sources_sha256(key: str) -> str:
+    h = hashlib.sha256()
+    for name in KERNELS[key][1]:
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def _traffic(key: str, workload: str):
+    """HBM bytes per launch from the committed counter summary for this kernel
+    and workload, if it was taken on the current sources; else None."""
+    path = os.path.join(PROFILES, f"pmc_{key}_{workload}.md")
     if not os.path.exists(path):
         return None
     m = re.search(r"```json\n(.*?)\n```", open(path).read(), re.S)
     if not m:
         return None
     d = json.loads(m.group(1))
-    if d.get("kernel_src_sha256") != _sha(KERNEL_SOURCES[kernel_key]):
+    if d.get("sources_sha256") != sources_sha256(key):
         return None
     return d.get("hbm_bytes_per_launch")
 
@@ -125,19 +147,23 @@ def main():
     Xg = torch.from_numpy(X).to(dev)
     Cg = torch.from_numpy(init).to(dev)
     n, M, K = w.n, w.M, w.K
+    path = None if args.path == "auto" else args.path
+    key = kernel_key(M, K, args.path)
+    flags = km._flags(path) | km.KMEANS_FIXED_ITERS
     out = (torch.empty(n, dtype=torch.int32, device=dev),
            torch.empty((K, M), dtype=torch.float32, device=dev),
            torch.empty(K, dtype=torch.int32, device=dev))
-    ws = km.workspace(n, M, K, dev)
+    ws = km.workspace(n, M, K, dev, flags)
 
     # warmup
-    km.kmeans_run(Xg, K, Cg, max(1, args.warmup), fixed_iters=True, path=args.path, out=out, ws=ws)
+    km.kmeans_run(Xg, K, Cg, max(1, args.warmup), fixed_iters=True, path=path, out=out, ws=ws)
     torch.cuda.synchronize()
 
-    # timed region: exactly `steps` Lloyd iterations in one fixed-count run
+    # timed region: exactly `steps` Lloyd iterations in one fixed-count run;
+    # the library records a HIP event on the launch stream after every launch
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    _, _, _, iters, tm = km.kmeans_run(Xg, K, Cg, args.steps, fixed_iters=True, path=args.path,
+    _, _, _, iters, tm = km.kmeans_run(Xg, K, Cg, args.steps, fixed_iters=True, path=path,
                                        timing=True, out=out, ws=ws)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
@@ -148,11 +174,10 @@ def main():
     launch_bytes = n * bytes_per_point
     step_avg_s = tm.step_ms / 1e3 / tm.step_launches
     achieved = launch_bytes / step_avg_s / 1e9
-    kernel_key = args.path or ("mfma" if K >= 16 else "direct")
-    traffic = _traffic(kernel_key, w.name, launch_bytes)
+    traffic = _traffic(key, w.name)
 
     result = {
-        "metric": "Lloyd iters/sec at n=2e6,M=25,K=16 (also points*iters/sec, % of HBM peak)",
+        "metric": METRIC,
         "value": round(iters_per_s, 2),
         "unit": "iters/s",
         "n_gpus": 1,
@@ -165,7 +190,7 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": w.name, "n": n, "M": M, "K": K, "mode": "fixed iterations",
-                   "accumulation": "f64", "path": args.path or "auto"},
+                   "accumulation": "f64", "path": args.path},
         "points_iters_per_s": round(iters_per_s * n, 1),
         "algorithmic_GBps_whole_step": round(launch_bytes * iters_per_s / 1e9, 1),
         "pct_hbm_peak_whole_step": round(100 * launch_bytes * iters_per_s / 1e9 / HBM_PEAK_GBPS, 2),
@@ -177,7 +202,7 @@ def main():
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
             "traffic": traffic,
-            "kernel": KERNEL_NAMES[kernel_key].replace("<M,", f"<{M},"),
+            "kernel": KERNELS[key][0].replace("<M,", f"<{M},"),
             "bytes_per_launch": launch_bytes,
         },
     }
@@ -188,8 +213,8 @@ def main():
         nc = 8_000_000
         Xc = torch.from_numpy(rng.uniform(-50, 50, (nc, M)).astype(np.float32)).to(dev)
         Cc = Xc[:K].clone()
-        km.kmeans_run(Xc, K, Cc, 5, fixed_iters=True, path=args.path)
-        _, _, _, _, tmc = km.kmeans_run(Xc, K, Cc, 50, fixed_iters=True, path=args.path,
+        km.kmeans_run(Xc, K, Cc, 5, fixed_iters=True, path=path)
+        _, _, _, _, tmc = km.kmeans_run(Xc, K, Cc, 50, fixed_iters=True, path=path,
                                         timing=True)
         avg = tmc.step_ms / 1e3 / tmc.step_launches
         result["control_n8m_uniform"] = {
@@ -213,7 +238,8 @@ def main():
             "unit": "iters/s",
             "cores": 1,
             "kind": "oracle",
-            "sample": f"{T} fixed Lloyd iterations over all {n} objects (single-threaded C, fp64)",
+            "sample": f"{T} fixed Lloyd iterations over all {n} objects of the same workload "
+                      "(single-threaded C, fp64)",
         }
     print(json.dumps(result), flush=True)
 

@@ -53,11 +53,14 @@ extern "C" {
 /* Flags (bitwise OR). */
 #define KMEANS_FIXED_ITERS  (1u << 0) /* kmeans_run: run exactly max_iter iterations, no early stop */
 #define KMEANS_PATH_DIRECT  (1u << 1) /* force the vector-ALU distance path                          */
-#define KMEANS_PATH_MFMA    (1u << 2) /* force the matrix-core (expanded-form) distance path;         */
-                                      /* KMEANS_EUNSUPPORTED when its per-workgroup state (centre     */
-                                      /* operands, fp64 sums) does not fit in LDS for this K and M    */
-/* Without a path flag the matrix-core path is used for K >= 16 where it fits,
- * the vector-ALU path otherwise. Both give the same labels, centres and counts. */
+#define KMEANS_PATH_MFMA    (1u << 2) /* force a matrix-core (expanded-form) distance path: one      */
+                                      /* object per lane for K <= 16 and M <= 27, else 64-object      */
+                                      /* tiles; KMEANS_EUNSUPPORTED when the tiles' per-workgroup     */
+                                      /* state (centre operands, fp64 sums) does not fit in LDS       */
+#define KMEANS_PATH_TILES   (1u << 3) /* force the 64-object-tile matrix-core path (any K)           */
+/* Without a path flag: 64-object tiles on the matrix cores for K > 16, one
+ * object per lane on the matrix cores for 5 <= K <= 16 (M <= 27), the vector
+ * ALU otherwise. Every path gives the same labels, centres and counts. */
 
 /* Optional per-call timing, filled by kmeans_run when a non-NULL pointer is
  * passed: device time of the per-iteration launches (each one assigns,

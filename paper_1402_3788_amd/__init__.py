@@ -31,6 +31,7 @@ KMEANS_EHIP = -4
 KMEANS_FIXED_ITERS = 1 << 0
 KMEANS_PATH_DIRECT = 1 << 1
 KMEANS_PATH_MFMA = 1 << 2
+KMEANS_PATH_TILES = 1 << 3
 
 EXPORTED = ("kmeans_workspace_bytes", "kmeans_strerror", "kmeans_assign", "kmeans_update",
             "kmeans_run")
@@ -102,6 +103,8 @@ def _flags(path):
         return KMEANS_PATH_DIRECT
     if path == "mfma":
         return KMEANS_PATH_MFMA
+    if path == "tiles":
+        return KMEANS_PATH_TILES
     raise ValueError(f"unknown path {path!r}")
 
 

@@ -10,7 +10,8 @@ using namespace lloyd;
 
 namespace {
 
-constexpr uint32_t kKnownFlags = KMEANS_FIXED_ITERS | KMEANS_PATH_DIRECT | KMEANS_PATH_MFMA;
+constexpr uint32_t kKnownFlags =
+    KMEANS_FIXED_ITERS | KMEANS_PATH_DIRECT | KMEANS_PATH_MFMA | KMEANS_PATH_TILES;
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
@@ -25,31 +26,40 @@ int check_shape(int64_t n, int32_t M, int32_t K)
 int check_flags(uint32_t flags)
 {
     if (flags & ~kKnownFlags) return KMEANS_EINVAL;
-    if ((flags & KMEANS_PATH_DIRECT) && (flags & KMEANS_PATH_MFMA)) return KMEANS_EINVAL;
+    const uint32_t paths = flags & (KMEANS_PATH_DIRECT | KMEANS_PATH_MFMA | KMEANS_PATH_TILES);
+    if (paths & (paths - 1)) return KMEANS_EINVAL;          // at most one path flag
     return KMEANS_OK;
 }
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-// Distance path: forced by a flag, else the matrix cores from K >= 16 on (one
-// full 16-centre tile) when their workgroup state fits in LDS, else the vector
-// ALU. Returns -1 when a forced matrix-core path does not fit.
+// Distance path. KMEANS_PATH_DIRECT: the vector ALU. KMEANS_PATH_TILES: the
+// 64-object tiles (-1 when their workgroup state does not fit in LDS).
+// KMEANS_PATH_MFMA: the
+// matrix cores, one object per lane when the centre operands fit in registers
+// (K <= 16, M <= 27), else 64-object tiles when their workgroup state fits in
+// LDS, else -1 (refused). No flag: tiles for K > 16, one object per lane on the
+// matrix cores for 5 <= K <= 16, the vector ALU otherwise (and wherever the
+// matrix-core forms do not fit).
 int select_path(int32_t M, int32_t K, uint32_t flags)
 {
     if (flags & KMEANS_PATH_DIRECT) return kPathValu;
-    const bool fits = mfma_fits(M, K);
-    if (flags & KMEANS_PATH_MFMA) return fits ? kPathMfma : -1;
-    return (K >= 16 && fits) ? kPathMfma : kPathValu;
+    const bool lane = lane_mfma_fits(M, K), tile = tile_fits(M, K);
+    if (flags & KMEANS_PATH_TILES) return tile ? kPathTile : -1;
+    if (flags & KMEANS_PATH_MFMA) return lane ? kPathLaneMfma : tile ? kPathTile : -1;
+    if (K > 16) return tile ? kPathTile : kPathValu;
+    return (lane && K >= 5) ? kPathLaneMfma : kPathValu;
 }
 
 AccumPlan plan_for(int p, int64_t n, int32_t M, int32_t K, Mode mode)
 {
-    return p == kPathMfma ? plan_mfma(n, M, K, mode) : plan_valu(n, M, K, mode);
+    if (p == kPathTile) return plan_tile(n, M, K, mode);
+    return plan_lane(n, M, K, mode, p == kPathLaneMfma);
 }
 
 hipError_t launch_step(const StepArgs &a, Mode mode, const AccumPlan &plan, hipStream_t s)
 {
-    return plan.path == kPathMfma ? launch_mfma(a, mode, plan, s) : launch_valu(a, mode, plan, s);
+    return plan.path == kPathTile ? launch_tile(a, mode, plan, s) : launch_lane(a, mode, plan, s);
 }
 
 // Workspace: [Ctl (256 B)] [fp64 group partials NG*K*M] [int32 group counts NG*K]

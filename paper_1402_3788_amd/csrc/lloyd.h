@@ -50,22 +50,39 @@ enum Mode : int {
     kAccumLabels = 2,   // partial sums/counts from caller-provided labels
 };
 
-enum Path : int { kPathValu = 0, kPathMfma = 1 };
+// Distance paths: one object per lane with the direct form on the vector ALU
+// (lloyd_lane.hip), one object per lane with 4x4x1 matrix-core blocks (same
+// kernel, K <= 16), or 64-object tiles with 16x16x4 matrix-core blocks
+// (lloyd_tile.hip, any K).
+enum Path : int { kPathValu = 0, kPathTile = 1, kPathLaneMfma = 2 };
+
+// Static LDS of a kernel (bytes), from the runtime's attributes; SIZE_MAX when
+// they cannot be read. Launches check static + dynamic LDS against kMaxLds, so
+// a plan that would not fit is refused on the host instead of dispatched.
+inline size_t static_lds_bytes(const void *kernel)
+{
+    hipFuncAttributes attr{};
+    if (hipFuncGetAttributes(&attr, kernel) != hipSuccess) return SIZE_MAX;
+    return attr.sharedSizeBytes;
+}
 
 struct AccumPlan {
     Path path;
     int waves;          // wavefronts per workgroup
     int groups;         // workgroups (persistent, strided over 64-object tiles)
-    int accum;          // accumulation form of the matrix-core kernel (1 wave, 2 block)
+    int accum;          // accumulation form (kernel-specific code)
     size_t lds_bytes;   // dynamic LDS per workgroup
 };
 
 // Launch geometry for a problem shape (pure host code).
-AccumPlan plan_valu(int64_t n, int M, int K, Mode mode);
-AccumPlan plan_mfma(int64_t n, int M, int K, Mode mode);
-// Whether the matrix-core kernel's per-workgroup state (centre operands and
-// fp64 slab) fits in one workgroup's LDS for this shape.
-bool mfma_fits(int M, int K);
+AccumPlan plan_lane(int64_t n, int M, int K, Mode mode, bool mfma);
+AccumPlan plan_tile(int64_t n, int M, int K, Mode mode);
+// Whether the tile kernel's per-workgroup state (centre operands and fp64
+// slab) fits in one workgroup's LDS for this shape.
+bool tile_fits(int M, int K);
+// Whether the one-object-per-lane matrix-core form supports this shape (its
+// centre operands live in registers).
+bool lane_mfma_fits(int M, int K);
 
 struct StepArgs {
     const float *X;
@@ -88,8 +105,8 @@ struct StepArgs {
     int compare;               // record the change flag of iteration t
 };
 
-hipError_t launch_valu(const StepArgs &a, Mode mode, const AccumPlan &plan, hipStream_t s);
-hipError_t launch_mfma(const StepArgs &a, Mode mode, const AccumPlan &plan, hipStream_t s);
+hipError_t launch_lane(const StepArgs &a, Mode mode, const AccumPlan &plan, hipStream_t s);
+hipError_t launch_tile(const StepArgs &a, Mode mode, const AccumPlan &plan, hipStream_t s);
 
 hipError_t launch_ctl_reset(Ctl *ctl, hipStream_t s);
 

@@ -1,5 +1,6 @@
 // Device helpers shared by the distance kernels: streaming a 64-object tile of
-// X through registers into LDS, and the fp64 re-decision of close calls.
+// X through registers into LDS, the per-wave fp64 accumulation of Eq. (1)'s
+// sums, and the fp64 re-decision of close calls.
 #pragma once
 
 #include "lloyd.h"
@@ -13,42 +14,51 @@ struct TileGeom {
     static constexpr int kFloats = kWave * M;          // floats per 64-object tile
     static constexpr int kVec = kFloats / 4;           // float4s per tile (64*M divisible by 4)
     static constexpr int kVecPerLane = (kVec + kWave - 1) / kWave;
+    // floats per LDS tile slot: the 64 objects, then zeros (at least one full
+    // row, and at least 4 floats for the matrix-core operand reads that run
+    // past a row)
+    static constexpr int kSlot = (kWave * M + (M > 4 ? M : 4) + 3) / 4 * 4;
 };
 
-// Issue the loads of tile q (objects 64q .. 64q+63) into registers.
+// Issue the loads of full tile q (objects 64q .. 64q+63, all < n) into
+// registers: a fixed number of 16-byte loads with no branches, so the compiler
+// can count them when it waits for them.
 template <int M>
-__device__ inline void load_tile(const float *__restrict__ X, int64_t n, int64_t q, int lane,
+__device__ inline void load_tile(const float *__restrict__ X, int64_t q, int lane,
                                  float4 (&buf)[TileGeom<M>::kVecPerLane])
 {
     using G = TileGeom<M>;
-    const int64_t f0 = q * (int64_t)G::kFloats;
-    const int64_t total = n * (int64_t)M;
-    const int64_t left = total - f0;
-    const int nf = left < G::kFloats ? (int)left : G::kFloats;   // floats present
-    const float4 *src = reinterpret_cast<const float4 *>(X + f0);
-    if (nf == G::kFloats) {             // every tile but possibly the last
+    const float4 *src = reinterpret_cast<const float4 *>(X + q * (int64_t)G::kFloats);
 #pragma unroll
-        for (int v = 0; v < G::kVecPerLane; ++v) {
-            const int idx = lane + kWave * v;
-            if (idx < G::kVec) buf[v] = src[idx];
-        }
-        return;
+    for (int v = 0; v < G::kVecPerLane; ++v) {
+        // lanes past the tile's last float4 reload it (in bounds; store_tile
+        // drops them), so every lane issues every load
+        const int idx = lane + kWave * v;
+        buf[v] = src[idx < G::kVec ? idx : G::kVec - 1];
     }
+}
+
+// Loads of the last, partial tile q (objects 64q .. n-1): floats past the end of
+// X read as zero. Used once per launch, outside the streaming loop.
+template <int M>
+__device__ inline void load_tail_tile(const float *__restrict__ X, int64_t n, int64_t q, int lane,
+                                      float4 (&buf)[TileGeom<M>::kVecPerLane])
+{
+    using G = TileGeom<M>;
+    const int64_t f0 = q * (int64_t)G::kFloats;
+    const int nf = (int)(n * (int64_t)M - f0);          // floats present, < kFloats
 #pragma unroll
     for (int v = 0; v < G::kVecPerLane; ++v) {
         const int idx = lane + kWave * v;
+        float4 r = make_float4(0.f, 0.f, 0.f, 0.f);
         if (idx < G::kVec) {
-            if (4 * idx + 3 < nf) {
-                buf[v] = src[idx];
-            } else {
-                const float *s = X + f0 + 4 * idx;
-                float4 r = make_float4(0.f, 0.f, 0.f, 0.f);
-                if (4 * idx + 0 < nf) r.x = s[0];
-                if (4 * idx + 1 < nf) r.y = s[1];
-                if (4 * idx + 2 < nf) r.z = s[2];
-                buf[v] = r;
-            }
+            const float *s = X + f0 + 4 * idx;
+            if (4 * idx + 0 < nf) r.x = s[0];
+            if (4 * idx + 1 < nf) r.y = s[1];
+            if (4 * idx + 2 < nf) r.z = s[2];
+            if (4 * idx + 3 < nf) r.w = s[3];
         }
+        buf[v] = r;
     }
 }
 
@@ -67,9 +77,11 @@ __device__ inline void store_tile(float *tile, int lane,
 
 // fp64 squared distance in the reference operation order: for j ascending,
 // e = x_j - c_j, then d = d + e*e, every operation rounded on its own (this file
-// is compiled with -ffp-contract=off, so nothing is fused).
+// is compiled with -ffp-contract=off, so nothing is fused). xs: the object's M
+// features (in LDS); read per centre so the rare re-decision holds no fp64 copy
+// of the object in registers.
 template <int M>
-__device__ inline int argmin_fp64(const float (&x)[M], const float *__restrict__ C, int K,
+__device__ inline int argmin_fp64(const float *xs, const float *__restrict__ C, int K,
                                   double &best_out)
 {
     double best = INFINITY;
@@ -79,7 +91,7 @@ __device__ inline int argmin_fp64(const float (&x)[M], const float *__restrict__
         double d = 0.0;
 #pragma unroll
         for (int j = 0; j < M; ++j) {
-            const double e = (double)x[j] - (double)c[j];
+            const double e = (double)xs[j] - (double)c[j];
             const double sq = e * e;
             d = d + sq;
         }
@@ -92,83 +104,95 @@ __device__ inline int argmin_fp64(const float (&x)[M], const float *__restrict__
     return lab;
 }
 
-}  // namespace lloyd
-
-namespace lloyd {
-
-// Accumulation layout: a wavefront adds up to P members of one cluster per step,
-// one member per group of MW = M + 1 lanes (lane = slot * MW + column); columns
-// 0..M-1 carry the features and column M carries the member count (adding 1.0
-// per member, exact in fp64).
-template <int M>
-struct Slots {
+// ---------------------------------------------------------------------------
+// Per-wave accumulation of the numerator and denominator of Eq. (1).
+//
+// A wave owns P fp64 slabs of K rows x (M+1) columns: columns 0..M-1 hold the
+// feature sums of a cluster's members and column M their count (adding 1.0
+// per member is exact in fp64). The wave's lanes are split into P groups of
+// LW = 64 / P >= M+1 lanes; in step s, lane (h, j) adds
+// feature j of the tile's object s*P + h into slab h, row label(object). So slab
+// h receives the members at tile positions h, h+P, h+2P, ... in ascending
+// order, every addition is an LDS fp64 add done in program order, and no two
+// lanes of one instruction touch the same address: the sums are deterministic
+// and need no barriers.
+template <int M, int P_ = 0>
+struct WaveAcc {
     static constexpr int MW = M + 1;
-    static constexpr int P = (kWave / MW >= 4) ? 4 : ((kWave / MW >= 2) ? 2 : 1);
-    // floats per wave tile slot: 64 objects, then zeros (one full row, and at
-    // least 4 floats for the matrix-core operand reads that run past a row)
-    static constexpr int kTileFloats = (kWave * M + (M > 4 ? M : 4) + 3) / 4 * 4;
+    static constexpr int LWmin = (M + 1 <= 2) ? 2 : (M + 1 <= 4) ? 4 : (M + 1 <= 8) ? 8
+                               : (M + 1 <= 16) ? 16 : (M + 1 <= 32) ? 32 : 64;
+    static constexpr int Pmax = kWave / LWmin;
+    static constexpr int P = P_ == 0 ? Pmax : P_;   // objects added per step
+    static constexpr int LW = kWave / P;            // lanes per object
+    static constexpr int kSteps = kWave / P;
+    static_assert(P >= 1 && P <= Pmax && (kWave % P) == 0, "slab count");
 };
 
-
-// Add the members of one 64-object tile into the wave's private fp64 slab
-// slab[k][0..M] (feature sums and the count of cluster k: the numerator and
-// denominator of Eq. (1)).
-//
-// lab is this lane's object label (-1: no object). tile holds the 64 objects'
-// features, object-major, followed by at least one row of zeros; ones[0..63] = 1
-// and ones[64] = 0. For each cluster present in the tile a ballot lists its
-// members; member m (in ascending lane order) goes to slot m % P, each slot
-// adds its members in order in fp64, the P slot sums are combined in a fixed
-// tree and added once to the slab. Absent members read the zero row, so the
-// loop has no branches. The order of every addition depends only on the labels.
-template <int M>
-__device__ inline void wave_accumulate(int lab, const float *tile, const float *ones,
-                                       double *slab, int K, int lane)
+// P (a power of two, at most 64 / (M+1) rounded down to a power of two; 0 =
+// that maximum) trades LDS for steps: P slabs, 64 / P steps per tile.
+// lab: this lane's object label (-1: no object). tile: the wave's LDS tile
+// (object-major, with at least one float of slack after the 64 rows). offs: 64
+// ints of wave-private LDS. slabs: the wave's P slabs (P*K*(M+1) doubles).
+template <int M, int P_>
+__device__ inline void accumulate_tile(int lab, const float *tile, int32_t *offs, double *slabs,
+                                       int K, int lane)
 {
-    constexpr int MW = Slots<M>::MW, P = Slots<M>::P;
-    const int s = lane / MW, j = lane - (lane / MW) * MW;
-    // Value of member p for this lane: *(base + p * stride) (bytes). Lanes of
-    // slot u take the position p_u of their step; the per-slot strides are zero
-    // for the other slots, so the address is base + sum_u p_u * stride_u with
-    // one multiply-add per slot and no selects. Lanes outside every slot read
-    // row 0 and their sums are never used.
-    const char *base = (j < M) ? reinterpret_cast<const char *>(tile + j)
-                               : reinterpret_cast<const char *>(ones);
-    const uint32_t stride = (j < M) ? M * 4 : 4;
-    uint32_t st[P];
+    using A = WaveAcc<M, P_>;
+    constexpr int MW = A::MW, LW = A::LW, P = A::P;
+    // row offset (in doubles) of this lane's object in its slab
+    offs[lane] = lab >= 0 ? ((lane % P) * K + lab) * MW : -1;
+    __builtin_amdgcn_wave_barrier();
+    const int h = lane / LW, j = lane % LW;
+    const int jr = j < M ? j : M;              // count lanes read a value they ignore
+    const float *xp = tile + h * M + jr;
+    const int32_t *op = offs + h;
+    const bool feat = j < M;
+    const bool used = j <= M;
+    // Batches of steps: all LDS reads of a batch first, then its adds back to
+    // back (an add cannot be hoisted above a read the compiler cannot prove
+    // disjoint, so interleaving them would serialise every step on LDS latency).
+    constexpr int B = A::kSteps < 16 ? A::kSteps : 16;
 #pragma unroll
-    for (int u = 0; u < P; ++u) st[u] = (s == u) ? stride : 0u;
-    for (int k = 0; k < K; ++k) {
-        uint64_t mask = __ballot(lab == k);
-        if (mask == 0) continue;
-        const int members = __popcll(mask);
-        const double old = (lane < MW) ? slab[k * MW + lane] : 0.0;
-        double acc = 0.0;
-        do {
-            uint32_t offa = 0, offb = 0;
+    for (int s0 = 0; s0 < A::kSteps; s0 += B) {
+        int o[B];
+        float x[B];
 #pragma unroll
-            for (int u = 0; u < P; ++u) {          // positions off the mask, in order
-                const uint32_t p = mask ? (uint32_t)__builtin_ctzll(mask) : (uint32_t)kWave;
-                mask &= ~(1ull << (p & 63));
-                offa += p * st[u];
-            }
+        for (int b = 0; b < B; ++b) {
+            o[b] = op[(s0 + b) * P];
+            x[b] = xp[(s0 + b) * P * M];
+        }
 #pragma unroll
-            for (int u = 0; u < P; ++u) {
-                const uint32_t p = mask ? (uint32_t)__builtin_ctzll(mask) : (uint32_t)kWave;
-                mask &= ~(1ull << (p & 63));
-                offb += p * st[u];
-            }
-            const float va = *reinterpret_cast<const float *>(base + offa);
-            const float vb = *reinterpret_cast<const float *>(base + offb);
-            acc = acc + (double)va;
-            acc = acc + (double)vb;
-        } while (mask);
-        double t = acc;
-        if (P >= 2) t = t + __shfl_down(t, MW, kWave);        // slots (0,1) and (2,3)
-        if (P >= 4) t = t + __shfl_down(t, 2 * MW, kWave);    // then the two pairs
-        if (lane < MW) slab[k * MW + lane] = old + t;
-        if (MW > kWave && lane == 0)                          // M = 64: no lane for the count
-            slab[k * MW + M] = slab[k * MW + M] + (double)members;
+        for (int b = 0; b < B; ++b) {
+            const double v = (double)(feat ? x[b] : 1.0f);
+            if (used && o[b] >= 0)
+                __hip_atomic_fetch_add(slabs + o[b] + j, v, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_WAVEFRONT);
+            if (M + 1 > kWave && lane == 0 && o[b] >= 0)   // M = 64: no lane left for the count
+                __hip_atomic_fetch_add(slabs + o[b] + M, 1.0, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_WAVEFRONT);
+        }
+    }
+    __builtin_amdgcn_wave_barrier();
+}
+
+// Workgroup partial of the wave-accumulation form: for every (cluster, feature)
+// the sum over waves w and slabs h (w, then h, ascending) written to
+// part_sums[K][M], and the counts to part_counts[K]. Call after a barrier.
+template <int M, int P_>
+__device__ inline void write_wave_partials(const double *slabs, int W, int K,
+                                           double *__restrict__ part_sums,
+                                           int32_t *__restrict__ part_counts)
+{
+    using A = WaveAcc<M, P_>;
+    constexpr int MW = A::MW, P = A::P;
+    const int tid = threadIdx.x, nthr = blockDim.x;
+    const size_t rows = (size_t)W * P;          // slabs in the workgroup
+    for (int e = tid; e < K * MW; e += nthr) {
+        const int k = e / MW, j = e - (e / MW) * MW;
+        double s = 0.0;
+        for (size_t r = 0; r < rows; ++r) s = s + slabs[(r * K + k) * MW + j];
+        if (j < M) part_sums[(int64_t)k * M + j] = s;
+        else part_counts[k] = (int32_t)s;
     }
 }
 

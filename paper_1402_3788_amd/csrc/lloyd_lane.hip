@@ -1,0 +1,422 @@
+// Fused assign + accumulate with one object per lane (small K).
+//
+// One wavefront owns a 64-object tile at a time (object l of the tile in lane
+// l) and walks its tiles with a fixed stride, so every sum below is formed in an
+// order that depends only on the problem shape:
+//   1. the tile's 64*M fp32 values are streamed from HBM with 16-byte loads into
+//      the wave's LDS slot (the loads of the tile one or two strides ahead are
+//      issued before the current tile is processed) and each lane reads its
+//      own object's M features into registers;
+//   2. assignment (Algorithm 1 steps 2/4, Eq. (2)), in one of two forms:
+//        DIST = kDistValu: the direct form |x - c|^2 on the vector ALU (centres
+//          are wave-uniform and come through scalar loads); its fp32 error is
+//          at most gamma_{M+1} |x - c|^2, so the two best distances are called
+//          in fp32 only when their gap exceeds 4 gamma_{M+2} of the second;
+//        DIST = kDistMfma: the expanded form score = |c|^2 - 2 x.c on the
+//          matrix cores with v_mfma_f32_4x4x1f32. That instruction runs 16
+//          independent 4x4 outer products; with A[i] = -2 c_{4q+i, f} in every
+//          group of four lanes and B = the lane's own x_f, register i of lane
+//          l accumulates sum_f -2 c_{4q+i, f} x_{l, f}. A chain over the M
+//          features plus one step with A = |c|^2, B = 1 leaves every lane
+//          with its own object's scores for centres 4q .. 4q+3, so a lane
+//          scans K scores of one object with no cross-lane merge. The -2C and
+//          |c|^2 operands stay in registers for the whole launch (K <= 16).
+//          The expanded form's fp32 error is bounded by
+//          gamma_{M+2} (3|c|^2 + |x|^2), so a label is accepted only if the
+//          two best scores differ by more than 2.5 times that bound;
+//      either way, a lane whose call is too close recomputes all K distances
+//      in fp64 in the oracle's operation order and takes the lowest-index
+//      minimum, so the label is the exact-arithmetic argmin;
+//   3. accumulation (the numerator and denominator of Eq. (1)) into the wave's
+//      private fp64 slabs (accumulate_tile), no barriers;
+//   4. at the end the workgroup adds its waves' slabs in a fixed order, writes
+//      one fp64 partial per (cluster, feature) plus one count per cluster, and
+//      the last workgroup forms the centres (tree_finalize).
+#include "lloyd.h"
+#include "lloyd_device.h"
+#include "lloyd_reduce.h"
+
+#include <math.h>
+
+#include <array>
+#include <type_traits>
+#include <utility>
+
+#include "lloyd_parts.h"
+
+namespace lloyd {
+
+namespace {
+
+typedef float f4v __attribute__((ext_vector_type(4)));
+
+constexpr int kMaxWaves = 12;
+constexpr int kMinWavesPerSimd = 3;   // caps registers at 168 per lane
+constexpr int kDistValu = 0;
+constexpr int kDistMfma = 1;
+constexpr int kLaneMfmaMaxK = 16;     // four 4-centre operand columns
+constexpr int kLaneMfmaMaxM = 27;
+
+// LDS carve-up: [operand table] [W tile slots] [W x 64 ints of slab offsets]
+// [W x P slabs]. The operand table (matrix-core form only) holds, for centre
+// quad qq and lane group r = lane % 4, the row -2 c_{4qq+r, 0..M-1}, |c|^2,
+// zero-padded to a multiple of 4 floats.
+__host__ __device__ inline size_t lane_tile_bytes(int M)
+{
+    return (size_t)((kWave * M + (M > 4 ? M : 4) + 3) / 4 * 4) * 4;
+}
+
+__host__ __device__ inline int lane_atab_row(int M) { return (M + 1 + 3) / 4 * 4; }
+
+__host__ __device__ inline size_t lane_atab_bytes(int M, bool mfma)
+{
+    return mfma ? (size_t)(kLaneMfmaMaxK / 4) * 4 * lane_atab_row(M) * 4 : 0;
+}
+
+// Objects per accumulation step: the most the lanes allow (pa = 0) or one (pa = 1).
+[[maybe_unused]] __host__ __device__ inline int lane_acc_p(int M, int pa)
+{
+    if (pa == 1) return 1;
+    const int lw = (M + 1 <= 2) ? 2 : (M + 1 <= 4) ? 4 : (M + 1 <= 8) ? 8
+                 : (M + 1 <= 16) ? 16 : (M + 1 <= 32) ? 32 : 64;
+    return kWave / lw;
+}
+
+__host__ __device__ inline size_t lane_slab_off(int M, int W, bool mfma)
+{
+    return lane_atab_bytes(M, mfma) + (size_t)W * (lane_tile_bytes(M) + kWave * 4);
+}
+
+template <int M, int MODE, int PA, int DIST>
+__global__ void __launch_bounds__(kMaxWaves * kWave, kMinWavesPerSimd)
+lloyd_lane_kernel(const float *__restrict__ X, int64_t n, const float *__restrict__ C, int K,
+                  int32_t *__restrict__ labels, const int32_t *__restrict__ labels_in,
+                  float *__restrict__ min_d2, double *__restrict__ part_sums,
+                  int32_t *__restrict__ part_counts, Ctl *__restrict__ ctl, int t, int fixed,
+                  TreeArgs tree)
+{
+    using G = TileGeom<M>;
+    constexpr int V = G::kVecPerLane;
+    constexpr int kP = WaveAcc<M, PA>::P;
+    constexpr bool kMfma = DIST == kDistMfma;
+    constexpr int KQ = kMfma ? kLaneMfmaMaxK / 4 : 1;    // centre quads held in registers
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int W = blockDim.x / kWave;
+    const int wave = threadIdx.x / kWave;
+    const int lane = threadIdx.x % kWave;
+
+    if (MODE == kAssignAccum && stop_before(ctl, t, fixed)) return;
+
+    constexpr int FP = (M + 1 + 3) / 4 * 4;               // operand table row (lane_atab_row)
+    constexpr size_t kAtab = kMfma ? (size_t)KQ * 4 * FP * 4 : 0;   // lane_atab_bytes
+    float *atab = reinterpret_cast<float *>(smem);
+    float *tile = reinterpret_cast<float *>(smem + kAtab) + wave * G::kSlot;
+    int32_t *offs = reinterpret_cast<int32_t *>(smem + kAtab + (size_t)W * G::kSlot * 4) + wave * kWave;
+    double *slabs_all = reinterpret_cast<double *>(smem + lane_slab_off(M, W, kMfma));
+    double *slabs = slabs_all + (size_t)wave * kP * K * (M + 1);
+
+    // Full tiles (all 64 objects present) are streamed in the main loop; the
+    // last, partial tile (if n is not a multiple of 64) is handled after it.
+    const int64_t nfull = n / kWave;
+    const int64_t stride = (int64_t)gridDim.x * W;
+    const int64_t q0 = (int64_t)blockIdx.x * W + wave;
+
+    // tiles in flight per wave: two ahead, or one where the matrix-core
+    // operands take the registers
+    constexpr int kDepth = kMfma ? 1 : 2;
+    float4 buf[2][V];   // register buffers, selected by compile-time index
+    if (q0 < nfull) load_tile<M>(X, q0, lane, buf[0]);
+    if (kDepth == 2 && q0 + stride < nfull) load_tile<M>(X, q0 + stride, lane, buf[1]);
+
+    for (int i = lane; i < G::kSlot - kWave * M; i += kWave) tile[kWave * M + i] = 0.f;
+    if (MODE != kAssign) {
+        for (int i = lane; i < kP * K * (M + 1); i += kWave) slabs[i] = 0.0;
+    }
+
+    // Matrix-core operand table (see lane_atab_bytes): -2c (exact), then |c|^2
+    // in fp32 with the features in order (+inf for centres past K, so they
+    // never win), then zeros; and cmax = the largest |c|^2.
+    float cmax = 0.f;
+    if (kMfma && MODE != kAccumLabels) {
+        if (threadIdx.x < KQ * 4) {
+            const int k = threadIdx.x;                 // row qq * 4 + r holds centre k
+            float *row = atab + k * FP;
+            float nk = 0.f;
+            for (int f = 0; f < M; ++f) {
+                const float c = k < K ? C[(int64_t)k * M + f] : 0.f;
+                row[f] = -2.0f * c;
+                nk = __builtin_fmaf(c, c, nk);
+            }
+            row[M] = k < K ? nk : INFINITY;
+            for (int f = M + 1; f < FP; ++f) row[f] = 0.f;
+        }
+        __syncthreads();
+        for (int k = 0; k < K; ++k) cmax = fmaxf(cmax, atab[k * FP + M]);
+    }
+
+    // fp32 call thresholds (see the header comment)
+    constexpr float kTau = 4.0f * (float)(M + 2) * 5.9604645e-8f;
+    constexpr float kGuard = 2.5f * 1.01f * (float)(M + 2) * 5.9604645e-8f;
+    int nfallback = 0;
+
+    auto step = [&](int64_t qq_, auto bi, bool prefetch) {
+        float4 (&bb)[V] = buf[decltype(bi)::value];
+        store_tile<M>(tile, lane, bb);
+        __builtin_amdgcn_wave_barrier();
+        if (prefetch && qq_ + kDepth * stride < nfull)
+            load_tile<M>(X, qq_ + kDepth * stride, lane, bb);
+
+        const int64_t i = qq_ * kWave + lane;
+        const bool valid = i < n;
+        int lab;
+        if (MODE == kAccumLabels) {
+            lab = valid ? labels_in[i] : -1;
+            if (lab < 0 || lab >= K) lab = -1;
+        } else {
+            float x[M];
+#pragma unroll
+            for (int j = 0; j < M; ++j) x[j] = tile[lane * M + j];
+            float b1 = INFINITY, b2 = INFINITY;
+            lab = 0;
+            bool ok;
+            if (kMfma) {
+                // the KQ chains interleaved feature by feature (independent
+                // accumulators keep the matrix pipe busy; each x_f is used by
+                // all chains and |x|^2 as soon as it arrives). All KQ chains
+                // run whatever K is: centres past K score +inf, so the code
+                // has no branch on K.
+                // A operands come from the operand table, four features per
+                // 16-byte read (four distinct addresses per read: broadcast).
+                f4v d[KQ];
+#pragma unroll
+                for (int qq = 0; qq < KQ; ++qq) d[qq] = f4v{0.f, 0.f, 0.f, 0.f};
+                float xsq = 0.f;
+                const float *arow = atab + (lane & 3) * FP;
+#pragma unroll
+                for (int f4 = 0; f4 < FP / 4; ++f4) {
+                    f4v a[KQ];
+#pragma unroll
+                    for (int qq = 0; qq < KQ; ++qq)
+                        a[qq] = *reinterpret_cast<const f4v *>(arow + qq * 4 * FP + 4 * f4);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int f = 4 * f4 + e;
+                        if (f > M) break;
+                        const float b = f < M ? x[f < M ? f : 0] : 1.0f;
+#pragma unroll
+                        for (int qq = 0; qq < KQ; ++qq)
+                            d[qq] = __builtin_amdgcn_mfma_f32_4x4x1f32(a[qq][e], b, d[qq], 0, 0, 0);
+                        if (f < M) xsq = __builtin_fmaf(b, b, xsq);
+                    }
+                }
+#pragma unroll
+                for (int qq = 0; qq < KQ; ++qq) {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const float sc = d[qq][r];
+                        const bool lt = sc < b1;
+                        b2 = __builtin_amdgcn_fmed3f(b1, b2, sc);
+                        b1 = lt ? sc : b1;
+                        lab = lt ? 4 * qq + r : lab;
+                    }
+                }
+                const float thr = kGuard * (3.02f * cmax + 1.0001f * xsq) + 1e-30f;
+                ok = (K == 1) || (b2 - b1 > thr);
+            } else {
+                for (int k = 0; k < K; ++k) {
+                    float d = 0.f;
+#pragma unroll
+                    for (int j = 0; j < M; ++j) {
+                        const float e = x[j] - C[k * M + j];
+                        d = __builtin_fmaf(e, e, d);
+                    }
+                    // top-2: with b1 <= b2, the new second-best is the median of
+                    // (b1, b2, d) and the new best is min(b1, d)
+                    const bool lt = d < b1;
+                    b2 = __builtin_amdgcn_fmed3f(b1, b2, d);
+                    b1 = lt ? d : b1;
+                    lab = lt ? k : lab;
+                }
+                ok = (K == 1) || ((b2 - b1) > kTau * b2 && b2 >= 1e-30f);
+            }
+            float dmin = kMfma ? 0.f : b1;
+            if (valid && !ok) {
+                double bd;
+                lab = argmin_fp64<M>(tile + lane * M, C, K, bd);
+                dmin = (float)bd;
+            } else if (kMfma && valid && MODE == kAssign && min_d2 != nullptr) {
+                const float *c = C + (int64_t)lab * M;
+                float d = 0.f;
+#pragma unroll
+                for (int j = 0; j < M; ++j) {
+                    const float e = x[j] - c[j];
+                    d = __builtin_fmaf(e, e, d);
+                }
+                dmin = d;
+            }
+            if (ctl != nullptr) nfallback += __popcll(__ballot(valid && !ok));
+            if (valid) {
+                labels[i] = lab;
+                if (MODE == kAssign && min_d2 != nullptr) min_d2[i] = dmin;
+            }
+            if (!valid) lab = -1;
+        }
+
+        if (MODE != kAssign) accumulate_tile<M, PA>(lab, tile, offs, slabs, K, lane);
+    };
+
+    if (kDepth == 1) {
+        for (int64_t q = q0; q < nfull; q += stride) step(q, std::integral_constant<int, 0>{}, true);
+    } else {
+        for (int64_t q = q0; q < nfull; q += 2 * stride) {
+            step(q, std::integral_constant<int, 0>{}, true);
+            if (q + stride < nfull) step(q + stride, std::integral_constant<int, 1>{}, true);
+        }
+    }
+    if (nfull * kWave < n && nfull >= q0 && (nfull - q0) % stride == 0) {
+        load_tail_tile<M>(X, n, nfull, lane, buf[0]);
+        step(nfull, std::integral_constant<int, 0>{}, false);
+    }
+
+    if (ctl != nullptr && lane == 0 && nfallback > 0) atomicAdd(&ctl->fallbacks, nfallback);
+
+    if (MODE != kAssign) {
+        __syncthreads();
+        write_wave_partials<M, PA>(slabs_all, W, K, part_sums + (int64_t)blockIdx.x * K * M,
+                                   part_counts + (int64_t)blockIdx.x * K);
+        tree_finalize(tree, reinterpret_cast<uint32_t *>(slabs_all));
+    }
+}
+
+TreeArgs tree_args(const StepArgs &a, int groups)
+{
+    TreeArgs r{};
+    r.part_sums = a.part_sums;
+    r.part_counts = a.part_counts;
+    r.grp_sums = a.grp_sums;
+    r.grp_counts = a.grp_counts;
+    r.tickets = a.ctl != nullptr ? a.ctl->tickets : nullptr;
+    r.G = groups;
+    r.K = a.K;
+    r.M = a.M;
+    r.prev = a.C;
+    r.centers = a.centers_out;
+    r.counts = a.counts_out;
+    r.ctl = a.ctl;
+    r.t = a.t;
+    r.compare = a.compare;
+    return r;
+}
+
+template <int M, int DIST>
+hipError_t launch_m(const StepArgs &a, Mode mode, const AccumPlan &p, hipStream_t s)
+{
+    const dim3 grid(p.groups), block(p.waves * kWave);
+    const TreeArgs tr = tree_args(a, p.groups);
+#define LLOYD_LANE_LAUNCH(MD, PA)                                                              \
+    do {                                                                                       \
+        auto kern = lloyd_lane_kernel<M, MD, PA, DIST>;                                        \
+        static const size_t st = static_lds_bytes(reinterpret_cast<const void *>(kern));       \
+        if (st > (size_t)kMaxLds || st + p.lds_bytes > (size_t)kMaxLds)                        \
+            return hipErrorInvalidConfiguration;                                               \
+        hipLaunchKernelGGL(kern, grid, block, p.lds_bytes, s, a.X, a.n, a.C, a.K, a.labels,    \
+                           a.labels_in, a.min_d2, a.part_sums, a.part_counts, a.ctl, a.t,      \
+                           a.fixed, tr);                                                       \
+    } while (0)
+    const bool one = p.accum == 1;
+    switch (mode) {
+    case kAssign: LLOYD_LANE_LAUNCH(kAssign, 0); break;
+    case kAssignAccum:
+        if (one) LLOYD_LANE_LAUNCH(kAssignAccum, 1);
+        else LLOYD_LANE_LAUNCH(kAssignAccum, 0);
+        break;
+    case kAccumLabels:
+        if (one) LLOYD_LANE_LAUNCH(kAccumLabels, 1);
+        else LLOYD_LANE_LAUNCH(kAccumLabels, 0);
+        break;
+    }
+#undef LLOYD_LANE_LAUNCH
+    return hipGetLastError();
+}
+
+using LaunchFn = hipError_t (*)(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
+
+// This translation unit instantiates the kernels for the feature counts of
+// one part of [1, kMaxM] (the build compiles it once per part, in parallel);
+// the matrix-core form only up to kLaneMfmaMaxM features.
+constexpr int kPartLo = LLOYD_PART * kMaxM / LLOYD_PARTS + 1;
+constexpr int kPartN = kMaxM / LLOYD_PARTS;
+
+template <int M>
+constexpr LaunchFn mfma_entry()
+{
+    if constexpr (M <= kLaneMfmaMaxM) return &launch_m<M, kDistMfma>;
+    else return nullptr;
+}
+
+template <int... Is>
+constexpr auto make_table(std::integer_sequence<int, Is...>)
+{
+    return std::array<LaunchFn, 2 * sizeof...(Is)>{&launch_m<kPartLo + Is, kDistValu>...,
+                                                   mfma_entry<kPartLo + Is>()...};
+}
+
+}  // namespace
+
+hipError_t LLOYD_PART_FN(launch_lane_part)(const StepArgs &a, Mode mode, const AccumPlan &plan,
+                                           hipStream_t s)
+{
+    static constexpr auto table = make_table(std::make_integer_sequence<int, kPartN>{});
+    if (a.M < kPartLo || a.M >= kPartLo + kPartN) return hipErrorInvalidValue;
+    const LaunchFn fn = table[(plan.path == kPathLaneMfma ? kPartN : 0) + a.M - kPartLo];
+    return fn ? fn(a, mode, plan, s) : hipErrorInvalidValue;
+}
+
+#if LLOYD_PART == 0
+bool lane_mfma_fits(int M, int K) { return K <= kLaneMfmaMaxK && M <= kLaneMfmaMaxM; }
+
+AccumPlan plan_lane(int64_t n, int M, int K, Mode mode, bool mfma)
+{
+    AccumPlan p{};
+    p.path = mfma ? kPathLaneMfma : kPathValu;
+    auto bytes = [&](int W, int pa) {
+        size_t b = lane_slab_off(M, W, mfma);
+        if (mode != kAssign) b += (size_t)W * lane_acc_p(M, pa) * K * (M + 1) * 8;
+        return b;
+    };
+    auto most_waves = [&](int pa) {
+        int w = kMaxWaves;
+        while (w > 0 && bytes(w, pa) > (size_t)kMaxLds) --w;
+        return w;
+    };
+    // slabs with the most objects per step unless one object per step leaves
+    // more waves
+    int pa = 0, W = most_waves(0);
+    if (mode != kAssign && most_waves(1) > W) {
+        pa = 1;
+        W = most_waves(1);
+    }
+    const int64_t nq = (n + kWave - 1) / kWave;
+    while (W > 1 && W / 2 >= nq) W /= 2;
+    int64_t groups = (nq + W - 1) / W;
+    if (groups > kCUs) groups = kCUs;       // one persistent workgroup per compute unit
+    p.waves = W;
+    p.groups = (int)groups;
+    p.accum = pa;
+    p.lds_bytes = bytes(W, pa);
+    return p;
+}
+
+hipError_t launch_lane(const StepArgs &a, Mode mode, const AccumPlan &plan, hipStream_t s)
+{
+    if (a.M < 1 || a.M > kMaxM) return hipErrorInvalidValue;
+    switch ((a.M - 1) / (kMaxM / LLOYD_PARTS)) {
+#define LLOYD_CASE(P) case P: return launch_lane_part_##P(a, mode, plan, s);
+        LLOYD_PART_CASES
+#undef LLOYD_CASE
+    }
+    return hipErrorInvalidValue;
+}
+#endif
+
+}  // namespace lloyd

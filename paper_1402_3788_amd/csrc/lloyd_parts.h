@@ -17,12 +17,12 @@
 static_assert(lloyd::kMaxM % LLOYD_PARTS == 0, "parts split the feature counts evenly");
 
 namespace lloyd {
-hipError_t launch_mfma_part_0(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
-hipError_t launch_mfma_part_1(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
-hipError_t launch_mfma_part_2(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
-hipError_t launch_mfma_part_3(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
-hipError_t launch_valu_part_0(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
-hipError_t launch_valu_part_1(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
-hipError_t launch_valu_part_2(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
-hipError_t launch_valu_part_3(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
+hipError_t launch_tile_part_0(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
+hipError_t launch_tile_part_1(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
+hipError_t launch_tile_part_2(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
+hipError_t launch_tile_part_3(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
+hipError_t launch_lane_part_0(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
+hipError_t launch_lane_part_1(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
+hipError_t launch_lane_part_2(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
+hipError_t launch_lane_part_3(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
 }  // namespace lloyd

@@ -51,12 +51,14 @@ __device__ inline void tree_finalize(const TreeArgs &r, uint32_t *s_scratch)
 
     // ---- first level: the last workgroup of group q
     // The barrier completes every wave's stores (workgroup release); one
-    // device-scope release fence per workgroup then publishes them.
+    // device-scope release fence per workgroup then publishes them, and only
+    // the last arrival takes a device-scope acquire (a full fence would also
+    // invalidate the caches in every workgroup).
     __syncthreads();
     if (tid == 0) {
-        __threadfence();
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
         s_scratch[0] = atomicAdd(&r.tickets[q], 1u);
-        if (s_scratch[0] == (uint32_t)(g1 - g0 - 1)) __threadfence();   // acquire
+        if (s_scratch[0] == (uint32_t)(g1 - g0 - 1)) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     }
     __syncthreads();
     if (s_scratch[0] != (uint32_t)(g1 - g0 - 1)) return;
@@ -84,9 +86,9 @@ __device__ inline void tree_finalize(const TreeArgs &r, uint32_t *s_scratch)
     // ---- second level: the last group reducer
     __syncthreads();
     if (tid == 0) {
-        __threadfence();
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
         s_scratch[0] = atomicAdd(&r.tickets[NG], 1u);
-        if (s_scratch[0] == (uint32_t)(NG - 1)) __threadfence();        // acquire
+        if (s_scratch[0] == (uint32_t)(NG - 1)) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     }
     __syncthreads();
     if (s_scratch[0] != (uint32_t)(NG - 1)) return;
@@ -98,6 +100,8 @@ __device__ inline void tree_finalize(const TreeArgs &r, uint32_t *s_scratch)
         s_cnt[k] = c;
         r.counts[k] = c;
     }
+    __syncthreads();                 // every thread has read the ticket; counts are in LDS
+    if (tid == 0) s_scratch[0] = 0;  // reused as the "some centre changed" flag
     __syncthreads();
     int changed = 0;
     for (int e = tid; e < KM; e += nthr) {
@@ -114,7 +118,10 @@ __device__ inline void tree_finalize(const TreeArgs &r, uint32_t *s_scratch)
         changed |= (__float_as_uint(nv) != __float_as_uint(old)) ? 1 : 0;
         r.centers[e] = nv;
     }
-    const int any = __syncthreads_or(changed);
+    // (an explicit LDS flag rather than __syncthreads_or, which takes static LDS)
+    if (changed) s_scratch[0] = 1;
+    __syncthreads();
+    const int any = (int)s_scratch[0];
     if (tid == 0) {
         if (r.compare && r.ctl != nullptr) r.ctl->changed[r.t & 1] = any ? 1 : 0;
         r.tickets[NG] = 0;

@@ -1,4 +1,5 @@
-// Fused assign + accumulate with the distances on the matrix cores.
+// Fused assign + accumulate with the distances on the matrix cores, 64-object
+// tiles against 16-centre blocks (any K).
 //
 // Expanded form of the squared distance of Eq. (2): for object x and centre c,
 //     |x - c|^2 = |x|^2 + score,   score = |c|^2 - 2 x.c,
@@ -13,8 +14,9 @@
 // Layout of v_mfma_f32_16x16x4f32 (64 lanes): A[i][k] is in lane i + 16k,
 // B[k][j] in lane j + 16k, and D[i][j] in lane j + 16(i/4), register i%4. So
 // after a chain every lane holds the scores of 4 centres for one object; a lane
-// keeps a running best / second-best over its centres, and two xor-shuffles
-// (16, 32) merge the four lanes that share an object.
+// keeps a running best / second-best over its centres, and two row swaps
+// (v_permlane16_swap, v_permlane32_swap) merge the four lanes that share an
+// object.
 //
 // The expanded form cancels: its fp32 error is bounded by
 // gamma_{M+2} (3|c|^2 + |x|^2), so a label is accepted only if the two best
@@ -22,11 +24,16 @@
 // largest centre norm). Other objects are re-decided with fp64 distances in the
 // fixed operation order, over all centres, lowest index on ties.
 //
-// Accumulation (the sums of Eq. (1)) has two forms, both free of atomics and
-// with every addition in an order fixed by the problem shape:
-//   wave    -- each wavefront adds its own tiles into a private fp64 slab (no
-//              barriers); at the end the workgroup adds the slabs in wave order.
-//              Used while W private slabs fit in LDS (small K*M).
+// Each wavefront streams 64-object tiles: the next two tiles' loads are in
+// flight in registers while the current tile is staged in the wave's LDS slot.
+//
+// Accumulation (the sums of Eq. (1)) has two forms, both free of atomics across
+// lanes that share an address and with every addition in an order fixed by the
+// problem shape:
+//   wave    -- each wavefront adds its own tiles into private fp64 slabs
+//              (accumulate_tile: LDS fp64 adds in program order, no barriers);
+//              at the end the workgroup adds the slabs in a fixed order. Used
+//              while W >= 4 waves' private slabs fit in LDS (small K*M).
 //   block   -- one fp64 slab per workgroup: after a barrier, wave w owns the
 //              clusters k = w, w+W, ...; for each it lists the workgroup tile's
 //              members in ascending object order (ballot + prefix count) and
@@ -38,6 +45,7 @@
 #include <math.h>
 
 #include <array>
+#include <type_traits>
 #include <utility>
 
 #include "lloyd_parts.h"
@@ -49,31 +57,42 @@ namespace {
 typedef float f4v __attribute__((ext_vector_type(4)));
 
 constexpr int kCols = 4;      // 16-object columns per wave tile (64 objects)
-constexpr int kAccWave = 1;
-constexpr int kAccBlock = 2;
-constexpr int kMaxWaves = 16;
+constexpr int kAccWave = 1;    // per-wave slabs, WaveAcc<M>::Pmax objects per step
+constexpr int kAccBlock = 2;   // one slab per workgroup
+constexpr int kAccWave1 = 3;   // per-wave slab, one object per step (less LDS)
+constexpr int kMaxWaves = 8;
+[[maybe_unused]] constexpr int kMinWaveForm = 4;   // fewest waves the wave form is used with
 
 // LDS carve-up of a workgroup (dynamic shared memory).
 struct MfmaLds {
-    size_t ones, tiles, aswz, cnorm, misc, labs, members, scratch, slab, cnt, total;
+    size_t aswz, cnorm, misc, tiles, offs, labs, members, scratch, slab, cnt, total;
     int tile_floats;
 };
 
 __host__ __device__ inline size_t al16(size_t v) { return (v + 15) & ~size_t(15); }
 
+// Objects added per accumulation step of a wave form (WaveAcc<M, P>::P).
+__host__ __device__ inline int wave_acc_p(int M, int acc)
+{
+    if (acc == kAccWave1) return 1;
+    const int lw = (M + 1 <= 2) ? 2 : (M + 1 <= 4) ? 4 : (M + 1 <= 8) ? 8
+                 : (M + 1 <= 16) ? 16 : (M + 1 <= 32) ? 32 : 64;
+    return kWave / lw;
+}
+
 __host__ __device__ inline MfmaLds mfma_lds(int M, int K, int W, int acc)
 {
     const int KS = (M + 3) / 4, KT = (K + 15) / 16;
     MfmaLds L{};
-    L.tile_floats = (kWave * M + (M > 4 ? M : 4) + 3) / 4 * 4;    // tile + zero slack
+    L.tile_floats = (kWave * M + (M > 4 ? M : 4) + 3) / 4 * 4;    // TileGeom<M>::kSlot
     size_t o = 0;
-    L.ones = o;    o = al16(o + 68 * 4);
-    L.tiles = o;   o = al16(o + (size_t)W * L.tile_floats * 4);
     L.aswz = o;    o = al16(o + (size_t)KT * KS * kWave * 4);
     L.cnorm = o;   o = al16(o + (size_t)KT * 16 * 4);
     L.misc = o;    o = al16(o + 16);
-    if (acc == kAccWave) {
-        L.slab = o;    o = al16(o + (size_t)W * K * (M + 1) * 8);
+    L.tiles = o;   o = al16(o + (size_t)W * L.tile_floats * 4);
+    L.offs = o;    o = al16(o + (size_t)W * kWave * 4);
+    if (acc == kAccWave || acc == kAccWave1) {
+        L.slab = o;    o = al16(o + (size_t)W * wave_acc_p(M, acc) * K * (M + 1) * 8);
     } else if (acc == kAccBlock) {
         L.labs = o;    o = al16(o + (size_t)W * kWave * 4);
         L.members = o; o = al16(o + (size_t)W * W * kWave * 4);
@@ -85,9 +104,47 @@ __host__ __device__ inline MfmaLds mfma_lds(int M, int K, int W, int acc)
     return L;
 }
 
+// Second-best of two (best, second) pairs, b1 <= b2 and p1 <= p2:
+// min(max(b1, p1), min(b2, p2)).
+__device__ inline float second_of(float b1, float b2, float p1, float p2)
+{
+    return __builtin_amdgcn_fmed3f(b1, p1, fminf(b2, p2));
+}
+
+// Merge the (best, second, label) triples of lanes l and l ^ 16 (ROW = 16) or
+// l and l ^ 32 (ROW = 32): the row swap returns, in every lane, the triples of
+// both lanes of its pair; the merge keeps the lower label on equal scores.
+template <int ROW>
+__device__ inline void merge_rows(float &b1, float &b2, int &lb)
+{
+    auto swap = [](uint32_t v) {
+        if (ROW == 16) return __builtin_amdgcn_permlane16_swap(v, v, false, false);
+        return __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    };
+    const auto s1 = swap(__float_as_uint(b1));
+    const auto s2 = swap(__float_as_uint(b2));
+    const auto sl = swap((uint32_t)lb);
+    const float f1 = __uint_as_float(s1[0]), g1 = __uint_as_float(s1[1]);
+    const float f2 = __uint_as_float(s2[0]), g2 = __uint_as_float(s2[1]);
+    const int fl = (int)sl[0], gl = (int)sl[1];
+    const bool take = (g1 < f1) | ((g1 == f1) & (gl < fl));
+    b2 = second_of(f1, f2, g1, g2);
+    b1 = take ? g1 : f1;
+    lb = take ? gl : fl;
+}
+
+template <int ROW>
+__device__ inline float sum_rows(float v)
+{
+    uint32_t u = __float_as_uint(v);
+    const auto s = (ROW == 16) ? __builtin_amdgcn_permlane16_swap(u, u, false, false)
+                               : __builtin_amdgcn_permlane32_swap(u, u, false, false);
+    return __uint_as_float(s[0]) + __uint_as_float(s[1]);
+}
+
 template <int M, int MODE, int ACC>
 __global__ void __launch_bounds__(kMaxWaves * kWave)
-lloyd_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict__ C, int K,
+lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restrict__ C, int K,
                   int32_t *__restrict__ labels, const int32_t *__restrict__ labels_in,
                   float *__restrict__ min_d2, double *__restrict__ part_sums,
                   int32_t *__restrict__ part_counts, Ctl *__restrict__ ctl, int t, int fixed,
@@ -95,10 +152,13 @@ lloyd_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restric
 {
     using TG = TileGeom<M>;
     constexpr int KS = (M + 3) / 4;
-    constexpr int kTilePad = Slots<M>::kTileFloats;   // floats per wave tile slot
-    constexpr int MW = Slots<M>::MW;
+    constexpr int kSlot = TG::kSlot;
+    constexpr int V = TG::kVecPerLane;
     constexpr bool kAccum = MODE != kAssign;
     constexpr int kAcc = kAccum ? ACC : 0;
+    constexpr bool kWaveForm = kAcc == kAccWave || kAcc == kAccWave1;
+    constexpr int PA = kAcc == kAccWave1 ? 1 : 0;        // WaveAcc slab-count parameter
+    constexpr int kP = WaveAcc<M, PA>::P;
     extern __shared__ __align__(16) unsigned char smem[];
     const int W = blockDim.x / kWave;
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
@@ -108,20 +168,29 @@ lloyd_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restric
     if (MODE == kAssignAccum && stop_before(ctl, t, fixed)) return;
 
     const MfmaLds L = mfma_lds(M, K, W, kAcc);
-    float *ones = reinterpret_cast<float *>(smem + L.ones);
     float *tiles = reinterpret_cast<float *>(smem + L.tiles);
-    float *tile = tiles + wave * kTilePad;
+    float *tile = tiles + wave * kSlot;
+    int32_t *offs = reinterpret_cast<int32_t *>(smem + L.offs) + wave * kWave;
     float *aswz = reinterpret_cast<float *>(smem + L.aswz);
     float *cnorm = reinterpret_cast<float *>(smem + L.cnorm);
     float *s_cmax = reinterpret_cast<float *>(smem + L.misc);
+    double *wslabs = reinterpret_cast<double *>(smem + L.slab) + (size_t)wave * kP * K * (M + 1);
 
+    // A block tile is the W wave tiles bt*W .. bt*W+W-1 of one workgroup step.
+    // Block tiles whose wave tiles are all full (64 objects present) are
+    // streamed in the main loop; the one block tile after them (partial tiles
+    // or tiles past the end) is handled after it.
     const int64_t nq = (n + kWave - 1) / kWave;
+    const int64_t nfull = n / kWave;
+    const int64_t nbt_main = nfull / W;
     const int64_t nbt = (nq + W - 1) / W;
+    const int64_t G = gridDim.x;
 
-    // first tile's loads go out before the prologue
-    float4 buf[TG::kVecPerLane];
-    int64_t bt = blockIdx.x;
-    if (bt < nbt && bt * W + wave < nq) load_tile<M>(X, n, bt * W + wave, lane, buf);
+    // the first two tiles' loads go out before the prologue
+    float4 buf[2][V];   // register buffers, selected by compile-time index
+    const int64_t bt0 = blockIdx.x;
+    if (bt0 < nbt_main) load_tile<M>(X, bt0 * W + wave, lane, buf[0]);
+    if (bt0 + G < nbt_main) load_tile<M>(X, (bt0 + G) * W + wave, lane, buf[1]);
 
     // ---- prologue: A operands (-2C in lane order), centre norms, slabs
     if (MODE != kAccumLabels) {
@@ -132,14 +201,13 @@ lloyd_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restric
         }
     }
     {
-        constexpr int kSlack = kTilePad - kWave * M;     // zeros after each tile
+        constexpr int kSlack = kSlot - kWave * M;     // zeros after each tile
         for (int i = tid; i < W * kSlack; i += blockDim.x)
-            tiles[(i / kSlack) * kTilePad + kWave * M + (i % kSlack)] = 0.f;
+            tiles[(i / kSlack) * kSlot + kWave * M + (i % kSlack)] = 0.f;
     }
-    if (kAcc == kAccWave) {
+    if (kWaveForm) {
         double *slabs = reinterpret_cast<double *>(smem + L.slab);
-        for (int i = tid; i < W * K * MW; i += blockDim.x) slabs[i] = 0.0;
-        for (int i = tid; i < 68; i += blockDim.x) ones[i] = i < kWave ? 1.f : 0.f;
+        for (int i = tid; i < W * kP * K * (M + 1); i += blockDim.x) slabs[i] = 0.0;
     } else if (kAcc == kAccBlock) {
         double *slab = reinterpret_cast<double *>(smem + L.slab);
         int32_t *cnt = reinterpret_cast<int32_t *>(smem + L.cnt);
@@ -178,16 +246,15 @@ lloyd_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restric
     const int g = lane >> 4, l16 = lane & 15;
     int nfallback = 0;
 
-    for (; bt < nbt; bt += gridDim.x) {
-        const int64_t q = bt * W + wave;
+    // One wave tile: stage it in LDS, put the loads of the tile two strides
+    // ahead in flight in the same registers, assign, accumulate.
+    auto step = [&](int64_t b, auto bi, bool prefetch) {
+        float4 (&bb)[V] = buf[decltype(bi)::value];
+        const int64_t q = b * W + wave;
         const bool have = q < nq;
-        if (kAcc != kAccBlock && !have) break;      // no barriers inside: a wave may stop
-        if (have) store_tile<M>(tile, lane, buf);
+        if (have) store_tile<M>(tile, lane, bb);
         __builtin_amdgcn_wave_barrier();
-        {
-            const int64_t qn = (bt + gridDim.x) * W + wave;
-            if (bt + gridDim.x < nbt && qn < nq) load_tile<M>(X, n, qn, lane, buf);
-        }
+        if (prefetch && b + 2 * G < nbt_main) load_tile<M>(X, (b + 2 * G) * W + wave, lane, bb);
         const int64_t i = q * kWave + lane;
         const bool valid = have && i < n;
         int my_lab = -1;
@@ -199,7 +266,7 @@ lloyd_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restric
             }
         } else if (have) {
             // B operands: object 16c + l16, features 4s + g
-            float b[kCols][KS];
+            float bop[kCols][KS];
             float xsq[kCols];
 #pragma unroll
             for (int c = 0; c < kCols; ++c) {
@@ -209,12 +276,10 @@ lloyd_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restric
                 for (int s = 0; s < KS; ++s) {
                     float v = row[4 * s];
                     if ((M % 4) != 0 && s == KS - 1 && 4 * s + g >= M) v = 0.f;
-                    b[c][s] = v;
+                    bop[c][s] = v;
                     acc = __builtin_fmaf(v, v, acc);
                 }
-                acc += __shfl_xor(acc, 16, kWave);
-                acc += __shfl_xor(acc, 32, kWave);
-                xsq[c] = acc;
+                xsq[c] = sum_rows<32>(sum_rows<16>(acc));
             }
             float b1[kCols], b2[kCols];
             int lb[kCols];
@@ -236,7 +301,7 @@ lloyd_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restric
                 for (int s = 0; s < KS; ++s)
 #pragma unroll
                     for (int c = 0; c < kCols; ++c)
-                        d[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], b[c][s], d[c], 0, 0, 0);
+                        d[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], bop[c][s], d[c], 0, 0, 0);
                 const int kb = tt * 16 + 4 * g;
 #pragma unroll
                 for (int c = 0; c < kCols; ++c)
@@ -249,23 +314,12 @@ lloyd_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restric
                         lb[c] = lt ? kb + r : lb[c];
                     }
             }
-            // merge the four lanes that hold the same object (no branches: the
-            // second best of two (best, second) pairs is the median of
-            // (b1, pb1, min(b2, pb2)) when b1 <= b2 and pb1 <= pb2)
+            // merge the four lanes that hold the same object (rows r, r^1, r^2)
 #pragma unroll
-            for (int c = 0; c < kCols; ++c)
-#pragma unroll
-                for (int off = 16; off <= 32; off <<= 1) {
-                    const float pb1 = __shfl_xor(b1[c], off, kWave);
-                    const float pb2 = __shfl_xor(b2[c], off, kWave);
-                    const int pl = __shfl_xor(lb[c], off, kWave);
-                    const float m2 = __builtin_amdgcn_fmed3f(b2[c], pb2, -INFINITY);
-                    const float nb2 = __builtin_amdgcn_fmed3f(b1[c], pb1, m2);
-                    const bool take = (pb1 < b1[c]) | ((pb1 == b1[c]) & (pl < lb[c]));
-                    b1[c] = take ? pb1 : b1[c];
-                    lb[c] = take ? pl : lb[c];
-                    b2[c] = nb2;
-                }
+            for (int c = 0; c < kCols; ++c) {
+                merge_rows<16>(b1[c], b2[c], lb[c]);
+                merge_rows<32>(b1[c], b2[c], lb[c]);
+            }
             // lane l reports object l, which sits in column c = l / 16 = g
             float mb1 = b1[0], mb2 = b2[0], mx = xsq[0];
             int ml = lb[0];
@@ -281,11 +335,8 @@ lloyd_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restric
             const bool ok = (K == 1) || (mb2 - mb1 > thr);
             float dmin = 0.f;
             if (valid && !ok) {
-                float x[M];
-#pragma unroll
-                for (int j = 0; j < M; ++j) x[j] = tile[lane * M + j];
                 double bd;
-                ml = argmin_fp64<M>(x, C, K, bd);
+                ml = argmin_fp64<M>(tile + lane * M, C, K, bd);
                 dmin = (float)bd;
             } else if (valid && MODE == kAssign && min_d2 != nullptr) {
                 const float *c = C + (int64_t)ml * M;
@@ -305,10 +356,8 @@ lloyd_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restric
             }
         }
 
-        if (kAcc == kAccWave) {
-            double *slab = reinterpret_cast<double *>(smem + L.slab) + (size_t)wave * K * MW;
-            wave_accumulate<M>(valid ? my_lab : -1, tile, ones, slab, K, lane);
-            __builtin_amdgcn_wave_barrier();
+        if (kWaveForm) {
+            if (have) accumulate_tile<M, PA>(valid ? my_lab : -1, tile, offs, wslabs, K, lane);
         } else if (kAcc == kAccBlock) {
             int32_t *labs = reinterpret_cast<int32_t *>(smem + L.labs);
             int32_t *members = reinterpret_cast<int32_t *>(smem + L.members) + wave * W * kWave;
@@ -326,7 +375,7 @@ lloyd_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restric
                     const uint64_t mask = __ballot(mine);
                     const int rank = __builtin_amdgcn_mbcnt_hi(
                         (uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
-                    if (mine) members[cnt_k + rank] = v * kTilePad + lane * M;
+                    if (mine) members[cnt_k + rank] = v * kSlot + lane * M;
                     cnt_k += __popcll(mask);
                 }
                 if (cnt_k == 0) continue;
@@ -350,25 +399,29 @@ lloyd_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restric
             }
             __syncthreads();
         }
+    };
+
+    // Block tiles are taken in strides of the grid; the register buffers
+    // alternate. Every wave of a workgroup runs the same steps (the block form
+    // has barriers inside).
+    for (int64_t bt = bt0; bt < nbt_main; bt += 2 * G) {
+        step(bt, std::integral_constant<int, 0>{}, true);
+        if (bt + G < nbt_main) step(bt + G, std::integral_constant<int, 1>{}, true);
+    }
+    if (nbt_main < nbt && nbt_main >= bt0 && (nbt_main - bt0) % G == 0) {
+        const int64_t q = nbt_main * W + wave;
+        if (q < nfull) load_tile<M>(X, q, lane, buf[0]);
+        else if (q < nq) load_tail_tile<M>(X, n, q, lane, buf[0]);
+        step(nbt_main, std::integral_constant<int, 0>{}, false);
     }
 
     if (ctl != nullptr && lane == 0 && nfallback > 0) atomicAdd(&ctl->fallbacks, nfallback);
 
-    if (kAcc == kAccWave) {
+    if (kWaveForm) {
         __syncthreads();
-        const double *slabs = reinterpret_cast<const double *>(smem + L.slab);
-        double *out = part_sums + (int64_t)blockIdx.x * K * M;
-        for (int e = tid; e < K * M; e += blockDim.x) {
-            const int k = e / M, j = e - (e / M) * M;
-            double s = slabs[k * MW + j];
-            for (int w = 1; w < W; ++w) s = s + slabs[(size_t)w * K * MW + k * MW + j];
-            out[e] = s;
-        }
-        for (int k = tid; k < K; k += blockDim.x) {
-            double c = 0.0;
-            for (int w = 0; w < W; ++w) c = c + slabs[(size_t)w * K * MW + k * MW + M];
-            part_counts[(int64_t)blockIdx.x * K + k] = (int32_t)c;
-        }
+        write_wave_partials<M, PA>(reinterpret_cast<const double *>(smem + L.slab), W, K,
+                               part_sums + (int64_t)blockIdx.x * K * M,
+                               part_counts + (int64_t)blockIdx.x * K);
     } else if (kAcc == kAccBlock) {
         const double *slab = reinterpret_cast<const double *>(smem + L.slab);
         const int32_t *cnt = reinterpret_cast<const int32_t *>(smem + L.cnt);
@@ -405,18 +458,25 @@ hipError_t launch_m(const StepArgs &a, Mode mode, const AccumPlan &p, hipStream_
     const dim3 grid(p.groups), block(p.waves * kWave);
     const TreeArgs tr = tree_args(a, p.groups);
 #define LLOYD_MFMA_LAUNCH(MD, AC)                                                              \
-    hipLaunchKernelGGL((lloyd_mfma_kernel<M, MD, AC>), grid, block, p.lds_bytes, s, a.X, a.n,   \
-                       a.C, a.K, a.labels, a.labels_in, a.min_d2, a.part_sums, a.part_counts,  \
-                       a.ctl, a.t, a.fixed, tr)
-    const bool wave_acc = p.accum == kAccWave;
+    do {                                                                                       \
+        auto kern = lloyd_tile_kernel<M, MD, AC>;                                              \
+        static const size_t st = static_lds_bytes(reinterpret_cast<const void *>(kern));       \
+        if (st > (size_t)kMaxLds || st + p.lds_bytes > (size_t)kMaxLds)                        \
+            return hipErrorInvalidConfiguration;                                               \
+        hipLaunchKernelGGL(kern, grid, block, p.lds_bytes, s, a.X, a.n, a.C, a.K, a.labels,    \
+                           a.labels_in, a.min_d2, a.part_sums, a.part_counts, a.ctl, a.t,      \
+                           a.fixed, tr);                                                       \
+    } while (0)
     switch (mode) {
-    case kAssign: LLOYD_MFMA_LAUNCH(kAssign, kAccWave); break;
+    case kAssign: LLOYD_MFMA_LAUNCH(kAssign, 0); break;
     case kAssignAccum:
-        if (wave_acc) LLOYD_MFMA_LAUNCH(kAssignAccum, kAccWave);
+        if (p.accum == kAccWave) LLOYD_MFMA_LAUNCH(kAssignAccum, kAccWave);
+        else if (p.accum == kAccWave1) LLOYD_MFMA_LAUNCH(kAssignAccum, kAccWave1);
         else LLOYD_MFMA_LAUNCH(kAssignAccum, kAccBlock);
         break;
     case kAccumLabels:
-        if (wave_acc) LLOYD_MFMA_LAUNCH(kAccumLabels, kAccWave);
+        if (p.accum == kAccWave) LLOYD_MFMA_LAUNCH(kAccumLabels, kAccWave);
+        else if (p.accum == kAccWave1) LLOYD_MFMA_LAUNCH(kAccumLabels, kAccWave1);
         else LLOYD_MFMA_LAUNCH(kAccumLabels, kAccBlock);
         break;
     }
@@ -439,7 +499,7 @@ constexpr auto make_table(std::integer_sequence<int, Is...>)
 
 }  // namespace
 
-hipError_t LLOYD_PART_FN(launch_mfma_part)(const StepArgs &a, Mode mode, const AccumPlan &plan, hipStream_t s)
+hipError_t LLOYD_PART_FN(launch_tile_part)(const StepArgs &a, Mode mode, const AccumPlan &plan, hipStream_t s)
 {
     static constexpr auto table = make_table(std::make_integer_sequence<int, kPartN>{});
     if (a.M < kPartLo || a.M >= kPartLo + kPartN) return hipErrorInvalidValue;
@@ -447,23 +507,33 @@ hipError_t LLOYD_PART_FN(launch_mfma_part)(const StepArgs &a, Mode mode, const A
 }
 
 #if LLOYD_PART == 0
-AccumPlan plan_mfma(int64_t n, int M, int K, Mode mode)
+AccumPlan plan_tile(int64_t n, int M, int K, Mode mode)
 {
     AccumPlan p{};
-    p.path = kPathMfma;
+    p.path = kPathTile;
     const int64_t nq = (n + kWave - 1) / kWave;
     auto fits = [&](int W, int acc) { return mfma_lds(M, K, W, acc).total <= (size_t)kMaxLds; };
+    auto most_waves = [&](int acc) {      // 0 when not even one wave fits
+        int w = kMaxWaves;
+        while (w > 0 && !fits(w, acc)) --w;
+        return w;
+    };
     int W = kMaxWaves, acc = 0;
     if (mode == kAssign) {
-        while (W > 1 && !fits(W, 0)) W /= 2;
+        W = most_waves(0);
     } else {
-        // private slabs while at least 8 waves fit, else one shared slab
-        acc = kAccWave;
-        while (W > 8 && !fits(W, kAccWave)) --W;
-        if (!fits(W, kAccWave)) {
+        // private slabs (the most objects per step that leaves the most waves)
+        // while at least kMinWaveForm waves fit, else one shared slab
+        const int w_p = most_waves(kAccWave), w_1 = most_waves(kAccWave1);
+        if (w_p >= kMinWaveForm && w_p >= w_1) {
+            acc = kAccWave;
+            W = w_p;
+        } else if (w_1 >= kMinWaveForm) {
+            acc = kAccWave1;
+            W = w_1;
+        } else {
             acc = kAccBlock;
-            W = kMaxWaves;
-            while (W > 1 && !fits(W, kAccBlock)) W /= 2;
+            W = most_waves(kAccBlock);
         }
     }
     // no more waves than there are 64-object tiles
@@ -477,16 +547,16 @@ AccumPlan plan_mfma(int64_t n, int M, int K, Mode mode)
     return p;
 }
 
-bool mfma_fits(int M, int K)
+bool tile_fits(int M, int K)
 {
     return mfma_lds(M, K, 1, kAccBlock).total <= (size_t)kMaxLds;
 }
 
-hipError_t launch_mfma(const StepArgs &a, Mode mode, const AccumPlan &plan, hipStream_t s)
+hipError_t launch_tile(const StepArgs &a, Mode mode, const AccumPlan &plan, hipStream_t s)
 {
     if (a.M < 1 || a.M > kMaxM) return hipErrorInvalidValue;
     switch ((a.M - 1) / (kMaxM / LLOYD_PARTS)) {
-#define LLOYD_CASE(P) case P: return launch_mfma_part_##P(a, mode, plan, s);
+#define LLOYD_CASE(P) case P: return launch_tile_part_##P(a, mode, plan, s);
         LLOYD_PART_CASES
 #undef LLOYD_CASE
     }

@@ -42,7 +42,8 @@ def test_header_constants_match_binding():
                  "KMEANS_EHIP"]:
         m = re.search(rf"#define {name}\s+(-?\d+)", text)
         assert int(m.group(1)) == getattr(km, name)
-    for name in ["KMEANS_FIXED_ITERS", "KMEANS_PATH_DIRECT", "KMEANS_PATH_MFMA"]:
+    for name in ["KMEANS_FIXED_ITERS", "KMEANS_PATH_DIRECT", "KMEANS_PATH_MFMA",
+                 "KMEANS_PATH_TILES"]:
         m = re.search(rf"#define {name}\s+\(1u << (\d+)\)", text)
         assert (1 << int(m.group(1))) == getattr(km, name)
 
@@ -92,6 +93,9 @@ def _run(X=FAKE, n=100, M=4, K=3, init=FAKE, max_iter=5, flags=0, labels=FAKE, C
     (dict(K=1025), km.KMEANS_EUNSUPPORTED), (dict(M=64, K=257), km.KMEANS_EUNSUPPORTED),
     (dict(n=2**31), km.KMEANS_EUNSUPPORTED), (dict(X=FAKE_MISALIGNED), km.KMEANS_EINVAL),
     (dict(flags=km.KMEANS_PATH_DIRECT | km.KMEANS_PATH_MFMA), km.KMEANS_EINVAL),
+    (dict(flags=km.KMEANS_PATH_TILES | km.KMEANS_PATH_MFMA), km.KMEANS_EINVAL),
+    (dict(flags=km.KMEANS_PATH_TILES | km.KMEANS_PATH_DIRECT), km.KMEANS_EINVAL),
+    (dict(flags=km.KMEANS_PATH_TILES, M=16, K=1024), km.KMEANS_EUNSUPPORTED),
     (dict(flags=1 << 7), km.KMEANS_EINVAL),
 ])
 def test_assign_validation(kw, code):
@@ -117,6 +121,8 @@ def test_update_validation(kw, code):
     (dict(max_iter=-3), km.KMEANS_EINVAL), (dict(K=0), km.KMEANS_EINVAL),
     (dict(K=2000), km.KMEANS_EUNSUPPORTED), (dict(X=FAKE_MISALIGNED), km.KMEANS_EINVAL),
     (dict(flags=km.KMEANS_PATH_DIRECT | km.KMEANS_PATH_MFMA), km.KMEANS_EINVAL),
+    (dict(flags=km.KMEANS_PATH_MFMA | km.KMEANS_PATH_TILES), km.KMEANS_EINVAL),
+    (dict(flags=km.KMEANS_PATH_TILES, M=16, K=1024, wsb=1 << 30), km.KMEANS_EUNSUPPORTED),
     (dict(flags=1 << 5), km.KMEANS_EINVAL), (dict(ws=None), km.KMEANS_EWORKSPACE),
     (dict(wsb=16), km.KMEANS_EWORKSPACE),
 ])

@@ -48,9 +48,10 @@ def check_labels(lab, olab, gap):
 
 def outside_mfma_envelope(n, M, K, path):
     """A forced matrix-core path is refused (EUNSUPPORTED) exactly when its
-    workgroup state does not fit in LDS; the library reports that as a zero
-    workspace size."""
-    return path == "mfma" and km.kmeans_workspace_bytes(n, M, K, km.KMEANS_PATH_MFMA) == 0
+    workgroup state does not fit (the library reports that as a zero workspace
+    size)."""
+    flag = {"mfma": km.KMEANS_PATH_MFMA, "tiles": km.KMEANS_PATH_TILES}.get(path)
+    return flag is not None and km.kmeans_workspace_bytes(n, M, K, flag) == 0
 
 
 def run_parity(X, init, K, max_iter, fixed=False, path=None, name=""):
@@ -99,7 +100,7 @@ SHAPES = [
 ]
 
 
-PATHS = ["direct", "mfma"]
+PATHS = ["direct", "mfma", "tiles"]
 
 
 @pytest.mark.parametrize("path", PATHS)
