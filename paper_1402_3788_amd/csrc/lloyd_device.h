@@ -175,6 +175,58 @@ __device__ inline void accumulate_tile(int lab, const float *tile, int32_t *offs
     __builtin_amdgcn_wave_barrier();
 }
 
+// The same accumulation in two parts, so the tile's feature reads (which do
+// not depend on the labels) can be issued before the assignment and wait in
+// registers: accumulate_fetch reads every step's value for this lane,
+// accumulate_commit adds them once the labels are known.
+template <int M, int P_>
+struct AccFetch {
+    float x[WaveAcc<M, P_>::kSteps];
+};
+
+template <int M, int P_>
+__device__ inline void accumulate_fetch(const float *tile, int lane, AccFetch<M, P_> &f)
+{
+    using A = WaveAcc<M, P_>;
+    constexpr int LW = A::LW, P = A::P;
+    const int h = lane / LW, j = lane % LW;
+    const float *xp = tile + h * M + (j < M ? j : M);
+#pragma unroll
+    for (int s = 0; s < A::kSteps; ++s) f.x[s] = xp[s * P * M];
+}
+
+template <int M, int P_>
+__device__ inline void accumulate_commit(int lab, const AccFetch<M, P_> &f, int32_t *offs,
+                                         double *slabs, int K, int lane)
+{
+    using A = WaveAcc<M, P_>;
+    constexpr int MW = A::MW, LW = A::LW, P = A::P;
+    offs[lane] = lab >= 0 ? ((lane % P) * K + lab) * MW : -1;
+    __builtin_amdgcn_wave_barrier();
+    const int h = lane / LW, j = lane % LW;
+    const int32_t *op = offs + h;
+    const bool feat = j < M;
+    const bool used = j <= M;
+    constexpr int B = A::kSteps < 16 ? A::kSteps : 16;
+#pragma unroll
+    for (int s0 = 0; s0 < A::kSteps; s0 += B) {
+        int o[B];
+#pragma unroll
+        for (int b = 0; b < B; ++b) o[b] = op[(s0 + b) * P];
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+            const double v = feat ? (double)f.x[s0 + b] : 1.0;
+            if (used && o[b] >= 0)
+                __hip_atomic_fetch_add(slabs + o[b] + j, v, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_WAVEFRONT);
+            if (M + 1 > kWave && lane == 0 && o[b] >= 0)   // M = 64: no lane left for the count
+                __hip_atomic_fetch_add(slabs + o[b] + M, 1.0, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_WAVEFRONT);
+        }
+    }
+    __builtin_amdgcn_wave_barrier();
+}
+
 // Workgroup partial of the wave-accumulation form: for every (cluster, feature)
 // the sum over waves w and slabs h (w, then h, ascending) written to
 // part_sums[K][M], and the counts to part_counts[K]. Call after a barrier.

@@ -168,6 +168,11 @@ lloyd_lane_kernel(const float *__restrict__ X, int64_t n, const float *__restric
 
         const int64_t i = qq_ * kWave + lane;
         const bool valid = i < n;
+        // the accumulation's feature reads go out now and wait in registers
+        // (matrix-core form, where the registers are there)
+        constexpr bool kEarly = kMfma && WaveAcc<M, PA>::kSteps <= 32;
+        AccFetch<M, PA> af;
+        if (MODE != kAssign && kEarly) accumulate_fetch<M, PA>(tile, lane, af);
         int lab;
         if (MODE == kAccumLabels) {
             lab = valid ? labels_in[i] : -1;
@@ -262,7 +267,10 @@ lloyd_lane_kernel(const float *__restrict__ X, int64_t n, const float *__restric
             if (!valid) lab = -1;
         }
 
-        if (MODE != kAssign) accumulate_tile<M, PA>(lab, tile, offs, slabs, K, lane);
+        if (MODE != kAssign) {
+            if (kEarly) accumulate_commit<M, PA>(lab, af, offs, slabs, K, lane);
+            else accumulate_tile<M, PA>(lab, tile, offs, slabs, K, lane);
+        }
     };
 
     if (kDepth == 1) {

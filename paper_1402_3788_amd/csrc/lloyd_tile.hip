@@ -25,7 +25,8 @@
 // fixed operation order, over all centres, lowest index on ties.
 //
 // Each wavefront streams 64-object tiles: the next two tiles' loads are in
-// flight in registers while the current tile is staged in the wave's LDS slot.
+// flight in registers while the current tile is staged in the wave's LDS slot;
+// the ragged last tile (n not a multiple of 64) is handled after the loop.
 //
 // Accumulation (the sums of Eq. (1)) has two forms, both free of atomics across
 // lanes that share an address and with every addition in an order fixed by the
@@ -35,9 +36,9 @@
 //              at the end the workgroup adds the slabs in a fixed order. Used
 //              while W >= 4 waves' private slabs fit in LDS (small K*M).
 //   block   -- one fp64 slab per workgroup: after a barrier, wave w owns the
-//              clusters k = w, w+W, ...; for each it lists the workgroup tile's
-//              members in ascending object order (ballot + prefix count) and
-//              adds them. Used for large K*M.
+//              clusters k with k % W == w; it lists their members over the
+//              workgroup's W tiles in (tile, object) order (ballot + prefix
+//              count) and adds them one member per step. Used for large K*M.
 #include "lloyd.h"
 #include "lloyd_device.h"
 #include "lloyd_reduce.h"
@@ -65,7 +66,7 @@ constexpr int kMaxWaves = 8;
 
 // LDS carve-up of a workgroup (dynamic shared memory).
 struct MfmaLds {
-    size_t aswz, cnorm, misc, tiles, offs, labs, members, scratch, slab, cnt, total;
+    size_t aswz, cnorm, misc, tiles, offs, labs, members, slab, total;
     int tile_floats;
 };
 
@@ -80,9 +81,13 @@ __host__ __device__ inline int wave_acc_p(int M, int acc)
     return kWave / lw;
 }
 
+// 16-centre blocks, rounded up to an even count (the assignment loop works on
+// pairs of blocks; the padding centres score +inf).
+__host__ __device__ inline int centre_blocks(int K) { return ((K + 15) / 16 + 1) / 2 * 2; }
+
 __host__ __device__ inline MfmaLds mfma_lds(int M, int K, int W, int acc)
 {
-    const int KS = (M + 3) / 4, KT = (K + 15) / 16;
+    const int KS = (M + 3) / 4, KT = centre_blocks(K);
     MfmaLds L{};
     L.tile_floats = (kWave * M + (M > 4 ? M : 4) + 3) / 4 * 4;    // TileGeom<M>::kSlot
     size_t o = 0;
@@ -96,9 +101,7 @@ __host__ __device__ inline MfmaLds mfma_lds(int M, int K, int W, int acc)
     } else if (acc == kAccBlock) {
         L.labs = o;    o = al16(o + (size_t)W * kWave * 4);
         L.members = o; o = al16(o + (size_t)W * W * kWave * 4);
-        L.scratch = o; o = al16(o + (size_t)W * kWave * 8);
-        L.slab = o;    o = al16(o + (size_t)K * M * 8);
-        L.cnt = o;     o = al16(o + (size_t)K * 4);
+        L.slab = o;    o = al16(o + (size_t)K * (M + 1) * 8);
     }
     L.total = o;
     return L;
@@ -163,7 +166,7 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
     const int W = blockDim.x / kWave;
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int tid = threadIdx.x;
-    const int KT = (K + 15) / 16;
+    const int KT = centre_blocks(K);       // even
 
     if (MODE == kAssignAccum && stop_before(ctl, t, fixed)) return;
 
@@ -210,9 +213,7 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
         for (int i = tid; i < W * kP * K * (M + 1); i += blockDim.x) slabs[i] = 0.0;
     } else if (kAcc == kAccBlock) {
         double *slab = reinterpret_cast<double *>(smem + L.slab);
-        int32_t *cnt = reinterpret_cast<int32_t *>(smem + L.cnt);
-        for (int i = tid; i < K * M; i += blockDim.x) slab[i] = 0.0;
-        for (int i = tid; i < K; i += blockDim.x) cnt[i] = 0;
+        for (int i = tid; i < K * (M + 1); i += blockDim.x) slab[i] = 0.0;
     }
     __syncthreads();
     if (MODE != kAccumLabels) {
@@ -289,19 +290,28 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
                 b2[c] = INFINITY;
                 lb[c] = 0;
             }
-            for (int tt = 0; tt < KT; ++tt) {
+            // operands of centre block tt (A in lane order, seeds |c|^2)
+            struct Ops {
                 float a[KS];
+                f4v c0;
+            };
+            auto load_ops = [&](int tt, Ops &o) {
 #pragma unroll
-                for (int s = 0; s < KS; ++s) a[s] = aswz[(tt * KS + s) * kWave + lane];
-                f4v d[kCols];
-                const f4v cinit = *reinterpret_cast<const f4v *>(cnorm + tt * 16 + 4 * g);
+                for (int s = 0; s < KS; ++s) o.a[s] = aswz[(tt * KS + s) * kWave + lane];
+                o.c0 = *reinterpret_cast<const f4v *>(cnorm + tt * 16 + 4 * g);
+            };
+            // scores of one centre block for the four columns
+            auto chain = [&](const Ops &o, f4v (&d)[kCols]) {
 #pragma unroll
-                for (int c = 0; c < kCols; ++c) d[c] = cinit;
+                for (int c = 0; c < kCols; ++c) d[c] = o.c0;
 #pragma unroll
                 for (int s = 0; s < KS; ++s)
 #pragma unroll
                     for (int c = 0; c < kCols; ++c)
-                        d[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], bop[c][s], d[c], 0, 0, 0);
+                        d[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(o.a[s], bop[c][s], d[c], 0, 0, 0);
+            };
+            // running best / second best / label over the lane's 4 centres
+            auto scan = [&](int tt, const f4v (&d)[kCols]) {
                 const int kb = tt * 16 + 4 * g;
 #pragma unroll
                 for (int c = 0; c < kCols; ++c)
@@ -313,7 +323,28 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
                         b1[c] = lt ? sc : b1[c];
                         lb[c] = lt ? kb + r : lb[c];
                     }
+            };
+            // Two accumulator sets and two operand sets: the matrix cores
+            // compute one block while the vector ALU scans the previous one and
+            // the next block's operands arrive from LDS (no branch inside the
+            // loop body).
+            f4v dA[kCols], dB[kCols];
+            Ops oA, oB;
+            load_ops(0, oA);
+            load_ops(1, oB);
+            chain(oA, dA);
+            int tt = 0;
+            for (; tt + 2 < KT; tt += 2) {
+                load_ops(tt + 2, oA);
+                chain(oB, dB);
+                scan(tt, dA);
+                load_ops(tt + 3, oB);
+                chain(oA, dA);
+                scan(tt + 1, dB);
             }
+            chain(oB, dB);
+            scan(tt, dA);
+            scan(tt + 1, dB);
             // merge the four lanes that hold the same object (rows r, r^1, r^2)
 #pragma unroll
             for (int c = 0; c < kCols; ++c) {
@@ -359,43 +390,74 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
         if (kWaveForm) {
             if (have) accumulate_tile<M, PA>(valid ? my_lab : -1, tile, offs, wslabs, K, lane);
         } else if (kAcc == kAccBlock) {
+            // Wave w owns the clusters k with k % W == w (W is a power of two).
+            // After a barrier it lists the members of its clusters over the
+            // workgroup's W tiles in (tile, object) order (ballot + prefix
+            // count), in two lists by the parity of k / W when a row fits in 32
+            // lanes, and adds them: per step, each half-wave takes the next
+            // member of its list, lane j adds feature j and lane M the count
+            // into the workgroup slab rows this wave owns. Two lanes of one step
+            // never share a row, every row is written by one wave only, and the
+            // order of its additions is fixed by the data.
             int32_t *labs = reinterpret_cast<int32_t *>(smem + L.labs);
-            int32_t *members = reinterpret_cast<int32_t *>(smem + L.members) + wave * W * kWave;
-            double *scratch = reinterpret_cast<double *>(smem + L.scratch) + wave * kWave;
+            int32_t *list = reinterpret_cast<int32_t *>(smem + L.members) + wave * W * kWave;
             double *slab = reinterpret_cast<double *>(smem + L.slab);
-            int32_t *cnt = reinterpret_cast<int32_t *>(smem + L.cnt);
-            constexpr int P = kWave / M;
+            constexpr int MW = M + 1;
+            constexpr bool kTwo = MW <= 32;            // two half-wave lists
+            const int cap = W * kWave;                 // list capacity
+            const int wshift = __builtin_ctz((unsigned)W);
             labs[wave * kWave + lane] = valid ? my_lab : -1;
             __syncthreads();
-            const int s = lane / M, j = lane % M;
-            for (int k = wave; k < K; k += W) {
-                int cnt_k = 0;
-                for (int v = 0; v < W; ++v) {
-                    const bool mine = labs[v * kWave + lane] == k;
-                    const uint64_t mask = __ballot(mine);
-                    const int rank = __builtin_amdgcn_mbcnt_hi(
-                        (uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
-                    if (mine) members[cnt_k + rank] = v * kSlot + lane * M;
-                    cnt_k += __popcll(mask);
-                }
-                if (cnt_k == 0) continue;
-                __builtin_amdgcn_wave_barrier();
-                double acc = 0.0;
-                if (s < P) {
-                    for (int base = 0; base < cnt_k; base += P) {
-                        const int idx = base + s;
-                        if (idx < cnt_k) acc = acc + (double)tiles[members[idx] + j];
+            int cnt0 = 0, cnt1 = 0;
+            for (int v = 0; v < W; ++v) {
+                const int l = labs[v * kWave + lane];
+                const bool mine = l >= 0 && (l & (W - 1)) == wave;
+                const bool odd = kTwo && ((l >> wshift) & 1);
+                // entry: label in the high half, the member's row offset in the
+                // low half (< W * kSlot <= 8 * 4160)
+                const int ent = (l << 16) | (v * kSlot + lane * M);
+                const uint64_t m0 = __ballot(mine && !odd);
+                const uint64_t m1 = __ballot(mine && odd);
+                const uint64_t mm = odd ? m1 : m0;
+                const int rank = __builtin_amdgcn_mbcnt_hi(
+                    (uint32_t)(mm >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mm, 0u));
+                if (mine && !odd) list[cnt0 + rank] = ent;
+                if (mine && odd) list[cap - 1 - (cnt1 + rank)] = ent;   // second list grows down
+                cnt0 += __popcll(m0);
+                cnt1 += __popcll(m1);
+            }
+            __builtin_amdgcn_wave_barrier();
+            const int h = kTwo ? (lane >> 5) : 0;
+            const int j = kTwo ? (lane & 31) : lane;
+            const bool feat = j < M;
+            const int jr = feat ? j : 0;
+            const int my_cnt = h ? cnt1 : cnt0;
+            const int steps = kTwo ? (cnt0 > cnt1 ? cnt0 : cnt1) : cnt0;
+            if (j <= M) {
+                constexpr int B = 8;
+                for (int e0 = 0; e0 < steps; e0 += B) {
+                    int ent[B];
+                    float xv[B];
+#pragma unroll
+                    for (int b = 0; b < B; ++b) {    // past the list: entry 0, ignored below
+                        const int e = e0 + b;
+                        ent[b] = e < my_cnt ? list[h ? cap - 1 - e : e] : 0;
+                    }
+#pragma unroll
+                    for (int b = 0; b < B; ++b) xv[b] = tiles[(ent[b] & 0xFFFF) + jr];
+#pragma unroll
+                    for (int b = 0; b < B; ++b) {
+                        if (e0 + b < my_cnt) {
+                            const double v = (double)(feat ? xv[b] : 1.0f);
+                            double *row = slab + (int64_t)(ent[b] >> 16) * MW;
+                            __hip_atomic_fetch_add(row + j, v, __ATOMIC_RELAXED,
+                                                   __HIP_MEMORY_SCOPE_WAVEFRONT);
+                            if (M + 1 > kWave && lane == 0)   // M = 64: no lane left for the count
+                                __hip_atomic_fetch_add(row + M, 1.0, __ATOMIC_RELAXED,
+                                                       __HIP_MEMORY_SCOPE_WAVEFRONT);
+                        }
                     }
                 }
-                scratch[lane] = acc;
-                __builtin_amdgcn_wave_barrier();
-                if (lane < M) {
-                    double tsum = 0.0;
-                    for (int u = 0; u < P; ++u) tsum = tsum + scratch[u * M + lane];
-                    slab[k * M + lane] = slab[k * M + lane] + tsum;
-                }
-                if (lane == 0) cnt[k] += cnt_k;
-                __builtin_amdgcn_wave_barrier();
             }
             __syncthreads();
         }
@@ -423,11 +485,12 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
                                part_sums + (int64_t)blockIdx.x * K * M,
                                part_counts + (int64_t)blockIdx.x * K);
     } else if (kAcc == kAccBlock) {
+        __syncthreads();
         const double *slab = reinterpret_cast<const double *>(smem + L.slab);
-        const int32_t *cnt = reinterpret_cast<const int32_t *>(smem + L.cnt);
         double *out = part_sums + (int64_t)blockIdx.x * K * M;
-        for (int e = tid; e < K * M; e += blockDim.x) out[e] = slab[e];
-        for (int k = tid; k < K; k += blockDim.x) part_counts[(int64_t)blockIdx.x * K + k] = cnt[k];
+        for (int e = tid; e < K * M; e += blockDim.x) out[e] = slab[(e / M) * (M + 1) + e % M];
+        for (int k = tid; k < K; k += blockDim.x)
+            part_counts[(int64_t)blockIdx.x * K + k] = (int32_t)slab[k * (M + 1) + M];
     }
     if (kAccum) tree_finalize(tree, reinterpret_cast<uint32_t *>(smem + L.slab));
 }
@@ -534,6 +597,7 @@ AccumPlan plan_tile(int64_t n, int M, int K, Mode mode)
         } else {
             acc = kAccBlock;
             W = most_waves(kAccBlock);
+            while (W & (W - 1)) --W;          // cluster ownership is k % W, W a power of two
         }
     }
     // no more waves than there are 64-object tiles
