@@ -37,7 +37,7 @@ METRIC = "Lloyd iters/sec and points·iters/sec at n=2e6,M=25,K=16; % of HBM pea
 # kernel that does the work of a step on each distance path, and the sources
 # it is built from (a committed counter summary is used only while they match)
 KERNELS = {
-    "lane-mfma": ("lloyd_lane_kernel<M, assign+accumulate, dist=mfma 4x4x1>",
+    "lane-mfma": ("lloyd_lane_kernel<M, assign+accumulate, dist=mfma 16x16x4>",
                   ["lloyd_lane.hip", "lloyd_device.h", "lloyd_reduce.h", "lloyd.h"]),
     "direct": ("lloyd_lane_kernel<M, assign+accumulate, dist=valu>",
                ["lloyd_lane.hip", "lloyd_device.h", "lloyd_reduce.h", "lloyd.h"]),

@@ -51,9 +51,9 @@ enum Mode : int {
 };
 
 // Distance paths: one object per lane with the direct form on the vector ALU
-// (lloyd_lane.hip), one object per lane with 4x4x1 matrix-core blocks (same
-// kernel, K <= 16), or 64-object tiles with 16x16x4 matrix-core blocks
-// (lloyd_tile.hip, any K).
+// (lloyd_lane.hip), one object per lane with the scores formed on 16x16x4
+// matrix-core blocks (same kernel, K <= 16), or 64-object tiles with 16x16x4
+// matrix-core blocks and a cross-lane argmin (lloyd_tile.hip, any K).
 enum Path : int { kPathValu = 0, kPathTile = 1, kPathLaneMfma = 2 };
 
 // Static LDS of a kernel (bytes), from the runtime's attributes; SIZE_MAX when

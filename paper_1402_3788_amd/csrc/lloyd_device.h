@@ -49,19 +49,23 @@ __device__ inline void load_tail_tile(const float *__restrict__ X, int64_t n, in
     const int nf = (int)(n * (int64_t)M - f0);          // floats present, < kFloats
 #pragma unroll
     for (int v = 0; v < G::kVecPerLane; ++v) {
-        const int idx = lane + kWave * v;
+        // lanes past the tile's last float4 read that one again, as in load_tile
+        const int idx0 = lane + kWave * v;
+        const int idx = idx0 < G::kVec ? idx0 : G::kVec - 1;
         float4 r = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (idx < G::kVec) {
-            const float *s = X + f0 + 4 * idx;
-            if (4 * idx + 0 < nf) r.x = s[0];
-            if (4 * idx + 1 < nf) r.y = s[1];
-            if (4 * idx + 2 < nf) r.z = s[2];
-            if (4 * idx + 3 < nf) r.w = s[3];
-        }
+        const float *s = X + f0 + 4 * idx;
+        if (4 * idx + 0 < nf) r.x = s[0];
+        if (4 * idx + 1 < nf) r.y = s[1];
+        if (4 * idx + 2 < nf) r.z = s[2];
+        if (4 * idx + 3 < nf) r.w = s[3];
         buf[v] = r;
     }
 }
 
+// Lanes past the tile's last float4 hold a copy of it (load_tile clamps their
+// index) and write it to the same place: every lane stores, with no branch, so
+// every load is waited for on every path (a masked store would leave the last
+// load's wait to a later, coarser one).
 template <int M>
 __device__ inline void store_tile(float *tile, int lane,
                                   const float4 (&buf)[TileGeom<M>::kVecPerLane])
@@ -71,15 +75,15 @@ __device__ inline void store_tile(float *tile, int lane,
 #pragma unroll
     for (int v = 0; v < G::kVecPerLane; ++v) {
         const int idx = lane + kWave * v;
-        if (idx < G::kVec) dst[idx] = buf[v];
+        dst[idx < G::kVec ? idx : G::kVec - 1] = buf[v];
     }
 }
 
 // fp64 squared distance in the reference operation order: for j ascending,
 // e = x_j - c_j, then d = d + e*e, every operation rounded on its own (this file
 // is compiled with -ffp-contract=off, so nothing is fused). xs: the object's M
-// features (in LDS); read per centre so the rare re-decision holds no fp64 copy
-// of the object in registers.
+// features; read per centre so the rare re-decision holds no fp64 copy of the
+// object in registers.
 template <int M>
 __device__ inline int argmin_fp64(const float *xs, const float *__restrict__ C, int K,
                                   double &best_out)
@@ -195,33 +199,60 @@ __device__ inline void accumulate_fetch(const float *tile, int lane, AccFetch<M,
     for (int s = 0; s < A::kSteps; ++s) f.x[s] = xp[s * P * M];
 }
 
-template <int M, int P_>
+// kFull: every object of the tile is present (lab >= 0 in every lane), so the
+// per-step validity test drops out and the lanes past the count column are
+// masked once for the whole tile.
+template <int M, int P_, bool kFull = false>
 __device__ inline void accumulate_commit(int lab, const AccFetch<M, P_> &f, int32_t *offs,
                                          double *slabs, int K, int lane)
 {
     using A = WaveAcc<M, P_>;
     constexpr int MW = A::MW, LW = A::LW, P = A::P;
-    offs[lane] = lab >= 0 ? ((lane % P) * K + lab) * MW : -1;
+    offs[lane] = (kFull || lab >= 0) ? ((lane % P) * K + lab) * MW : -1;
     __builtin_amdgcn_wave_barrier();
     const int h = lane / LW, j = lane % LW;
     const int32_t *op = offs + h;
     const bool feat = j < M;
     const bool used = j <= M;
     constexpr int B = A::kSteps < 16 ? A::kSteps : 16;
+    if constexpr (kFull && M + 1 <= kWave) {
+        if (used) {
+            double *col = slabs + j;
+            // 1.0f the optimiser cannot see through, so the count lane's select
+            // stays one 32-bit select ahead of the conversion instead of two
+            // 32-bit selects on the converted double
+            float one;
+            asm("v_mov_b32 %0, 1.0" : "=v"(one));
 #pragma unroll
-    for (int s0 = 0; s0 < A::kSteps; s0 += B) {
-        int o[B];
+            for (int s0 = 0; s0 < A::kSteps; s0 += B) {
+                int o[B];
 #pragma unroll
-        for (int b = 0; b < B; ++b) o[b] = op[(s0 + b) * P];
+                for (int b = 0; b < B; ++b) o[b] = op[(s0 + b) * P];
 #pragma unroll
-        for (int b = 0; b < B; ++b) {
-            const double v = feat ? (double)f.x[s0 + b] : 1.0;
-            if (used && o[b] >= 0)
-                __hip_atomic_fetch_add(slabs + o[b] + j, v, __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_WAVEFRONT);
-            if (M + 1 > kWave && lane == 0 && o[b] >= 0)   // M = 64: no lane left for the count
-                __hip_atomic_fetch_add(slabs + o[b] + M, 1.0, __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_WAVEFRONT);
+                for (int b = 0; b < B; ++b) {
+                    // the count column adds 1 (exact in fp64)
+                    const float x = feat ? f.x[s0 + b] : one;
+                    __hip_atomic_fetch_add(col + o[b], (double)x, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_WAVEFRONT);
+                }
+            }
+        }
+    } else {
+#pragma unroll
+        for (int s0 = 0; s0 < A::kSteps; s0 += B) {
+            int o[B];
+#pragma unroll
+            for (int b = 0; b < B; ++b) o[b] = op[(s0 + b) * P];
+#pragma unroll
+            for (int b = 0; b < B; ++b) {
+                const double v = feat ? (double)f.x[s0 + b] : 1.0;
+                if (used && o[b] >= 0)
+                    __hip_atomic_fetch_add(slabs + o[b] + j, v, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_WAVEFRONT);
+                if (M + 1 > kWave && lane == 0 && o[b] >= 0)   // M = 64: no lane left for the count
+                    __hip_atomic_fetch_add(slabs + o[b] + M, 1.0, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_WAVEFRONT);
+            }
         }
     }
     __builtin_amdgcn_wave_barrier();

@@ -5,25 +5,27 @@
 // order that depends only on the problem shape:
 //   1. the tile's 64*M fp32 values are streamed from HBM with 16-byte loads into
 //      the wave's LDS slot (the loads of the tile one or two strides ahead are
-//      issued before the current tile is processed) and each lane reads its
-//      own object's M features into registers;
+//      issued before the current tile is processed);
 //   2. assignment (Algorithm 1 steps 2/4, Eq. (2)), in one of two forms:
-//        DIST = kDistValu: the direct form |x - c|^2 on the vector ALU (centres
-//          are wave-uniform and come through scalar loads); its fp32 error is
-//          at most gamma_{M+1} |x - c|^2, so the two best distances are called
-//          in fp32 only when their gap exceeds 4 gamma_{M+2} of the second;
+//        DIST = kDistValu: each lane reads its own object's M features into
+//          registers and evaluates the direct form |x - c|^2 on the vector
+//          ALU (centres are wave-uniform and come through scalar loads); its
+//          fp32 error is at most gamma_{M+1} |x - c|^2, so the two best
+//          distances are called in fp32 only when their gap exceeds
+//          4 gamma_{M+2} of the second;
 //        DIST = kDistMfma: the expanded form score = |c|^2 - 2 x.c on the
-//          matrix cores with v_mfma_f32_4x4x1f32. That instruction runs 16
-//          independent 4x4 outer products; with A[i] = -2 c_{4q+i, f} in every
-//          group of four lanes and B = the lane's own x_f, register i of lane
-//          l accumulates sum_f -2 c_{4q+i, f} x_{l, f}. A chain over the M
-//          features plus one step with A = |c|^2, B = 1 leaves every lane
-//          with its own object's scores for centres 4q .. 4q+3, so a lane
-//          scans K scores of one object with no cross-lane merge. The -2C and
-//          |c|^2 operands stay in registers for the whole launch (K <= 16).
-//          The expanded form's fp32 error is bounded by
-//          gamma_{M+2} (3|c|^2 + |x|^2), so a label is accepted only if the
-//          two best scores differ by more than 2.5 times that bound;
+//          matrix cores with v_mfma_f32_16x16x4f32: A = -2C for 16 centres
+//          by 4 feature columns (plus the |c|^2 column, which meets B = 1),
+//          held in registers for the whole launch (K <= 16); B = 4 features
+//          of 16 objects, read from the tile. The four 16-object blocks of a
+//          tile are four independent chains of ceil((M+1)/4) products. Each
+//          lane ends with 4 scores of one object; they go back into the slot
+//          (which is no longer needed) as one row of 16 scores per object, so
+//          that each lane again scans the K scores of its own object with no
+//          cross-lane merge. The expanded form's fp32 error is bounded by
+//          gamma_{M+2} (3|c|^2 + |x|^2) whatever the summation order, so a
+//          label is accepted only if the two best scores differ by more than
+//          2.5 times that bound;
 //      either way, a lane whose call is too close recomputes all K distances
 //      in fp64 in the oracle's operation order and takes the lowest-index
 //      minimum, so the label is the exact-arithmetic argmin;
@@ -61,9 +63,17 @@ constexpr int kLaneMfmaMaxM = 27;
 // [W x P slabs]. The operand table (matrix-core form only) holds, for centre
 // quad qq and lane group r = lane % 4, the row -2 c_{4qq+r, 0..M-1}, |c|^2,
 // zero-padded to a multiple of 4 floats.
-__host__ __device__ inline size_t lane_tile_bytes(int M)
+// Scores written back per object by the matrix-core form: 16 centre scores
+// and the four partial |x|^2 of the lanes that held its features.
+constexpr int kScoreRow = 20;
+
+// Per-wave tile slot: the 64 objects plus slack; in the matrix-core form at
+// least 64 score rows, which reuse the slot once the tile has been read.
+__host__ __device__ inline size_t lane_tile_bytes(int M, bool mfma)
 {
-    return (size_t)((kWave * M + (M > 4 ? M : 4) + 3) / 4 * 4) * 4;
+    const size_t tile = (size_t)((kWave * M + (M > 4 ? M : 4) + 3) / 4 * 4) * 4;
+    const size_t scores = (size_t)kWave * kScoreRow * 4;
+    return mfma && scores > tile ? scores : tile;
 }
 
 __host__ __device__ inline int lane_atab_row(int M) { return (M + 1 + 3) / 4 * 4; }
@@ -84,7 +94,7 @@ __host__ __device__ inline size_t lane_atab_bytes(int M, bool mfma)
 
 __host__ __device__ inline size_t lane_slab_off(int M, int W, bool mfma)
 {
-    return lane_atab_bytes(M, mfma) + (size_t)W * (lane_tile_bytes(M) + kWave * 4);
+    return lane_atab_bytes(M, mfma) + (size_t)W * (lane_tile_bytes(M, mfma) + kWave * 4);
 }
 
 template <int M, int MODE, int PA, int DIST>
@@ -110,8 +120,10 @@ lloyd_lane_kernel(const float *__restrict__ X, int64_t n, const float *__restric
     constexpr int FP = (M + 1 + 3) / 4 * 4;               // operand table row (lane_atab_row)
     constexpr size_t kAtab = kMfma ? (size_t)KQ * 4 * FP * 4 : 0;   // lane_atab_bytes
     float *atab = reinterpret_cast<float *>(smem);
-    float *tile = reinterpret_cast<float *>(smem + kAtab) + wave * G::kSlot;
-    int32_t *offs = reinterpret_cast<int32_t *>(smem + kAtab + (size_t)W * G::kSlot * 4) + wave * kWave;
+    // tile slot in floats (lane_tile_bytes / 4)
+    constexpr int kSlotL = kMfma && kWave * kScoreRow > G::kSlot ? kWave * kScoreRow : G::kSlot;
+    float *tile = reinterpret_cast<float *>(smem + kAtab) + wave * kSlotL;
+    int32_t *offs = reinterpret_cast<int32_t *>(smem + kAtab + (size_t)W * kSlotL * 4) + wave * kWave;
     double *slabs_all = reinterpret_cast<double *>(smem + lane_slab_off(M, W, kMfma));
     double *slabs = slabs_all + (size_t)wave * kP * K * (M + 1);
 
@@ -153,24 +165,52 @@ lloyd_lane_kernel(const float *__restrict__ X, int64_t n, const float *__restric
         __syncthreads();
         for (int k = 0; k < K; ++k) cmax = fmaxf(cmax, atab[k * FP + M]);
     }
+    // A operands of the 16x16x4 products for the whole launch: k-step s covers
+    // table columns 4s .. 4s+3; lane l holds row l % 16 (centre), column
+    // 4s + l / 16.
+    constexpr int kKS = FP / 4;
+    float aop[kKS];
+#pragma unroll
+    for (int ks = 0; ks < kKS; ++ks)
+        aop[ks] = (kMfma && MODE != kAccumLabels) ? atab[(lane % 16) * FP + 4 * ks + lane / 16] : 0.f;
 
     // fp32 call thresholds (see the header comment)
     constexpr float kTau = 4.0f * (float)(M + 2) * 5.9604645e-8f;
     constexpr float kGuard = 2.5f * 1.01f * (float)(M + 2) * 5.9604645e-8f;
     int nfallback = 0;
 
-    auto step = [&](int64_t qq_, auto bi, bool prefetch) {
+    // A tile's labels (and distances) are stored at the start of the next step,
+    // after that step's tile has arrived and before its successor's loads are
+    // issued: the wait for those loads then never waits on a store issued
+    // just before it.
+    int64_t pend_i = -1;      // this lane's object whose label waits to be stored
+    int pend_lab = 0;
+    float pend_d2 = 0.f;
+    auto flush = [&]() {
+        if (pend_i >= 0) {
+            labels[pend_i] = pend_lab;
+            if (MODE == kAssign && min_d2 != nullptr) min_d2[pend_i] = pend_d2;
+        }
+    };
+
+    // full: a tile of the main loop (all 64 objects present; the loads of the
+    // tile kDepth strides ahead are issued here) rather than the partial last one
+    auto step = [&](int64_t qq_, auto bi, auto full) {
+        constexpr bool kFullTile = decltype(full)::value;
         float4 (&bb)[V] = buf[decltype(bi)::value];
         store_tile<M>(tile, lane, bb);
         __builtin_amdgcn_wave_barrier();
-        if (prefetch && qq_ + kDepth * stride < nfull)
+        if (MODE != kAccumLabels) flush();
+        if (kFullTile && qq_ + kDepth * stride < nfull)
             load_tile<M>(X, qq_ + kDepth * stride, lane, bb);
 
         const int64_t i = qq_ * kWave + lane;
-        const bool valid = i < n;
+        const bool valid = kFullTile || i < n;
         // the accumulation's feature reads go out now and wait in registers
         // (matrix-core form, where the registers are there)
         constexpr bool kEarly = kMfma && WaveAcc<M, PA>::kSteps <= 32;
+        static_assert(!kMfma || MODE != kAssignAccum || kEarly,
+                      "the matrix-core form reads the accumulation values before the scores overwrite the tile");
         AccFetch<M, PA> af;
         if (MODE != kAssign && kEarly) accumulate_fetch<M, PA>(tile, lane, af);
         int lab;
@@ -178,56 +218,79 @@ lloyd_lane_kernel(const float *__restrict__ X, int64_t n, const float *__restric
             lab = valid ? labels_in[i] : -1;
             if (lab < 0 || lab >= K) lab = -1;
         } else {
-            float x[M];
-#pragma unroll
-            for (int j = 0; j < M; ++j) x[j] = tile[lane * M + j];
             float b1 = INFINITY, b2 = INFINITY;
             lab = 0;
             bool ok;
-            if (kMfma) {
-                // the KQ chains interleaved feature by feature (independent
-                // accumulators keep the matrix pipe busy; each x_f is used by
-                // all chains and |x|^2 as soon as it arrives). All KQ chains
-                // run whatever K is: centres past K score +inf, so the code
-                // has no branch on K.
-                // A operands come from the operand table, four features per
-                // 16-byte read (four distinct addresses per read: broadcast).
-                f4v d[KQ];
+            if constexpr (kMfma) {
+                // v_mfma_f32_16x16x4f32 on four blocks of 16 objects: A = the
+                // operand table (16 centres x 4 columns, in aop), B = 4
+                // features x 16 objects read from the tile, the |c|^2 column
+                // meeting B = 1. Lane l ends with the scores of centres
+                // 4(l/16) .. 4(l/16)+3 for object 16b + l%16 of block b; it
+                // also sums the squares of the features it read (a quarter
+                // of |x|^2). The four blocks are four independent chains.
+                const int g = lane / 16, o16 = lane % 16;
+                f4v d[4];
+                float xp[4];
+                float bv[4][kKS];
 #pragma unroll
-                for (int qq = 0; qq < KQ; ++qq) d[qq] = f4v{0.f, 0.f, 0.f, 0.f};
-                float xsq = 0.f;
-                const float *arow = atab + (lane & 3) * FP;
+                for (int b = 0; b < 4; ++b) {
+                    d[b] = f4v{0.f, 0.f, 0.f, 0.f};
+                    xp[b] = 0.f;
 #pragma unroll
-                for (int f4 = 0; f4 < FP / 4; ++f4) {
-                    f4v a[KQ];
-#pragma unroll
-                    for (int qq = 0; qq < KQ; ++qq)
-                        a[qq] = *reinterpret_cast<const f4v *>(arow + qq * 4 * FP + 4 * f4);
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const int f = 4 * f4 + e;
-                        if (f > M) break;
-                        const float b = f < M ? x[f < M ? f : 0] : 1.0f;
-#pragma unroll
-                        for (int qq = 0; qq < KQ; ++qq)
-                            d[qq] = __builtin_amdgcn_mfma_f32_4x4x1f32(a[qq][e], b, d[qq], 0, 0, 0);
-                        if (f < M) xsq = __builtin_fmaf(b, b, xsq);
+                    for (int ks = 0; ks < kKS; ++ks) {
+                        const float v = tile[(16 * b + o16) * M + 4 * ks + g];
+                        if (4 * ks + 3 < M) {
+                            bv[b][ks] = v;
+                            xp[b] = __builtin_fmaf(v, v, xp[b]);
+                        } else {
+                            const int f = 4 * ks + g;
+                            const float xv = f < M ? v : 0.f;
+                            bv[b][ks] = f < M ? v : (f == M ? 1.0f : 0.f);
+                            xp[b] = __builtin_fmaf(xv, xv, xp[b]);
+                        }
                     }
                 }
 #pragma unroll
-                for (int qq = 0; qq < KQ; ++qq) {
+                for (int ks = 0; ks < kKS; ++ks) {
+#pragma unroll
+                    for (int b = 0; b < 4; ++b)
+                        d[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(aop[ks], bv[b][ks], d[b], 0, 0, 0);
+                }
+                // every read of the tile (features above, accumulation values
+                // before) precedes these writes in program order, and a wave's
+                // LDS operations complete in order: the score rows may reuse
+                // the slot. Row o: 16 scores, then the 4 partial |x|^2.
+#pragma unroll
+                for (int b = 0; b < 4; ++b) {
+                    float *row = tile + (16 * b + o16) * kScoreRow;
+                    *reinterpret_cast<f4v *>(row + 4 * g) = d[b];
+                    row[16 + g] = xp[b];
+                }
+                __builtin_amdgcn_wave_barrier();
+                f4v sc[4];
+#pragma unroll
+                for (int qq = 0; qq < 4; ++qq)
+                    sc[qq] = *reinterpret_cast<const f4v *>(tile + lane * kScoreRow + 4 * qq);
+                const f4v pp = *reinterpret_cast<const f4v *>(tile + lane * kScoreRow + 16);
+                const float xsq = ((pp[0] + pp[1]) + pp[2]) + pp[3];
+#pragma unroll
+                for (int qq = 0; qq < 4; ++qq) {
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
-                        const float sc = d[qq][r];
-                        const bool lt = sc < b1;
-                        b2 = __builtin_amdgcn_fmed3f(b1, b2, sc);
-                        b1 = lt ? sc : b1;
+                        const float v = sc[qq][r];
+                        const bool lt = v < b1;
+                        b2 = __builtin_amdgcn_fmed3f(b1, b2, v);
+                        b1 = lt ? v : b1;
                         lab = lt ? 4 * qq + r : lab;
                     }
                 }
                 const float thr = kGuard * (3.02f * cmax + 1.0001f * xsq) + 1e-30f;
                 ok = (K == 1) || (b2 - b1 > thr);
             } else {
+                float x[M];
+#pragma unroll
+                for (int j = 0; j < M; ++j) x[j] = tile[lane * M + j];
                 for (int k = 0; k < K; ++k) {
                     float d = 0.f;
 #pragma unroll
@@ -244,47 +307,51 @@ lloyd_lane_kernel(const float *__restrict__ X, int64_t n, const float *__restric
                 }
                 ok = (K == 1) || ((b2 - b1) > kTau * b2 && b2 >= 1e-30f);
             }
+            // the object's features from X: in the matrix-core form the slot
+            // now holds scores (both uses are off the common path)
             float dmin = kMfma ? 0.f : b1;
             if (valid && !ok) {
                 double bd;
-                lab = argmin_fp64<M>(tile + lane * M, C, K, bd);
+                lab = argmin_fp64<M>(X + i * M, C, K, bd);
                 dmin = (float)bd;
             } else if (kMfma && valid && MODE == kAssign && min_d2 != nullptr) {
+                const float *xg = X + i * M;
                 const float *c = C + (int64_t)lab * M;
                 float d = 0.f;
 #pragma unroll
                 for (int j = 0; j < M; ++j) {
-                    const float e = x[j] - c[j];
+                    const float e = xg[j] - c[j];
                     d = __builtin_fmaf(e, e, d);
                 }
                 dmin = d;
             }
             if (ctl != nullptr) nfallback += __popcll(__ballot(valid && !ok));
-            if (valid) {
-                labels[i] = lab;
-                if (MODE == kAssign && min_d2 != nullptr) min_d2[i] = dmin;
-            }
+            pend_i = valid ? i : -1;
+            pend_lab = lab;
+            pend_d2 = dmin;
             if (!valid) lab = -1;
         }
 
         if (MODE != kAssign) {
-            if (kEarly) accumulate_commit<M, PA>(lab, af, offs, slabs, K, lane);
+            // (labels read back may be out of range even in a full tile)
+            if (kEarly) accumulate_commit<M, PA, kFullTile && MODE != kAccumLabels>(lab, af, offs, slabs, K, lane);
             else accumulate_tile<M, PA>(lab, tile, offs, slabs, K, lane);
         }
     };
 
     if (kDepth == 1) {
-        for (int64_t q = q0; q < nfull; q += stride) step(q, std::integral_constant<int, 0>{}, true);
+        for (int64_t q = q0; q < nfull; q += stride) step(q, std::integral_constant<int, 0>{}, std::true_type{});
     } else {
         for (int64_t q = q0; q < nfull; q += 2 * stride) {
-            step(q, std::integral_constant<int, 0>{}, true);
-            if (q + stride < nfull) step(q + stride, std::integral_constant<int, 1>{}, true);
+            step(q, std::integral_constant<int, 0>{}, std::true_type{});
+            if (q + stride < nfull) step(q + stride, std::integral_constant<int, 1>{}, std::true_type{});
         }
     }
     if (nfull * kWave < n && nfull >= q0 && (nfull - q0) % stride == 0) {
         load_tail_tile<M>(X, n, nfull, lane, buf[0]);
-        step(nfull, std::integral_constant<int, 0>{}, false);
+        step(nfull, std::integral_constant<int, 0>{}, std::false_type{});
     }
+    if (MODE != kAccumLabels) flush();
 
     if (ctl != nullptr && lane == 0 && nfallback > 0) atomicAdd(&ctl->fallbacks, nfallback);
 
@@ -335,8 +402,13 @@ hipError_t launch_m(const StepArgs &a, Mode mode, const AccumPlan &p, hipStream_
     switch (mode) {
     case kAssign: LLOYD_LANE_LAUNCH(kAssign, 0); break;
     case kAssignAccum:
-        if (one) LLOYD_LANE_LAUNCH(kAssignAccum, 1);
-        else LLOYD_LANE_LAUNCH(kAssignAccum, 0);
+        if constexpr (DIST == kDistMfma) {
+            if (one) return hipErrorInvalidConfiguration;   // plan_lane never asks for it
+            LLOYD_LANE_LAUNCH(kAssignAccum, 0);
+        } else {
+            if (one) LLOYD_LANE_LAUNCH(kAssignAccum, 1);
+            else LLOYD_LANE_LAUNCH(kAssignAccum, 0);
+        }
         break;
     case kAccumLabels:
         if (one) LLOYD_LANE_LAUNCH(kAccumLabels, 1);
@@ -398,9 +470,10 @@ AccumPlan plan_lane(int64_t n, int M, int K, Mode mode, bool mfma)
         return w;
     };
     // slabs with the most objects per step unless one object per step leaves
-    // more waves
+    // more waves (not in the matrix-core form, whose accumulation reads the
+    // tile before the score rows overwrite it, which needs at most 32 steps)
     int pa = 0, W = most_waves(0);
-    if (mode != kAssign && most_waves(1) > W) {
+    if (mode != kAssign && !mfma && most_waves(1) > W) {
         pa = 1;
         W = most_waves(1);
     }
