@@ -62,15 +62,23 @@ extern "C" {
  * object per lane on the matrix cores for 5 <= K <= 16 (M <= 27), the vector
  * ALU otherwise. Every path gives the same labels, centres and counts. */
 
-/* Optional per-call timing, filled by kmeans_run when a non-NULL pointer is
- * passed: device time of the per-iteration launches (each one assigns,
- * accumulates, forms the centres and compares them), measured with HIP events
- * recorded on `stream` between consecutive launches. Timing adds one event
- * record per launch; in early-stop mode the intervals also contain the host's
- * convergence polls, so it is meant for KMEANS_FIXED_ITERS runs. */
+/* Optional per-call timing for kmeans_run (pass NULL for none). Each
+ * iteration is two launches on `stream`: assign + accumulate (Algorithm 1
+ * steps 2/4 and the sums of Eq. (1)), then the centres and the congruence test
+ * (Eq. (1), steps 6-7). HIP events are recorded on `stream` before the first
+ * and after the last launch of the call (step_ms), and around the assign +
+ * accumulate launch of every sample_every-th iteration (assign_ms). An event
+ * between two launches costs the stream several microseconds, so the sampled
+ * launches are kept few. In early-stop mode step_ms also contains the host's
+ * convergence polls; timing is meant for KMEANS_FIXED_ITERS runs.
+ *   in:  sample_every  (0 = every 16th iteration, 1 = every iteration)
+ *   out: the other fields */
 typedef struct kmeans_timing {
-    double  step_ms;          /* summed duration of the iteration launches */
-    int32_t step_launches;    /* number of intervals summed                 */
+    double  step_ms;          /* device time of the whole call's iterations    */
+    double  assign_ms;        /* summed duration of the sampled assign launches */
+    int32_t step_launches;    /* iterations covered by step_ms                 */
+    int32_t assign_samples;   /* launches summed in assign_ms                  */
+    int32_t sample_every;     /* in: sampling stride of the assign launches    */
     int32_t reserved;
 } kmeans_timing_t;
 

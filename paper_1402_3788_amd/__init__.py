@@ -38,8 +38,9 @@ EXPORTED = ("kmeans_workspace_bytes", "kmeans_strerror", "kmeans_assign", "kmean
 
 
 class KmeansTiming(ctypes.Structure):
-    _fields_ = [("step_ms", ctypes.c_double), ("step_launches", ctypes.c_int32),
-                ("reserved", ctypes.c_int32)]
+    _fields_ = [("step_ms", ctypes.c_double), ("assign_ms", ctypes.c_double),
+                ("step_launches", ctypes.c_int32), ("assign_samples", ctypes.c_int32),
+                ("sample_every", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class KmeansError(RuntimeError):
@@ -150,11 +151,13 @@ def kmeans_update(X: torch.Tensor, labels: torch.Tensor, K: int, prev_centers: t
 
 def kmeans_run(X: torch.Tensor, K: int, init_centers: torch.Tensor, max_iter: int,
                fixed_iters: bool = False, path=None, timing: bool = False,
-               out=None, ws: torch.Tensor | None = None):
+               out=None, ws: torch.Tensor | None = None, sample_every: int = 0):
     """Algorithm 1 steps 2-7 from init_centers (synchronous).
 
     Returns (labels, centers, counts, iterations), plus a KmeansTiming when
-    timing=True. `out` may supply (labels, centers, counts) tensors to reuse.
+    timing=True (events around the whole call and around the assign launch of
+    every sample_every-th iteration; 0 = every 16th). `out` may supply
+    (labels, centers, counts) tensors to reuse.
     """
     _check_x(X)
     n, M = X.shape
@@ -170,6 +173,8 @@ def kmeans_run(X: torch.Tensor, K: int, init_centers: torch.Tensor, max_iter: in
         ws = workspace(n, M, K, X.device, flags)
     iters = ctypes.c_int32(0)
     tm = KmeansTiming() if timing else None
+    if tm is not None:
+        tm.sample_every = int(sample_every)
     rc = _lib.kmeans_run(_dev_ptr(X), n, M, int(K), _dev_ptr(init), int(max_iter), flags,
                          _dev_ptr(labels), _dev_ptr(centers), _dev_ptr(counts),
                          ctypes.byref(iters), _dev_ptr(ws), ws.numel(), _stream_ptr(X.device),

@@ -2,7 +2,6 @@
 // and the iteration control of Algorithm 1 (steps 2-7). See include/kmeans.h.
 #include "../../include/kmeans.h"
 #include "lloyd.h"
-#include "lloyd_reduce.h"
 
 #include <vector>
 
@@ -62,13 +61,11 @@ hipError_t launch_step(const StepArgs &a, Mode mode, const AccumPlan &plan, hipS
     return plan.path == kPathTile ? launch_tile(a, mode, plan, s) : launch_lane(a, mode, plan, s);
 }
 
-// Workspace: [Ctl (256 B)] [fp64 group partials NG*K*M] [int32 group counts NG*K]
-//            [fp64 workgroup partials G*K*M] [int32 workgroup counts G*K]
-// with G the persistent workgroups of the accumulating launch and
-// NG = ceil(G / kGroup) the first-level reduction groups.
+// Workspace: [Ctl (256 B)] [fp64 workgroup partials G*K*M] [int32 workgroup
+// counts G*K], with G the persistent workgroups of the accumulating launch.
 struct Layout {
     AccumPlan plan;
-    size_t grp_sums_off, grp_counts_off, sums_off, counts_off, total;
+    size_t sums_off, counts_off, total;
 };
 
 Layout layout(int64_t n, int32_t M, int32_t K, uint32_t flags)
@@ -76,10 +73,7 @@ Layout layout(int64_t n, int32_t M, int32_t K, uint32_t flags)
     Layout L{};
     L.plan = plan_for(select_path(M, K, flags), n, M, K, kAssignAccum);
     const size_t km = (size_t)K * M;
-    const size_t ng = (size_t)(L.plan.groups + kGroup - 1) / kGroup;
-    L.grp_sums_off = align_up(sizeof(Ctl), 256);
-    L.grp_counts_off = align_up(L.grp_sums_off + ng * km * sizeof(double), 256);
-    L.sums_off = align_up(L.grp_counts_off + ng * K * sizeof(int32_t), 256);
+    L.sums_off = align_up(sizeof(Ctl), 256);
     L.counts_off = align_up(L.sums_off + (size_t)L.plan.groups * km * sizeof(double), 256);
     L.total = align_up(L.counts_off + (size_t)L.plan.groups * K * sizeof(int32_t), 256);
     return L;
@@ -89,8 +83,6 @@ void bind_workspace(StepArgs &a, const Layout &L, char *ws)
 {
     a.part_sums = reinterpret_cast<double *>(ws + L.sums_off);
     a.part_counts = reinterpret_cast<int32_t *>(ws + L.counts_off);
-    a.grp_sums = reinterpret_cast<double *>(ws + L.grp_sums_off);
-    a.grp_counts = reinterpret_cast<int32_t *>(ws + L.grp_counts_off);
     a.ctl = reinterpret_cast<Ctl *>(ws);
 }
 
@@ -156,7 +148,8 @@ int kmeans_update(const float *X, int64_t n, int32_t M, const int32_t *labels, i
     a.fixed = 1;
     a.compare = 0;
     if ((rc = hip_status(launch_ctl_reset(a.ctl, s)))) return rc;
-    return hip_status(launch_step(a, kAccumLabels, L.plan, s));
+    if ((rc = hip_status(launch_step(a, kAccumLabels, L.plan, s)))) return rc;
+    return hip_status(launch_centres(a, L.plan.groups, s));
 }
 
 int kmeans_run(const float *X, int64_t n, int32_t M, int32_t K, const float *init_centers,
@@ -194,6 +187,8 @@ int kmeans_run(const float *X, int64_t n, int32_t M, int32_t K, const float *ini
         if (rc) return rc;
     }
 
+    // events: [0] before the first launch, then pairs around the sampled
+    // assign launches, and the last one after the final launch
     std::vector<hipEvent_t> ev;
     auto mark = [&]() -> int {
         if (!timing) return KMEANS_OK;
@@ -202,15 +197,17 @@ int kmeans_run(const float *X, int64_t n, int32_t M, int32_t K, const float *ini
         ev.push_back(e);
         return hip_status(hipEventRecord(e, s));
     };
+    const int every = timing == nullptr ? 0 : (timing->sample_every > 0 ? timing->sample_every : 16);
     auto cleanup = [&]() {
         for (hipEvent_t e : ev) (void)hipEventDestroy(e);
     };
 
-    // One launch per iteration (assign, accumulate, centres and compare fused).
+    // Two launches per iteration: assign + accumulate (fused), then the centres
+    // and the congruence test from the workgroup partials.
     // Enqueue iterations in chunks; between chunks (early-stop mode only) read
     // the control block to learn whether the centres have become congruent.
     // Launches past convergence return at their first instruction.
-    int t = 1, chunk = 3;
+    int t = 1, chunk = 3, launched = 0;
     Ctl host{};
     rc = mark();
     while (!rc && t <= max_iter) {
@@ -218,8 +215,12 @@ int kmeans_run(const float *X, int64_t n, int32_t M, int32_t K, const float *ini
         const int end = (fixed || t + chunk - 1 >= max_iter) ? max_iter : t + chunk - 1;
         for (int tt = t; tt <= end && !rc; ++tt) {
             a.t = tt;
-            rc = hip_status(launch_step(a, kAssignAccum, L.plan, s));
-            if (!rc) rc = mark();
+            const bool sampled = every > 0 && (tt - 1) % every == 0;
+            if (sampled) rc = mark();
+            if (!rc) rc = hip_status(launch_step(a, kAssignAccum, L.plan, s));
+            if (!rc && sampled) rc = mark();
+            if (!rc) rc = hip_status(launch_centres(a, L.plan.groups, s));
+            ++launched;
         }
         t = end + 1;
         if (rc || t > max_iter) break;
@@ -228,6 +229,7 @@ int kmeans_run(const float *X, int64_t n, int32_t M, int32_t K, const float *ini
         if (rc || host.converged_at != 0) break;
         chunk = chunk * 2 < 64 ? chunk * 2 : 64;
     }
+    if (!rc) rc = mark();
     if (!rc) rc = hip_status(hipMemcpyAsync(&host, ctl, sizeof(Ctl), hipMemcpyDeviceToHost, s));
     if (!rc) rc = hip_status(hipStreamSynchronize(s));
     if (rc) {
@@ -238,16 +240,23 @@ int kmeans_run(const float *X, int64_t n, int32_t M, int32_t K, const float *ini
 
     if (timing) {
         timing->step_ms = 0.0;
-        timing->step_launches = 0;
+        timing->assign_ms = 0.0;
+        timing->step_launches = launched;
+        timing->assign_samples = 0;
         timing->reserved = 0;
-        for (size_t e = 0; e + 1 < ev.size(); ++e) {
-            float ms = 0.f;
-            if (hipEventElapsedTime(&ms, ev[e], ev[e + 1]) != hipSuccess) {
-                rc = KMEANS_EHIP;
-                break;
+        float ms = 0.f;
+        if (ev.size() < 2 || hipEventElapsedTime(&ms, ev.front(), ev.back()) != hipSuccess) {
+            rc = KMEANS_EHIP;
+        } else {
+            timing->step_ms = ms;
+            for (size_t e = 1; e + 2 < ev.size(); e += 2) {
+                if (hipEventElapsedTime(&ms, ev[e], ev[e + 1]) != hipSuccess) {
+                    rc = KMEANS_EHIP;
+                    break;
+                }
+                timing->assign_ms += ms;
+                timing->assign_samples++;
             }
-            timing->step_ms += ms;
-            timing->step_launches++;
         }
     }
     cleanup();

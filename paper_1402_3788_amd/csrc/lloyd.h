@@ -15,19 +15,18 @@ constexpr int kMaxLds = 160 * 1024;  // LDS bytes per workgroup on gfx950
 constexpr int kCUs = 256;            // compute units the launch geometry is sized for
 
 // Iteration control block, kept at the start of the caller's workspace.
-//   changed[t & 1] : written by the launch of iteration t (its last workgroup):
-//                    1 when any centre coordinate differs bitwise from t-1's.
+//   changed[t & 1] : set by the centres launch of iteration t (each of its
+//                    workgroups ORs in 1 when one of its centre coordinates
+//                    differs bitwise from t-1's; the centres launch of t-1
+//                    cleared it).
 //   converged_at   : first t >= 2 whose centres were congruent with t-1's
-//                    (0 = not yet); written by the launch of iteration t+1.
+//                    (0 = not yet); written by the launches of iteration t+1.
 //   fallbacks      : objects whose label was re-decided in fp64 (diagnostic).
-//   tickets        : arrival counters of the cross-workgroup reduction; zero
-//                    between launches.
 struct Ctl {
     int32_t changed[2];
     int32_t converged_at;
     int32_t fallbacks;
-    uint32_t tickets[32];
-    int32_t pad[28];
+    int32_t pad[60];
 };
 static_assert(sizeof(Ctl) == 256, "control block is one 256-byte slot");
 
@@ -95,8 +94,6 @@ struct StepArgs {
     float *min_d2;             // optional out (mode 0)
     double *part_sums;         // [groups][K][M] (modes 1/2)
     int32_t *part_counts;      // [groups][K]
-    double *grp_sums;          // [ceil(groups/16)][K][M]
-    int32_t *grp_counts;       // [ceil(groups/16)][K]
     float *centers_out;        // new centres (may alias C)
     int32_t *counts_out;       // [K]
     Ctl *ctl;                  // control block (modes 1/2)
@@ -109,5 +106,9 @@ hipError_t launch_lane(const StepArgs &a, Mode mode, const AccumPlan &plan, hipS
 hipError_t launch_tile(const StepArgs &a, Mode mode, const AccumPlan &plan, hipStream_t s);
 
 hipError_t launch_ctl_reset(Ctl *ctl, hipStream_t s);
+
+// Centres of gravity and change flag of iteration a.t from the partials of an
+// accumulating launch with `groups` workgroups (lloyd_centres.hip).
+hipError_t launch_centres(const StepArgs &a, int groups, hipStream_t s);
 
 }  // namespace lloyd

@@ -31,12 +31,11 @@
 //      minimum, so the label is the exact-arithmetic argmin;
 //   3. accumulation (the numerator and denominator of Eq. (1)) into the wave's
 //      private fp64 slabs (accumulate_tile), no barriers;
-//   4. at the end the workgroup adds its waves' slabs in a fixed order, writes
-//      one fp64 partial per (cluster, feature) plus one count per cluster, and
-//      the last workgroup forms the centres (tree_finalize).
+//   4. at the end the workgroup adds its waves' slabs in a fixed order and
+//      writes one fp64 partial per (cluster, feature) plus one count per
+//      cluster; a second launch forms the centres (lloyd_centres.hip).
 #include "lloyd.h"
 #include "lloyd_device.h"
-#include "lloyd_reduce.h"
 
 #include <math.h>
 
@@ -102,8 +101,7 @@ __global__ void __launch_bounds__(kMaxWaves * kWave, kMinWavesPerSimd)
 lloyd_lane_kernel(const float *__restrict__ X, int64_t n, const float *__restrict__ C, int K,
                   int32_t *__restrict__ labels, const int32_t *__restrict__ labels_in,
                   float *__restrict__ min_d2, double *__restrict__ part_sums,
-                  int32_t *__restrict__ part_counts, Ctl *__restrict__ ctl, int t, int fixed,
-                  TreeArgs tree)
+                  int32_t *__restrict__ part_counts, Ctl *__restrict__ ctl, int t, int fixed)
 {
     using G = TileGeom<M>;
     constexpr int V = G::kVecPerLane;
@@ -359,35 +357,13 @@ lloyd_lane_kernel(const float *__restrict__ X, int64_t n, const float *__restric
         __syncthreads();
         write_wave_partials<M, PA>(slabs_all, W, K, part_sums + (int64_t)blockIdx.x * K * M,
                                    part_counts + (int64_t)blockIdx.x * K);
-        tree_finalize(tree, reinterpret_cast<uint32_t *>(slabs_all));
     }
-}
-
-TreeArgs tree_args(const StepArgs &a, int groups)
-{
-    TreeArgs r{};
-    r.part_sums = a.part_sums;
-    r.part_counts = a.part_counts;
-    r.grp_sums = a.grp_sums;
-    r.grp_counts = a.grp_counts;
-    r.tickets = a.ctl != nullptr ? a.ctl->tickets : nullptr;
-    r.G = groups;
-    r.K = a.K;
-    r.M = a.M;
-    r.prev = a.C;
-    r.centers = a.centers_out;
-    r.counts = a.counts_out;
-    r.ctl = a.ctl;
-    r.t = a.t;
-    r.compare = a.compare;
-    return r;
 }
 
 template <int M, int DIST>
 hipError_t launch_m(const StepArgs &a, Mode mode, const AccumPlan &p, hipStream_t s)
 {
     const dim3 grid(p.groups), block(p.waves * kWave);
-    const TreeArgs tr = tree_args(a, p.groups);
 #define LLOYD_LANE_LAUNCH(MD, PA)                                                              \
     do {                                                                                       \
         auto kern = lloyd_lane_kernel<M, MD, PA, DIST>;                                        \
@@ -396,7 +372,7 @@ hipError_t launch_m(const StepArgs &a, Mode mode, const AccumPlan &p, hipStream_
             return hipErrorInvalidConfiguration;                                               \
         hipLaunchKernelGGL(kern, grid, block, p.lds_bytes, s, a.X, a.n, a.C, a.K, a.labels,    \
                            a.labels_in, a.min_d2, a.part_sums, a.part_counts, a.ctl, a.t,      \
-                           a.fixed, tr);                                                       \
+                           a.fixed);                                                           \
     } while (0)
     const bool one = p.accum == 1;
     switch (mode) {

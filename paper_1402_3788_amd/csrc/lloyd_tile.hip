@@ -41,7 +41,6 @@
 //              count) and adds them one member per step. Used for large K*M.
 #include "lloyd.h"
 #include "lloyd_device.h"
-#include "lloyd_reduce.h"
 
 #include <math.h>
 
@@ -150,8 +149,7 @@ __global__ void __launch_bounds__(kMaxWaves * kWave)
 lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restrict__ C, int K,
                   int32_t *__restrict__ labels, const int32_t *__restrict__ labels_in,
                   float *__restrict__ min_d2, double *__restrict__ part_sums,
-                  int32_t *__restrict__ part_counts, Ctl *__restrict__ ctl, int t, int fixed,
-                  TreeArgs tree)
+                  int32_t *__restrict__ part_counts, Ctl *__restrict__ ctl, int t, int fixed)
 {
     using TG = TileGeom<M>;
     constexpr int KS = (M + 3) / 4;
@@ -492,34 +490,12 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
         for (int k = tid; k < K; k += blockDim.x)
             part_counts[(int64_t)blockIdx.x * K + k] = (int32_t)slab[k * (M + 1) + M];
     }
-    if (kAccum) tree_finalize(tree, reinterpret_cast<uint32_t *>(smem + L.slab));
-}
-
-TreeArgs tree_args(const StepArgs &a, int groups)
-{
-    TreeArgs r{};
-    r.part_sums = a.part_sums;
-    r.part_counts = a.part_counts;
-    r.grp_sums = a.grp_sums;
-    r.grp_counts = a.grp_counts;
-    r.tickets = a.ctl != nullptr ? a.ctl->tickets : nullptr;
-    r.G = groups;
-    r.K = a.K;
-    r.M = a.M;
-    r.prev = a.C;
-    r.centers = a.centers_out;
-    r.counts = a.counts_out;
-    r.ctl = a.ctl;
-    r.t = a.t;
-    r.compare = a.compare;
-    return r;
 }
 
 template <int M>
 hipError_t launch_m(const StepArgs &a, Mode mode, const AccumPlan &p, hipStream_t s)
 {
     const dim3 grid(p.groups), block(p.waves * kWave);
-    const TreeArgs tr = tree_args(a, p.groups);
 #define LLOYD_MFMA_LAUNCH(MD, AC)                                                              \
     do {                                                                                       \
         auto kern = lloyd_tile_kernel<M, MD, AC>;                                              \
@@ -528,7 +504,7 @@ hipError_t launch_m(const StepArgs &a, Mode mode, const AccumPlan &p, hipStream_
             return hipErrorInvalidConfiguration;                                               \
         hipLaunchKernelGGL(kern, grid, block, p.lds_bytes, s, a.X, a.n, a.C, a.K, a.labels,    \
                            a.labels_in, a.min_d2, a.part_sums, a.part_counts, a.ctl, a.t,      \
-                           a.fixed, tr);                                                       \
+                           a.fixed);                                                           \
     } while (0)
     switch (mode) {
     case kAssign: LLOYD_MFMA_LAUNCH(kAssign, 0); break;
