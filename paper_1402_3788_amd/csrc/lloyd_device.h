@@ -137,14 +137,17 @@ struct WaveAcc {
 // lab: this lane's object label (-1: no object). tile: the wave's LDS tile
 // (object-major, with at least one float of slack after the 64 rows). offs: 64
 // ints of wave-private LDS. slabs: the wave's P slabs (P*K*(M+1) doubles).
-template <int M, int P_>
+// kFull: every object of the tile is present (lab >= 0 in every lane): the
+// per-step validity test drops out and the lanes past the count column are
+// masked once for the whole tile.
+template <int M, int P_, bool kFull = false>
 __device__ inline void accumulate_tile(int lab, const float *tile, int32_t *offs, double *slabs,
                                        int K, int lane)
 {
     using A = WaveAcc<M, P_>;
     constexpr int MW = A::MW, LW = A::LW, P = A::P;
     // row offset (in doubles) of this lane's object in its slab
-    offs[lane] = lab >= 0 ? ((lane % P) * K + lab) * MW : -1;
+    offs[lane] = (kFull || lab >= 0) ? ((lane % P) * K + lab) * MW : -1;
     __builtin_amdgcn_wave_barrier();
     const int h = lane / LW, j = lane % LW;
     const int jr = j < M ? j : M;              // count lanes read a value they ignore
@@ -156,24 +159,49 @@ __device__ inline void accumulate_tile(int lab, const float *tile, int32_t *offs
     // back (an add cannot be hoisted above a read the compiler cannot prove
     // disjoint, so interleaving them would serialise every step on LDS latency).
     constexpr int B = A::kSteps < 16 ? A::kSteps : 16;
+    if constexpr (kFull && M + 1 <= kWave) {
+        if (used) {
+            double *col = slabs + j;
+            // 1.0f the optimiser cannot see through (see accumulate_commit)
+            float one;
+            asm("v_mov_b32 %0, 1.0" : "=v"(one));
 #pragma unroll
-    for (int s0 = 0; s0 < A::kSteps; s0 += B) {
-        int o[B];
-        float x[B];
+            for (int s0 = 0; s0 < A::kSteps; s0 += B) {
+                int o[B];
+                float x[B];
 #pragma unroll
-        for (int b = 0; b < B; ++b) {
-            o[b] = op[(s0 + b) * P];
-            x[b] = xp[(s0 + b) * P * M];
+                for (int b = 0; b < B; ++b) {
+                    o[b] = op[(s0 + b) * P];
+                    x[b] = xp[(s0 + b) * P * M];
+                }
+#pragma unroll
+                for (int b = 0; b < B; ++b) {
+                    const float v = feat ? x[b] : one;   // the count column adds 1
+                    __hip_atomic_fetch_add(col + o[b], (double)v, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_WAVEFRONT);
+                }
+            }
         }
+    } else {
 #pragma unroll
-        for (int b = 0; b < B; ++b) {
-            const double v = (double)(feat ? x[b] : 1.0f);
-            if (used && o[b] >= 0)
-                __hip_atomic_fetch_add(slabs + o[b] + j, v, __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_WAVEFRONT);
-            if (M + 1 > kWave && lane == 0 && o[b] >= 0)   // M = 64: no lane left for the count
-                __hip_atomic_fetch_add(slabs + o[b] + M, 1.0, __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_WAVEFRONT);
+        for (int s0 = 0; s0 < A::kSteps; s0 += B) {
+            int o[B];
+            float x[B];
+#pragma unroll
+            for (int b = 0; b < B; ++b) {
+                o[b] = op[(s0 + b) * P];
+                x[b] = xp[(s0 + b) * P * M];
+            }
+#pragma unroll
+            for (int b = 0; b < B; ++b) {
+                const double v = (double)(feat ? x[b] : 1.0f);
+                if (used && o[b] >= 0)
+                    __hip_atomic_fetch_add(slabs + o[b] + j, v, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_WAVEFRONT);
+                if (M + 1 > kWave && lane == 0 && o[b] >= 0)   // M = 64: no lane left for the count
+                    __hip_atomic_fetch_add(slabs + o[b] + M, 1.0, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_WAVEFRONT);
+            }
         }
     }
     __builtin_amdgcn_wave_barrier();

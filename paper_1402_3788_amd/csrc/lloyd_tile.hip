@@ -247,15 +247,19 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
 
     // One wave tile: stage it in LDS, put the loads of the tile two strides
     // ahead in flight in the same registers, assign, accumulate.
-    auto step = [&](int64_t b, auto bi, bool prefetch) {
+    // full: a block tile of the main loop (every wave tile present and full;
+    // the loads two strides ahead are issued here) rather than the last one
+    auto step = [&](int64_t b, auto bi, auto full) {
+        constexpr bool kFullTile = decltype(full)::value;
+        constexpr bool prefetch = kFullTile;
         float4 (&bb)[V] = buf[decltype(bi)::value];
         const int64_t q = b * W + wave;
-        const bool have = q < nq;
+        const bool have = kFullTile || q < nq;
         if (have) store_tile<M>(tile, lane, bb);
         __builtin_amdgcn_wave_barrier();
         if (prefetch && b + 2 * G < nbt_main) load_tile<M>(X, (b + 2 * G) * W + wave, lane, bb);
         const int64_t i = q * kWave + lane;
-        const bool valid = have && i < n;
+        const bool valid = kFullTile || (have && i < n);
         int my_lab = -1;
 
         if (have && MODE == kAccumLabels) {
@@ -386,7 +390,8 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
         }
 
         if (kWaveForm) {
-            if (have) accumulate_tile<M, PA>(valid ? my_lab : -1, tile, offs, wslabs, K, lane);
+            // (labels read back may be out of range even in a full tile)
+            if (have) accumulate_tile<M, PA, kFullTile && MODE != kAccumLabels>(valid ? my_lab : -1, tile, offs, wslabs, K, lane);
         } else if (kAcc == kAccBlock) {
             // Wave w owns the clusters k with k % W == w (W is a power of two).
             // After a barrier it lists the members of its clusters over the
@@ -465,14 +470,14 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
     // alternate. Every wave of a workgroup runs the same steps (the block form
     // has barriers inside).
     for (int64_t bt = bt0; bt < nbt_main; bt += 2 * G) {
-        step(bt, std::integral_constant<int, 0>{}, true);
-        if (bt + G < nbt_main) step(bt + G, std::integral_constant<int, 1>{}, true);
+        step(bt, std::integral_constant<int, 0>{}, std::true_type{});
+        if (bt + G < nbt_main) step(bt + G, std::integral_constant<int, 1>{}, std::true_type{});
     }
     if (nbt_main < nbt && nbt_main >= bt0 && (nbt_main - bt0) % G == 0) {
         const int64_t q = nbt_main * W + wave;
         if (q < nfull) load_tile<M>(X, q, lane, buf[0]);
         else if (q < nq) load_tail_tile<M>(X, n, q, lane, buf[0]);
-        step(nbt_main, std::integral_constant<int, 0>{}, false);
+        step(nbt_main, std::integral_constant<int, 0>{}, std::false_type{});
     }
 
     if (ctl != nullptr && lane == 0 && nfallback > 0) atomicAdd(&ctl->fallbacks, nfallback);
