@@ -189,3 +189,10 @@ def ctl_fallbacks(ws: torch.Tensor) -> int:
     """Objects re-decided in fp64 during the last kmeans_run that used `ws`
     (read from the control block at the start of the workspace)."""
     return int(ws[12:16].view(torch.int32).item())
+
+
+def ctl_reruns(ws: torch.Tensor) -> int:
+    """64-object tiles of the tile kernel whose split-precision scores left a
+    call too close, recomputed with fp32 products, during the last kmeans_run
+    that used `ws` (read from the control block)."""
+    return int(ws[16:20].view(torch.int32).item())

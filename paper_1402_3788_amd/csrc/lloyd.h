@@ -22,11 +22,14 @@ constexpr int kCUs = 256;            // compute units the launch geometry is siz
 //   converged_at   : first t >= 2 whose centres were congruent with t-1's
 //                    (0 = not yet); written by the launches of iteration t+1.
 //   fallbacks      : objects whose label was re-decided in fp64 (diagnostic).
+//   reruns         : wave tiles whose split-precision scores left a call too
+//                    close, recomputed with fp32 products (diagnostic).
 struct Ctl {
     int32_t changed[2];
     int32_t converged_at;
     int32_t fallbacks;
-    int32_t pad[60];
+    int32_t reruns;
+    int32_t pad[59];
 };
 static_assert(sizeof(Ctl) == 256, "control block is one 256-byte slot");
 

@@ -65,7 +65,7 @@ constexpr int kMaxWaves = 8;
 
 // LDS carve-up of a workgroup (dynamic shared memory).
 struct MfmaLds {
-    size_t aswz, cnorm, misc, tiles, offs, labs, members, slab, total;
+    size_t abf, cnorm, misc, tiles, offs, labs, members, slab, total;
     int tile_floats;
 };
 
@@ -86,11 +86,11 @@ __host__ __device__ inline int centre_blocks(int K) { return ((K + 15) / 16 + 1)
 
 __host__ __device__ inline MfmaLds mfma_lds(int M, int K, int W, int acc)
 {
-    const int KS = (M + 3) / 4, KT = centre_blocks(K);
+    const int KC = (M + 31) / 32, KT = centre_blocks(K);
     MfmaLds L{};
     L.tile_floats = (kWave * M + (M > 4 ? M : 4) + 3) / 4 * 4;    // TileGeom<M>::kSlot
     size_t o = 0;
-    L.aswz = o;    o = al16(o + (size_t)KT * KS * kWave * 4);
+    L.abf = o;     o = al16(o + (size_t)KT * KC * kWave * 32);
     L.cnorm = o;   o = al16(o + (size_t)KT * 16 * 4);
     L.misc = o;    o = al16(o + 16);
     L.tiles = o;   o = al16(o + (size_t)W * L.tile_floats * 4);
@@ -144,6 +144,33 @@ __device__ inline float sum_rows(float v)
     return __uint_as_float(s[0]) + __uint_as_float(s[1]);
 }
 
+// Split eight fp32 values v into bf16 parts by truncation: hi = the top 16
+// bits of v, lo = the top 16 bits of the exact remainder v - hi. Then
+// |v - hi| < 2^-7 |v| and |v - hi - lo| < 2^-14 |v| (v finite). Parts are
+// packed two per dword, element 2e in the low half of dword e, as the bf16
+// operands of v_mfma_f32_16x16x32_bf16 expect.
+__device__ inline void split_bf16x8(const float (&v)[8], uint32_t (&hi)[4], uint32_t (&lo)[4])
+{
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const uint32_t h0 = __float_as_uint(v[2 * e]) & 0xFFFF0000u;
+        const uint32_t h1 = __float_as_uint(v[2 * e + 1]) & 0xFFFF0000u;
+        const uint32_t l0 = __float_as_uint(v[2 * e] - __uint_as_float(h0)) & 0xFFFF0000u;
+        const uint32_t l1 = __float_as_uint(v[2 * e + 1] - __uint_as_float(h1)) & 0xFFFF0000u;
+        hi[e] = (h0 >> 16) | h1;
+        lo[e] = (l0 >> 16) | l1;
+    }
+}
+
+typedef __bf16 bf8v __attribute__((ext_vector_type(8)));
+
+__device__ inline bf8v as_bf8(const uint32_t (&u)[4])
+{
+    typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+    const u4v w = {u[0], u[1], u[2], u[3]};
+    return __builtin_bit_cast(bf8v, w);
+}
+
 template <int M, int MODE, int ACC>
 __global__ void __launch_bounds__(kMaxWaves * kWave)
 lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restrict__ C, int K,
@@ -152,7 +179,8 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
                   int32_t *__restrict__ part_counts, Ctl *__restrict__ ctl, int t, int fixed)
 {
     using TG = TileGeom<M>;
-    constexpr int KS = (M + 3) / 4;
+    constexpr int KS = (M + 3) / 4;          // 4-feature steps of the fp32 products
+    constexpr int KC = (M + 31) / 32;        // 32-feature chunks of the bf16 products
     constexpr int kSlot = TG::kSlot;
     constexpr int V = TG::kVecPerLane;
     constexpr bool kAccum = MODE != kAssign;
@@ -172,7 +200,7 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
     float *tiles = reinterpret_cast<float *>(smem + L.tiles);
     float *tile = tiles + wave * kSlot;
     int32_t *offs = reinterpret_cast<int32_t *>(smem + L.offs) + wave * kWave;
-    float *aswz = reinterpret_cast<float *>(smem + L.aswz);
+    uint32_t *abf = reinterpret_cast<uint32_t *>(smem + L.abf);
     float *cnorm = reinterpret_cast<float *>(smem + L.cnorm);
     float *s_cmax = reinterpret_cast<float *>(smem + L.misc);
     double *wslabs = reinterpret_cast<double *>(smem + L.slab) + (size_t)wave * kP * K * (M + 1);
@@ -193,12 +221,24 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
     if (bt0 < nbt_main) load_tile<M>(X, bt0 * W + wave, lane, buf[0]);
     if (bt0 + G < nbt_main) load_tile<M>(X, (bt0 + G) * W + wave, lane, buf[1]);
 
-    // ---- prologue: A operands (-2C in lane order), centre norms, slabs
+    // ---- prologue: split A operands (-2C, bf16 hi and lo, in lane order),
+    // centre norms, slabs
     if (MODE != kAccumLabels) {
-        for (int idx = tid; idx < KT * KS * kWave; idx += blockDim.x) {
-            const int tt = idx / (KS * kWave), s = (idx / kWave) % KS, l = idx % kWave;
-            const int k = tt * 16 + (l & 15), j = 4 * s + (l >> 4);
-            aswz[idx] = (k < K && j < M) ? -2.0f * C[(int64_t)k * M + j] : 0.0f;
+        for (int idx = tid; idx < KT * KC * kWave; idx += blockDim.x) {
+            const int tt = idx / (KC * kWave), qc = (idx / kWave) % KC, l = idx % kWave;
+            const int k = tt * 16 + (l & 15), j0 = 32 * qc + 8 * (l >> 4);
+            float a[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                a[e] = (k < K && j0 + e < M) ? -2.0f * C[(int64_t)k * M + j0 + e] : 0.0f;
+            uint32_t hi[4], lo[4];
+            split_bf16x8(a, hi, lo);
+            uint32_t *dst = abf + (size_t)idx * 8;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                dst[e] = hi[e];
+                dst[4 + e] = lo[e];
+            }
         }
     }
     {
@@ -215,15 +255,14 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
     }
     __syncthreads();
     if (MODE != kAccumLabels) {
-        // |c_k|^2 in fp32, features in order, from c = -a/2 (exact)
+        // |c_k|^2 in fp32, features in order
         for (int k = tid; k < KT * 16; k += blockDim.x) {
             float nk = INFINITY;
             if (k < K) {
-                const int tt = k / 16, i16 = k % 16;
                 nk = 0.f;
 #pragma unroll
                 for (int j = 0; j < M; ++j) {
-                    const float c = -0.5f * aswz[(tt * KS + j / 4) * kWave + i16 + 16 * (j % 4)];
+                    const float c = C[(int64_t)k * M + j];
                     nk = __builtin_fmaf(c, c, nk);
                 }
             }
@@ -244,6 +283,7 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
 
     const int g = lane >> 4, l16 = lane & 15;
     int nfallback = 0;
+    int nrerun = 0;     // wave tiles that needed the fp32 pass
 
     // One wave tile: stage it in LDS, put the loads of the tile two strides
     // ahead in flight in the same registers, assign, accumulate.
@@ -268,51 +308,21 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
                 if (my_lab < 0 || my_lab >= K) my_lab = -1;
             }
         } else if (have) {
-            // B operands: object 16c + l16, features 4s + g
-            float bop[kCols][KS];
-            float xsq[kCols];
-#pragma unroll
-            for (int c = 0; c < kCols; ++c) {
-                const float *row = tile + (16 * c + l16) * M + g;
-                float acc = 0.f;
-#pragma unroll
-                for (int s = 0; s < KS; ++s) {
-                    float v = row[4 * s];
-                    if ((M % 4) != 0 && s == KS - 1 && 4 * s + g >= M) v = 0.f;
-                    bop[c][s] = v;
-                    acc = __builtin_fmaf(v, v, acc);
-                }
-                xsq[c] = sum_rows<32>(sum_rows<16>(acc));
-            }
+            // Running best / second best / label of the lane's 4 centres of
+            // each column, over the centre blocks; then the four lanes that
+            // hold the same object merged (rows r, r^1, r^2), and lane l keeps
+            // column l / 16, i.e. object l.
             float b1[kCols], b2[kCols];
             int lb[kCols];
+            float xsq[kCols];
+            auto reset = [&]() {
 #pragma unroll
-            for (int c = 0; c < kCols; ++c) {
-                b1[c] = INFINITY;
-                b2[c] = INFINITY;
-                lb[c] = 0;
-            }
-            // operands of centre block tt (A in lane order, seeds |c|^2)
-            struct Ops {
-                float a[KS];
-                f4v c0;
+                for (int c = 0; c < kCols; ++c) {
+                    b1[c] = INFINITY;
+                    b2[c] = INFINITY;
+                    lb[c] = 0;
+                }
             };
-            auto load_ops = [&](int tt, Ops &o) {
-#pragma unroll
-                for (int s = 0; s < KS; ++s) o.a[s] = aswz[(tt * KS + s) * kWave + lane];
-                o.c0 = *reinterpret_cast<const f4v *>(cnorm + tt * 16 + 4 * g);
-            };
-            // scores of one centre block for the four columns
-            auto chain = [&](const Ops &o, f4v (&d)[kCols]) {
-#pragma unroll
-                for (int c = 0; c < kCols; ++c) d[c] = o.c0;
-#pragma unroll
-                for (int s = 0; s < KS; ++s)
-#pragma unroll
-                    for (int c = 0; c < kCols; ++c)
-                        d[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(o.a[s], bop[c][s], d[c], 0, 0, 0);
-            };
-            // running best / second best / label over the lane's 4 centres
             auto scan = [&](int tt, const f4v (&d)[kCols]) {
                 const int kb = tt * 16 + 4 * g;
 #pragma unroll
@@ -326,46 +336,171 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
                         lb[c] = lt ? kb + r : lb[c];
                     }
             };
-            // Two accumulator sets and two operand sets: the matrix cores
-            // compute one block while the vector ALU scans the previous one and
-            // the next block's operands arrive from LDS (no branch inside the
-            // loop body).
-            f4v dA[kCols], dB[kCols];
-            Ops oA, oB;
-            load_ops(0, oA);
-            load_ops(1, oB);
-            chain(oA, dA);
-            int tt = 0;
-            for (; tt + 2 < KT; tt += 2) {
-                load_ops(tt + 2, oA);
+            float mb1, mb2, mx;
+            int ml;
+            auto finish = [&]() {
+#pragma unroll
+                for (int c = 0; c < kCols; ++c) {
+                    merge_rows<16>(b1[c], b2[c], lb[c]);
+                    merge_rows<32>(b1[c], b2[c], lb[c]);
+                }
+                mb1 = b1[0];
+                mb2 = b2[0];
+                mx = xsq[0];
+                ml = lb[0];
+#pragma unroll
+                for (int c = 1; c < kCols; ++c) {
+                    const bool mine = g == c;
+                    mb1 = mine ? b1[c] : mb1;
+                    mb2 = mine ? b2[c] : mb2;
+                    mx = mine ? xsq[c] : mx;
+                    ml = mine ? lb[c] : ml;
+                }
+            };
+            // Both passes keep two accumulator sets and two operand sets: the
+            // matrix cores compute one centre block while the vector ALU scans
+            // the previous one and the next block's operands arrive.
+            auto blocks = [&](auto &oA, auto &oB, auto load_ops, auto chain) {
+                f4v dA[kCols], dB[kCols];
+                load_ops(0, oA);
+                load_ops(1, oB);
+                chain(oA, dA);
+                int tt = 0;
+                for (; tt + 2 < KT; tt += 2) {
+                    load_ops(tt + 2, oA);
+                    chain(oB, dB);
+                    scan(tt, dA);
+                    load_ops(tt + 3, oB);
+                    chain(oA, dA);
+                    scan(tt + 1, dB);
+                }
                 chain(oB, dB);
                 scan(tt, dA);
-                load_ops(tt + 3, oB);
-                chain(oA, dA);
                 scan(tt + 1, dB);
-            }
-            chain(oB, dB);
-            scan(tt, dA);
-            scan(tt + 1, dB);
-            // merge the four lanes that hold the same object (rows r, r^1, r^2)
+            };
+
+            // ---- pass 1: split-precision products on the bf16 matrix cores.
+            // B operands: object 16c + l16, features 32q + 8g .. 32q + 8g + 7
+            // (zero past M), split into bf16 hi and lo; A likewise (table in
+            // LDS). Each centre block is three products per column,
+            // lo(A) hi(B) + hi(A) lo(B) + hi(A) hi(B), on top of |c|^2.
+            {
+                uint32_t bh[kCols][KC][4], bl[kCols][KC][4];
 #pragma unroll
-            for (int c = 0; c < kCols; ++c) {
-                merge_rows<16>(b1[c], b2[c], lb[c]);
-                merge_rows<32>(b1[c], b2[c], lb[c]);
-            }
-            // lane l reports object l, which sits in column c = l / 16 = g
-            float mb1 = b1[0], mb2 = b2[0], mx = xsq[0];
-            int ml = lb[0];
+                for (int c = 0; c < kCols; ++c) {
+                    const float *row = tile + (16 * c + l16) * M;
+                    float acc = 0.f;
 #pragma unroll
-            for (int c = 1; c < kCols; ++c)
-                if (g == c) {
-                    mb1 = b1[c];
-                    mb2 = b2[c];
-                    mx = xsq[c];
-                    ml = lb[c];
+                    for (int qc = 0; qc < KC; ++qc) {
+                        float v[8];
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) {
+                            const int f = 32 * qc + 8 * g + e;
+                            // (the read stays inside the row; the value past M is 0)
+                            const float x = row[f < M ? f : M - 1];
+                            v[e] = f < M ? x : 0.f;
+                            acc = __builtin_fmaf(v[e], v[e], acc);
+                        }
+                        split_bf16x8(v, bh[c][qc], bl[c][qc]);
+                    }
+                    xsq[c] = sum_rows<32>(sum_rows<16>(acc));
                 }
-            const float thr = kGuard * (3.02f * cmax + 1.0001f * mx) + 1e-30f;
-            const bool ok = (K == 1) || (mb2 - mb1 > thr);
+                struct OpsH {
+                    uint32_t ah[KC][4], al[KC][4];
+                    f4v c0;
+                };
+                auto load_h = [&](int tt, OpsH &o) {
+#pragma unroll
+                    for (int qc = 0; qc < KC; ++qc) {
+                        const uint32_t *src = abf + ((size_t)(tt * KC + qc) * kWave + lane) * 8;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            o.ah[qc][e] = src[e];
+                            o.al[qc][e] = src[4 + e];
+                        }
+                    }
+                    o.c0 = *reinterpret_cast<const f4v *>(cnorm + tt * 16 + 4 * g);
+                };
+                auto chain_h = [&](const OpsH &o, f4v (&d)[kCols]) {
+#pragma unroll
+                    for (int c = 0; c < kCols; ++c) d[c] = o.c0;
+#pragma unroll
+                    for (int qc = 0; qc < KC; ++qc) {
+#pragma unroll
+                        for (int c = 0; c < kCols; ++c)
+                            d[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                as_bf8(o.al[qc]), as_bf8(bh[c][qc]), d[c], 0, 0, 0);
+#pragma unroll
+                        for (int c = 0; c < kCols; ++c)
+                            d[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                as_bf8(o.ah[qc]), as_bf8(bl[c][qc]), d[c], 0, 0, 0);
+#pragma unroll
+                        for (int c = 0; c < kCols; ++c)
+                            d[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                as_bf8(o.ah[qc]), as_bf8(bh[c][qc]), d[c], 0, 0, 0);
+                    }
+                };
+                OpsH oA, oB;
+                reset();
+                blocks(oA, oB, load_h, chain_h);
+                finish();
+            }
+            // Error of a pass-1 score against the exact score |c|^2 - 2 x.c:
+            // the dropped terms lo(A) lo(B), and the parts' truncation, are
+            // below 3.02 * 2^-14 |2 c_j x_j| per feature; the fp32 sums of the
+            // 96 KC + 1 exact terms add gamma_{96 KC + 2}; |c|^2 in fp32 adds
+            // gamma_M |c|^2. With 2|c_j x_j| <= c_j^2 + x_j^2 each score is
+            // within E (|x|^2 + 3|c|^2), E = 3.02 * 2^-14 + 1.03 gamma, so the
+            // label stands when the two best scores differ by more than twice
+            // that (with margins).
+            constexpr float kE1 = 3.02f * 6.1035156e-05f + 1.03f * (float)(96 * KC + 2) * 5.9604645e-8f;
+            const float thr1 = 2.02f * kE1 * (3.02f * cmax + 1.0001f * mx) + 1e-30f;
+            bool ok = (K == 1) || (mb2 - mb1 > thr1);
+
+            // ---- pass 2 (tiles with a call too close for pass 1): the fp32
+            // products, A = -2C read from C, B = X^T from the tile.
+            if (__ballot(valid && !ok) != 0) {
+                float bop[kCols][KS];
+#pragma unroll
+                for (int c = 0; c < kCols; ++c) {
+                    const float *row = tile + (16 * c + l16) * M + g;
+#pragma unroll
+                    for (int s = 0; s < KS; ++s) {
+                        float v = row[4 * s];
+                        if ((M % 4) != 0 && s == KS - 1 && 4 * s + g >= M) v = 0.f;
+                        bop[c][s] = v;
+                    }
+                }
+                struct Ops {
+                    float a[KS];
+                    f4v c0;
+                };
+                auto load_ops = [&](int tt, Ops &o) {
+                    const int k = tt * 16 + l16;
+#pragma unroll
+                    for (int s = 0; s < KS; ++s) {
+                        const int j = 4 * s + g;
+                        o.a[s] = (k < K && j < M) ? -2.0f * C[(int64_t)k * M + j] : 0.0f;
+                    }
+                    o.c0 = *reinterpret_cast<const f4v *>(cnorm + tt * 16 + 4 * g);
+                };
+                auto chain = [&](const Ops &o, f4v (&d)[kCols]) {
+#pragma unroll
+                    for (int c = 0; c < kCols; ++c) d[c] = o.c0;
+#pragma unroll
+                    for (int s = 0; s < KS; ++s)
+#pragma unroll
+                        for (int c = 0; c < kCols; ++c)
+                            d[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(o.a[s], bop[c][s], d[c], 0, 0, 0);
+                };
+                Ops oA, oB;
+                reset();
+                blocks(oA, oB, load_ops, chain);
+                finish();
+                const float thr = kGuard * (3.02f * cmax + 1.0001f * mx) + 1e-30f;
+                ok = (K == 1) || (mb2 - mb1 > thr);
+                if (ctl != nullptr && lane == 0) ++nrerun;
+            }
             float dmin = 0.f;
             if (valid && !ok) {
                 double bd;
@@ -481,6 +616,7 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
     }
 
     if (ctl != nullptr && lane == 0 && nfallback > 0) atomicAdd(&ctl->fallbacks, nfallback);
+    if (ctl != nullptr && lane == 0 && nrerun > 0) atomicAdd(&ctl->reruns, nrerun);
 
     if (kWaveForm) {
         __syncthreads();

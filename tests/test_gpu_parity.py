@@ -170,6 +170,33 @@ def test_assign_near_ties_are_exact():
             assert np.array_equal(lab, oracle.assign(X, CC)), path
 
 
+@pytest.mark.parametrize("K,M", [(64, 25), (256, 25), (40, 40)])
+def test_split_precision_rerun_parity(K, M):
+    # Half of the objects lie within 1e-4 (relative) of the bisector of two
+    # centres: the tile kernel's split-precision pass cannot call them, so
+    # their tiles are recomputed with fp32 products and the closest calls
+    # re-decided in fp64. Labels, counts and centres must still equal the
+    # oracle's, and the control block must show that tiles were recomputed.
+    _say(f"[rerun] K={K} M={M}")
+    rng = np.random.default_rng(K + M)
+    n = 20_000
+    C = rng.uniform(-50, 50, (K, M)).astype(np.float32)
+    a, b = rng.integers(0, K, n), rng.integers(0, K, n)
+    t = rng.uniform(0.4999, 0.5001, (n, 1))
+    X = (C[a] * t + C[b] * (1 - t)).astype(np.float32)
+    X[n // 2:] = rng.uniform(-50, 50, (n - n // 2, M)).astype(np.float32)
+    ws = km.workspace(n, M, K, DEV, km.KMEANS_PATH_TILES)
+    lab, Cn, cnt, it = km.kmeans_run(_gpu(X), K, _gpu(C), 2, fixed_iters=True, path="tiles", ws=ws)
+    olab, oC, ocnt, oit = oracle.run(X, K, C, 2, fixed=True)
+    assert np.array_equal(lab.cpu().numpy(), olab)
+    assert np.array_equal(cnt.cpu().numpy(), ocnt)
+    check_centers(Cn.cpu().numpy(), oC)
+    reruns = km.ctl_reruns(ws)
+    _say(f"[rerun] K={K}: {reruns} tiles recomputed with fp32 products, "
+         f"{km.ctl_fallbacks(ws)} objects re-decided in fp64")
+    assert reruns > 0
+
+
 @pytest.mark.parametrize("n,M,K", [(1, 2, 1), (1000, 3, 7), (65_537, 25, 16), (33_333, 64, 100),
                                    (10_000, 10, 1024)])
 def test_update_parity(n, M, K):
