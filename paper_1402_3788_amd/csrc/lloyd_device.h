@@ -140,14 +140,19 @@ struct WaveAcc {
 // kFull: every object of the tile is present (lab >= 0 in every lane): the
 // per-step validity test drops out and the lanes past the count column are
 // masked once for the whole tile.
-template <int M, int P_, bool kFull = false>
+// kShared: the P objects of a step add into one slab instead of P. Two lanes
+// of one instruction then meet on a row when their objects share a cluster;
+// the slab is the wave's own and the LDS applies the lanes of one instruction
+// in a fixed order, so the sums are still reproducible, with 1/P of the LDS.
+template <int M, int P_, bool kFull = false, bool kShared = false>
 __device__ inline void accumulate_tile(int lab, const float *tile, int32_t *offs, double *slabs,
                                        int K, int lane)
 {
     using A = WaveAcc<M, P_>;
     constexpr int MW = A::MW, LW = A::LW, P = A::P;
     // row offset (in doubles) of this lane's object in its slab
-    offs[lane] = (kFull || lab >= 0) ? ((lane % P) * K + lab) * MW : -1;
+    const int slab_of = kShared ? 0 : lane % P;
+    offs[lane] = (kFull || lab >= 0) ? (slab_of * K + lab) * MW : -1;
     __builtin_amdgcn_wave_barrier();
     const int h = lane / LW, j = lane % LW;
     const int jr = j < M ? j : M;              // count lanes read a value they ignore
@@ -289,13 +294,14 @@ __device__ inline void accumulate_commit(int lab, const AccFetch<M, P_> &f, int3
 // Workgroup partial of the wave-accumulation form: for every (cluster, feature)
 // the sum over waves w and slabs h (w, then h, ascending) written to
 // part_sums[K][M], and the counts to part_counts[K]. Call after a barrier.
-template <int M, int P_>
+// kShared: one slab per wave (see accumulate_tile).
+template <int M, int P_, bool kShared = false>
 __device__ inline void write_wave_partials(const double *slabs, int W, int K,
                                            double *__restrict__ part_sums,
                                            int32_t *__restrict__ part_counts)
 {
     using A = WaveAcc<M, P_>;
-    constexpr int MW = A::MW, P = A::P;
+    constexpr int MW = A::MW, P = kShared ? 1 : A::P;
     const int tid = threadIdx.x, nthr = blockDim.x;
     const size_t rows = (size_t)W * P;          // slabs in the workgroup
     for (int e = tid; e < K * MW; e += nthr) {

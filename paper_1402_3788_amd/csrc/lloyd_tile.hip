@@ -28,13 +28,15 @@
 // flight in registers while the current tile is staged in the wave's LDS slot;
 // the ragged last tile (n not a multiple of 64) is handled after the loop.
 //
-// Accumulation (the sums of Eq. (1)) has two forms, both free of atomics across
-// lanes that share an address and with every addition in an order fixed by the
-// problem shape:
+// Accumulation (the sums of Eq. (1)) has two forms, both with every addition in
+// an order fixed by the problem shape (and the hardware's lane order):
 //   wave    -- each wavefront adds its own tiles into private fp64 slabs
-//              (accumulate_tile: LDS fp64 adds in program order, no barriers);
-//              at the end the workgroup adds the slabs in a fixed order. Used
-//              while W >= 4 waves' private slabs fit in LDS (small K*M).
+//              (accumulate_tile: LDS fp64 adds in program order, no barriers),
+//              one slab per object of a step, or (when that leaves fewer
+//              waves) one slab that the objects of a step share, the LDS
+//              applying the lanes of one add in a fixed order; at the end the
+//              workgroup adds the slabs in a fixed order. Used while W >= 4
+//              waves' private slabs fit in LDS (small K*M).
 //   block   -- one fp64 slab per workgroup: after a barrier, wave w owns the
 //              clusters k with k % W == w; it lists their members over the
 //              workgroup's W tiles in (tile, object) order (ballot + prefix
@@ -59,7 +61,7 @@ typedef float f4v __attribute__((ext_vector_type(4)));
 constexpr int kCols = 4;      // 16-object columns per wave tile (64 objects)
 constexpr int kAccWave = 1;    // per-wave slabs, WaveAcc<M>::Pmax objects per step
 constexpr int kAccBlock = 2;   // one slab per workgroup
-constexpr int kAccWave1 = 3;   // per-wave slab, one object per step (less LDS)
+constexpr int kAccWave1 = 3;   // one slab per wave, WaveAcc<M>::Pmax objects per step (less LDS)
 constexpr int kMaxWaves = 8;
 [[maybe_unused]] constexpr int kMinWaveForm = 4;   // fewest waves the wave form is used with
 
@@ -72,6 +74,7 @@ struct MfmaLds {
 __host__ __device__ inline size_t al16(size_t v) { return (v + 15) & ~size_t(15); }
 
 // Objects added per accumulation step of a wave form (WaveAcc<M, P>::P).
+// Slabs per wave of a wave form.
 __host__ __device__ inline int wave_acc_p(int M, int acc)
 {
     if (acc == kAccWave1) return 1;
@@ -186,8 +189,9 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
     constexpr bool kAccum = MODE != kAssign;
     constexpr int kAcc = kAccum ? ACC : 0;
     constexpr bool kWaveForm = kAcc == kAccWave || kAcc == kAccWave1;
-    constexpr int PA = kAcc == kAccWave1 ? 1 : 0;        // WaveAcc slab-count parameter
-    constexpr int kP = WaveAcc<M, PA>::P;
+    constexpr int PA = 0;                                // most objects per step
+    constexpr bool kShared = kAcc == kAccWave1;          // ... into one slab per wave
+    constexpr int kP = kShared ? 1 : WaveAcc<M, PA>::P;  // slabs per wave
     extern __shared__ __align__(16) unsigned char smem[];
     const int W = blockDim.x / kWave;
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
@@ -526,7 +530,9 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
 
         if (kWaveForm) {
             // (labels read back may be out of range even in a full tile)
-            if (have) accumulate_tile<M, PA, kFullTile && MODE != kAccumLabels>(valid ? my_lab : -1, tile, offs, wslabs, K, lane);
+            if (have)
+                accumulate_tile<M, PA, kFullTile && MODE != kAccumLabels, kShared>(
+                    valid ? my_lab : -1, tile, offs, wslabs, K, lane);
         } else if (kAcc == kAccBlock) {
             // Wave w owns the clusters k with k % W == w (W is a power of two).
             // After a barrier it lists the members of its clusters over the
@@ -620,7 +626,7 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
 
     if (kWaveForm) {
         __syncthreads();
-        write_wave_partials<M, PA>(reinterpret_cast<const double *>(smem + L.slab), W, K,
+        write_wave_partials<M, PA, kShared>(reinterpret_cast<const double *>(smem + L.slab), W, K,
                                part_sums + (int64_t)blockIdx.x * K * M,
                                part_counts + (int64_t)blockIdx.x * K);
     } else if (kAcc == kAccBlock) {
