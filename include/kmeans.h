@@ -48,7 +48,8 @@ extern "C" {
 #define KMEANS_EINVAL        -1   /* NULL pointer, non-positive size, misaligned X, bad flags */
 #define KMEANS_EUNSUPPORTED  -2   /* shape outside the envelope above                        */
 #define KMEANS_EWORKSPACE    -3   /* workspace missing or smaller than kmeans_workspace_bytes */
-#define KMEANS_EHIP          -4   /* a HIP runtime call or kernel launch failed              */
+#define KMEANS_EHIP          -4   /* a HIP runtime call or kernel launch failed, or a kernel  */
+                                  /* reported that its ordered accumulation broke down      */
 
 /* Flags (bitwise OR). */
 #define KMEANS_FIXED_ITERS  (1u << 0) /* kmeans_run: run exactly max_iter iterations, no early stop */

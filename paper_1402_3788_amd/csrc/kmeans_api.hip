@@ -237,6 +237,7 @@ int kmeans_run(const float *X, int64_t n, int32_t M, int32_t K, const float *ini
         return rc;
     }
     *iterations = host.converged_at != 0 ? host.converged_at : max_iter;
+    if (host.ring_stalls != 0) rc = KMEANS_EHIP;
 
     if (timing) {
         timing->step_ms = 0.0;

@@ -24,12 +24,16 @@ constexpr int kCUs = 256;            // compute units the launch geometry is siz
 //   fallbacks      : objects whose label was re-decided in fp64 (diagnostic).
 //   reruns         : wave tiles whose split-precision scores left a call too
 //                    close, recomputed with fp32 products (diagnostic).
+//   ring_stalls    : waves of the tile kernel's ring form whose wait for their
+//                    turn gave up (never expected; the sums are then unordered
+//                    and kmeans_run fails with KMEANS_EHIP).
 struct Ctl {
     int32_t changed[2];
     int32_t converged_at;
     int32_t fallbacks;
     int32_t reruns;
-    int32_t pad[59];
+    int32_t ring_stalls;
+    int32_t pad[58];
 };
 static_assert(sizeof(Ctl) == 256, "control block is one 256-byte slot");
 

@@ -37,10 +37,12 @@
 //              applying the lanes of one add in a fixed order; at the end the
 //              workgroup adds the slabs in a fixed order. Used while W >= 4
 //              waves' private slabs fit in LDS (small K*M).
-//   block   -- one fp64 slab per workgroup: after a barrier, wave w owns the
-//              clusters k with k % W == w; it lists their members over the
-//              workgroup's W tiles in (tile, object) order (ballot + prefix
-//              count) and adds them one member per step. Used for large K*M.
+//   ring    -- one fp64 slab per workgroup that the waves take turns to add
+//              their tiles into, in the fixed cyclic order wave 0, 1, ..., W-1
+//              of every step (a turn counter in LDS; no barriers): one lane per
+//              object, one LDS fp64 add per feature, the LDS applying the lanes
+//              of one add in a fixed order. A wave's turn overlaps the other
+//              waves' distance work. Used for large K*M.
 #include "lloyd.h"
 #include "lloyd_device.h"
 
@@ -60,14 +62,14 @@ typedef float f4v __attribute__((ext_vector_type(4)));
 
 constexpr int kCols = 4;      // 16-object columns per wave tile (64 objects)
 constexpr int kAccWave = 1;    // per-wave slabs, WaveAcc<M>::Pmax objects per step
-constexpr int kAccBlock = 2;   // one slab per workgroup
+constexpr int kAccRing = 2;    // one slab per workgroup, waves add in turn
 constexpr int kAccWave1 = 3;   // one slab per wave, WaveAcc<M>::Pmax objects per step (less LDS)
 constexpr int kMaxWaves = 8;
 [[maybe_unused]] constexpr int kMinWaveForm = 4;   // fewest waves the wave form is used with
 
 // LDS carve-up of a workgroup (dynamic shared memory).
 struct MfmaLds {
-    size_t abf, cnorm, misc, tiles, offs, labs, members, slab, total;
+    size_t abf, cnorm, misc, tiles, offs, slab, total;
     int tile_floats;
 };
 
@@ -83,6 +85,11 @@ __host__ __device__ inline int wave_acc_p(int M, int acc)
     return kWave / lw;
 }
 
+// Row stride (doubles) of the ring form's slab: the M sums and the count,
+// rounded up to an odd count, so that rows of different clusters start on
+// different LDS banks (lanes of one add hit rows of arbitrary clusters).
+__host__ __device__ constexpr int ring_row(int M) { return (M + 1) | 1; }
+
 // 16-centre blocks, rounded up to an even count (the assignment loop works on
 // pairs of blocks; the padding centres score +inf).
 __host__ __device__ inline int centre_blocks(int K) { return ((K + 15) / 16 + 1) / 2 * 2; }
@@ -97,16 +104,41 @@ __host__ __device__ inline MfmaLds mfma_lds(int M, int K, int W, int acc)
     L.cnorm = o;   o = al16(o + (size_t)KT * 16 * 4);
     L.misc = o;    o = al16(o + 16);
     L.tiles = o;   o = al16(o + (size_t)W * L.tile_floats * 4);
-    L.offs = o;    o = al16(o + (size_t)W * kWave * 4);
     if (acc == kAccWave || acc == kAccWave1) {
+        L.offs = o;    o = al16(o + (size_t)W * kWave * 4);
         L.slab = o;    o = al16(o + (size_t)W * wave_acc_p(M, acc) * K * (M + 1) * 8);
-    } else if (acc == kAccBlock) {
-        L.labs = o;    o = al16(o + (size_t)W * kWave * 4);
-        L.members = o; o = al16(o + (size_t)W * W * kWave * 4);
-        L.slab = o;    o = al16(o + (size_t)K * (M + 1) * 8);
+    } else if (acc == kAccRing) {
+        L.slab = o;    o = al16(o + (size_t)K * ring_row(M) * 8);
     }
     L.total = o;
     return L;
+}
+
+// Turns of the ring form. The counter in LDS holds the number of turns taken
+// in the workgroup; wave w's turn of step s is number s*W + w. A wave waits for
+// its number with a bounded number of polls (so that every wave finishes even
+// if the order were ever broken; the caller reports a wait that gave up), and
+// passes the turn on once its LDS adds have completed.
+constexpr int kRingPolls = 1 << 22;
+
+__device__ inline bool ring_wait(const uint32_t *turn, uint32_t want)
+{
+    for (int p = 0; p < kRingPolls; ++p) {
+        const uint32_t now = __hip_atomic_load(turn, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        if (__builtin_amdgcn_readfirstlane(now) == want) {
+            __atomic_signal_fence(__ATOMIC_SEQ_CST);   // the adds stay after the wait
+            return true;
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
+    return false;
+}
+
+__device__ inline void ring_pass(uint32_t *turn, uint32_t next)
+{
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0xC07F);        // lgkmcnt(0): this wave's LDS adds are done
+    __hip_atomic_store(turn, next, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
 // Second-best of two (best, second) pairs, b1 <= b2 and p1 <= p2:
@@ -207,6 +239,7 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
     uint32_t *abf = reinterpret_cast<uint32_t *>(smem + L.abf);
     float *cnorm = reinterpret_cast<float *>(smem + L.cnorm);
     float *s_cmax = reinterpret_cast<float *>(smem + L.misc);
+    uint32_t *turn = reinterpret_cast<uint32_t *>(smem + L.misc + 4);
     double *wslabs = reinterpret_cast<double *>(smem + L.slab) + (size_t)wave * kP * K * (M + 1);
 
     // A block tile is the W wave tiles bt*W .. bt*W+W-1 of one workgroup step.
@@ -253,9 +286,10 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
     if (kWaveForm) {
         double *slabs = reinterpret_cast<double *>(smem + L.slab);
         for (int i = tid; i < W * kP * K * (M + 1); i += blockDim.x) slabs[i] = 0.0;
-    } else if (kAcc == kAccBlock) {
+    } else if (kAcc == kAccRing) {
         double *slab = reinterpret_cast<double *>(smem + L.slab);
-        for (int i = tid; i < K * (M + 1); i += blockDim.x) slab[i] = 0.0;
+        for (int i = tid; i < K * ring_row(M); i += blockDim.x) slab[i] = 0.0;
+        if (tid == 0) *turn = 0u;
     }
     __syncthreads();
     if (MODE != kAccumLabels) {
@@ -288,6 +322,8 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
     const int g = lane >> 4, l16 = lane & 15;
     int nfallback = 0;
     int nrerun = 0;     // wave tiles that needed the fp32 pass
+    uint32_t ring_seq = 0;   // steps taken (ring form)
+    bool ring_ok = true;     // every turn wait of this wave succeeded
 
     // One wave tile: stage it in LDS, put the loads of the tile two strides
     // ahead in flight in the same registers, assign, accumulate.
@@ -533,83 +569,35 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
             if (have)
                 accumulate_tile<M, PA, kFullTile && MODE != kAccumLabels, kShared>(
                     valid ? my_lab : -1, tile, offs, wslabs, K, lane);
-        } else if (kAcc == kAccBlock) {
-            // Wave w owns the clusters k with k % W == w (W is a power of two).
-            // After a barrier it lists the members of its clusters over the
-            // workgroup's W tiles in (tile, object) order (ballot + prefix
-            // count), in two lists by the parity of k / W when a row fits in 32
-            // lanes, and adds them: per step, each half-wave takes the next
-            // member of its list, lane j adds feature j and lane M the count
-            // into the workgroup slab rows this wave owns. Two lanes of one step
-            // never share a row, every row is written by one wave only, and the
-            // order of its additions is fixed by the data.
-            int32_t *labs = reinterpret_cast<int32_t *>(smem + L.labs);
-            int32_t *list = reinterpret_cast<int32_t *>(smem + L.members) + wave * W * kWave;
-            double *slab = reinterpret_cast<double *>(smem + L.slab);
-            constexpr int MW = M + 1;
-            constexpr bool kTwo = MW <= 32;            // two half-wave lists
-            const int cap = W * kWave;                 // list capacity
-            const int wshift = __builtin_ctz((unsigned)W);
-            labs[wave * kWave + lane] = valid ? my_lab : -1;
-            __syncthreads();
-            int cnt0 = 0, cnt1 = 0;
-            for (int v = 0; v < W; ++v) {
-                const int l = labs[v * kWave + lane];
-                const bool mine = l >= 0 && (l & (W - 1)) == wave;
-                const bool odd = kTwo && ((l >> wshift) & 1);
-                // entry: label in the high half, the member's row offset in the
-                // low half (< W * kSlot <= 8 * 4160)
-                const int ent = (l << 16) | (v * kSlot + lane * M);
-                const uint64_t m0 = __ballot(mine && !odd);
-                const uint64_t m1 = __ballot(mine && odd);
-                const uint64_t mm = odd ? m1 : m0;
-                const int rank = __builtin_amdgcn_mbcnt_hi(
-                    (uint32_t)(mm >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mm, 0u));
-                if (mine && !odd) list[cnt0 + rank] = ent;
-                if (mine && odd) list[cap - 1 - (cnt1 + rank)] = ent;   // second list grows down
-                cnt0 += __popcll(m0);
-                cnt1 += __popcll(m1);
+        } else if (kAcc == kAccRing) {
+            // This wave's turn of the step (every wave takes it, with or
+            // without objects): lane l adds object l's features and count to
+            // its cluster's row of the workgroup slab. The features are read
+            // from the wave's own tile before the wait.
+            const bool adds = valid && my_lab >= 0;
+            float xv[M];
+#pragma unroll
+            for (int j = 0; j < M; ++j) xv[j] = tile[lane * M + j];
+            const uint32_t want =
+                __builtin_amdgcn_readfirstlane(ring_seq * (uint32_t)W + (uint32_t)wave);
+            if (ring_ok) ring_ok = ring_wait(turn, want);
+            if (adds) {
+                constexpr int RS = ring_row(M);
+                double *row = reinterpret_cast<double *>(smem + L.slab) + (int64_t)my_lab * RS;
+#pragma unroll
+                for (int j = 0; j < M; ++j)
+                    __hip_atomic_fetch_add(row + j, (double)xv[j], __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_WORKGROUP);
+                __hip_atomic_fetch_add(row + M, 1.0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
             }
-            __builtin_amdgcn_wave_barrier();
-            const int h = kTwo ? (lane >> 5) : 0;
-            const int j = kTwo ? (lane & 31) : lane;
-            const bool feat = j < M;
-            const int jr = feat ? j : 0;
-            const int my_cnt = h ? cnt1 : cnt0;
-            const int steps = kTwo ? (cnt0 > cnt1 ? cnt0 : cnt1) : cnt0;
-            if (j <= M) {
-                constexpr int B = 8;
-                for (int e0 = 0; e0 < steps; e0 += B) {
-                    int ent[B];
-                    float xv[B];
-#pragma unroll
-                    for (int b = 0; b < B; ++b) {    // past the list: entry 0, ignored below
-                        const int e = e0 + b;
-                        ent[b] = e < my_cnt ? list[h ? cap - 1 - e : e] : 0;
-                    }
-#pragma unroll
-                    for (int b = 0; b < B; ++b) xv[b] = tiles[(ent[b] & 0xFFFF) + jr];
-#pragma unroll
-                    for (int b = 0; b < B; ++b) {
-                        if (e0 + b < my_cnt) {
-                            const double v = (double)(feat ? xv[b] : 1.0f);
-                            double *row = slab + (int64_t)(ent[b] >> 16) * MW;
-                            __hip_atomic_fetch_add(row + j, v, __ATOMIC_RELAXED,
-                                                   __HIP_MEMORY_SCOPE_WAVEFRONT);
-                            if (M + 1 > kWave && lane == 0)   // M = 64: no lane left for the count
-                                __hip_atomic_fetch_add(row + M, 1.0, __ATOMIC_RELAXED,
-                                                       __HIP_MEMORY_SCOPE_WAVEFRONT);
-                        }
-                    }
-                }
-            }
-            __syncthreads();
+            ring_pass(turn, want + 1);
+            ++ring_seq;
         }
     };
 
     // Block tiles are taken in strides of the grid; the register buffers
-    // alternate. Every wave of a workgroup runs the same steps (the block form
-    // has barriers inside).
+    // alternate. Every wave of a workgroup runs the same steps (the ring form
+    // needs every wave's turn in every step).
     for (int64_t bt = bt0; bt < nbt_main; bt += 2 * G) {
         step(bt, std::integral_constant<int, 0>{}, std::true_type{});
         if (bt + G < nbt_main) step(bt + G, std::integral_constant<int, 1>{}, std::true_type{});
@@ -623,19 +611,21 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
 
     if (ctl != nullptr && lane == 0 && nfallback > 0) atomicAdd(&ctl->fallbacks, nfallback);
     if (ctl != nullptr && lane == 0 && nrerun > 0) atomicAdd(&ctl->reruns, nrerun);
+    if (kAcc == kAccRing && ctl != nullptr && lane == 0 && !ring_ok) atomicAdd(&ctl->ring_stalls, 1);
 
     if (kWaveForm) {
         __syncthreads();
         write_wave_partials<M, PA, kShared>(reinterpret_cast<const double *>(smem + L.slab), W, K,
                                part_sums + (int64_t)blockIdx.x * K * M,
                                part_counts + (int64_t)blockIdx.x * K);
-    } else if (kAcc == kAccBlock) {
+    } else if (kAcc == kAccRing) {
         __syncthreads();
+        constexpr int RS = ring_row(M);
         const double *slab = reinterpret_cast<const double *>(smem + L.slab);
         double *out = part_sums + (int64_t)blockIdx.x * K * M;
-        for (int e = tid; e < K * M; e += blockDim.x) out[e] = slab[(e / M) * (M + 1) + e % M];
+        for (int e = tid; e < K * M; e += blockDim.x) out[e] = slab[(e / M) * RS + e % M];
         for (int k = tid; k < K; k += blockDim.x)
-            part_counts[(int64_t)blockIdx.x * K + k] = (int32_t)slab[k * (M + 1) + M];
+            part_counts[(int64_t)blockIdx.x * K + k] = (int32_t)slab[k * RS + M];
     }
 }
 
@@ -658,12 +648,12 @@ hipError_t launch_m(const StepArgs &a, Mode mode, const AccumPlan &p, hipStream_
     case kAssignAccum:
         if (p.accum == kAccWave) LLOYD_MFMA_LAUNCH(kAssignAccum, kAccWave);
         else if (p.accum == kAccWave1) LLOYD_MFMA_LAUNCH(kAssignAccum, kAccWave1);
-        else LLOYD_MFMA_LAUNCH(kAssignAccum, kAccBlock);
+        else LLOYD_MFMA_LAUNCH(kAssignAccum, kAccRing);
         break;
     case kAccumLabels:
         if (p.accum == kAccWave) LLOYD_MFMA_LAUNCH(kAccumLabels, kAccWave);
         else if (p.accum == kAccWave1) LLOYD_MFMA_LAUNCH(kAccumLabels, kAccWave1);
-        else LLOYD_MFMA_LAUNCH(kAccumLabels, kAccBlock);
+        else LLOYD_MFMA_LAUNCH(kAccumLabels, kAccRing);
         break;
     }
 #undef LLOYD_MFMA_LAUNCH
@@ -718,9 +708,8 @@ AccumPlan plan_tile(int64_t n, int M, int K, Mode mode)
             acc = kAccWave1;
             W = w_1;
         } else {
-            acc = kAccBlock;
-            W = most_waves(kAccBlock);
-            while (W & (W - 1)) --W;          // cluster ownership is k % W, W a power of two
+            acc = kAccRing;
+            W = most_waves(kAccRing);
         }
     }
     // no more waves than there are 64-object tiles
@@ -736,7 +725,7 @@ AccumPlan plan_tile(int64_t n, int M, int K, Mode mode)
 
 bool tile_fits(int M, int K)
 {
-    return mfma_lds(M, K, 1, kAccBlock).total <= (size_t)kMaxLds;
+    return mfma_lds(M, K, 1, kAccRing).total <= (size_t)kMaxLds;
 }
 
 hipError_t launch_tile(const StepArgs &a, Mode mode, const AccumPlan &plan, hipStream_t s)

@@ -217,12 +217,16 @@ def test_update_parity(n, M, K):
     check_centers(P.cpu().numpy(), oC)
 
 
+@pytest.mark.parametrize("K", [64, 256])
 @pytest.mark.parametrize("path", PATHS)
-def test_determinism(path):
-    X, C0 = workloads.random_case(200_003, 25, 64, seed=1, kind="uniform")
+def test_determinism(path, K):
+    # K = 64: per-wave slabs; K = 256: the tile kernel's workgroup slab that
+    # the waves add into in turn
+    _say(f"[determinism] K={K} path={path}")
+    X, C0 = workloads.random_case(200_003, 25, K, seed=1, kind="uniform")
     Xg, Cg = _gpu(X), _gpu(C0)
-    a = km.kmeans_run(Xg, 64, Cg, 12, fixed_iters=True, path=path)
-    b = km.kmeans_run(Xg, 64, Cg, 12, fixed_iters=True, path=path)
+    a = km.kmeans_run(Xg, K, Cg, 12, fixed_iters=True, path=path)
+    b = km.kmeans_run(Xg, K, Cg, 12, fixed_iters=True, path=path)
     for u, v in zip(a[:3], b[:3]):
         assert torch.equal(u, v)
     assert a[3] == b[3] == 12
