@@ -46,6 +46,7 @@
 #include "lloyd.h"
 #include "lloyd_device.h"
 
+#include <float.h>
 #include <math.h>
 
 #include <array>
@@ -61,9 +62,11 @@ namespace {
 typedef float f4v __attribute__((ext_vector_type(4)));
 
 constexpr int kCols = 4;      // 16-object columns per wave tile (64 objects)
+constexpr int kKeyBlocks = 16; // centre blocks per packed-key group (256 centres, 8 index bits)
 constexpr int kAccWave = 1;    // per-wave slabs, WaveAcc<M>::Pmax objects per step
 constexpr int kAccRing = 2;    // one slab per workgroup, waves add in turn
 constexpr int kAccWave1 = 3;   // one slab per wave, WaveAcc<M>::Pmax objects per step (less LDS)
+constexpr int kAccLane = 4;    // one slab per wave, one lane per object
 constexpr int kMaxWaves = 8;
 [[maybe_unused]] constexpr int kMinWaveForm = 4;   // fewest waves the wave form is used with
 
@@ -109,6 +112,8 @@ __host__ __device__ inline MfmaLds mfma_lds(int M, int K, int W, int acc)
         L.slab = o;    o = al16(o + (size_t)W * wave_acc_p(M, acc) * K * (M + 1) * 8);
     } else if (acc == kAccRing) {
         L.slab = o;    o = al16(o + (size_t)K * ring_row(M) * 8);
+    } else if (acc == kAccLane) {
+        L.slab = o;    o = al16(o + (size_t)W * K * ring_row(M) * 8);
     }
     L.total = o;
     return L;
@@ -183,18 +188,36 @@ __device__ inline float sum_rows(float v)
 // bits of v, lo = the top 16 bits of the exact remainder v - hi. Then
 // |v - hi| < 2^-7 |v| and |v - hi - lo| < 2^-14 |v| (v finite). Parts are
 // packed two per dword, element 2e in the low half of dword e, as the bf16
-// operands of v_mfma_f32_16x16x32_bf16 expect.
+// operands of v_mfma_f32_16x16x32_bf16 expect (v_perm_b32 takes the top two
+// bytes of each of the pair).
 __device__ inline void split_bf16x8(const float (&v)[8], uint32_t (&hi)[4], uint32_t (&lo)[4])
 {
+    constexpr uint32_t kTopHalves = 0x07060302u;   // bytes 2, 3 of the second, then of the first
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-        const uint32_t h0 = __float_as_uint(v[2 * e]) & 0xFFFF0000u;
-        const uint32_t h1 = __float_as_uint(v[2 * e + 1]) & 0xFFFF0000u;
-        const uint32_t l0 = __float_as_uint(v[2 * e] - __uint_as_float(h0)) & 0xFFFF0000u;
-        const uint32_t l1 = __float_as_uint(v[2 * e + 1] - __uint_as_float(h1)) & 0xFFFF0000u;
-        hi[e] = (h0 >> 16) | h1;
-        lo[e] = (l0 >> 16) | l1;
+        const uint32_t u0 = __float_as_uint(v[2 * e]), u1 = __float_as_uint(v[2 * e + 1]);
+        const uint32_t l0 = __float_as_uint(v[2 * e] - __uint_as_float(u0 & 0xFFFF0000u));
+        const uint32_t l1 = __float_as_uint(v[2 * e + 1] - __uint_as_float(u1 & 0xFFFF0000u));
+        hi[e] = __builtin_amdgcn_perm(u1, u0, kTopHalves);
+        lo[e] = __builtin_amdgcn_perm(l1, l0, kTopHalves);
     }
+}
+
+// Merge the packed (best, second) keys of lanes l and l ^ 16 (ROW = 16) or
+// l and l ^ 32 (ROW = 32); keys of different centres never compare equal.
+template <int ROW>
+__device__ inline void merge_keys(float &k1, float &k2)
+{
+    auto swap = [](uint32_t v) {
+        if (ROW == 16) return __builtin_amdgcn_permlane16_swap(v, v, false, false);
+        return __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    };
+    const auto s1 = swap(__float_as_uint(k1));
+    const auto s2 = swap(__float_as_uint(k2));
+    const float f1 = __uint_as_float(s1[0]), g1 = __uint_as_float(s1[1]);
+    const float f2 = __uint_as_float(s2[0]), g2 = __uint_as_float(s2[1]);
+    k2 = second_of(f1, f2, g1, g2);
+    k1 = fminf(f1, g1);
 }
 
 typedef __bf16 bf8v __attribute__((ext_vector_type(8)));
@@ -286,16 +309,19 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
     if (kWaveForm) {
         double *slabs = reinterpret_cast<double *>(smem + L.slab);
         for (int i = tid; i < W * kP * K * (M + 1); i += blockDim.x) slabs[i] = 0.0;
-    } else if (kAcc == kAccRing) {
+    } else if (kAcc == kAccRing || kAcc == kAccLane) {
         double *slab = reinterpret_cast<double *>(smem + L.slab);
-        for (int i = tid; i < K * ring_row(M); i += blockDim.x) slab[i] = 0.0;
+        const int rows = kAcc == kAccLane ? W * K : K;
+        for (int i = tid; i < rows * ring_row(M); i += blockDim.x) slab[i] = 0.0;
         if (tid == 0) *turn = 0u;
     }
     __syncthreads();
     if (MODE != kAccumLabels) {
         // |c_k|^2 in fp32, features in order
+        // padding centres (k >= K) get the largest finite norm: their scores
+        // stay finite (a packed key of an infinite score would be a NaN)
         for (int k = tid; k < KT * 16; k += blockDim.x) {
-            float nk = INFINITY;
+            float nk = FLT_MAX;
             if (k < K) {
                 nk = 0.f;
 #pragma unroll
@@ -400,31 +426,39 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
             // Both passes keep two accumulator sets and two operand sets: the
             // matrix cores compute one centre block while the vector ALU scans
             // the previous one and the next block's operands arrive.
-            auto blocks = [&](auto &oA, auto &oB, auto load_ops, auto chain) {
+            // Blocks t0 .. t1-1 (an even count).
+            auto blocks = [&](int t0, int t1, auto &oA, auto &oB, auto load_ops, auto chain,
+                              auto scan_fn) {
                 f4v dA[kCols], dB[kCols];
-                load_ops(0, oA);
-                load_ops(1, oB);
+                load_ops(t0, oA);
+                load_ops(t0 + 1, oB);
                 chain(oA, dA);
-                int tt = 0;
-                for (; tt + 2 < KT; tt += 2) {
+                int tt = t0;
+                for (; tt + 2 < t1; tt += 2) {
                     load_ops(tt + 2, oA);
                     chain(oB, dB);
-                    scan(tt, dA);
+                    scan_fn(tt, dA);
                     load_ops(tt + 3, oB);
                     chain(oA, dA);
-                    scan(tt + 1, dB);
+                    scan_fn(tt + 1, dB);
                 }
                 chain(oB, dB);
-                scan(tt, dA);
-                scan(tt + 1, dB);
+                scan_fn(tt, dA);
+                scan_fn(tt + 1, dB);
             };
 
             // ---- pass 1: split-precision products on the bf16 matrix cores.
-            // B operands: object 16c + l16, features 32q + 8g .. 32q + 8g + 7
-            // (zero past M), split into bf16 hi and lo; A likewise (table in
-            // LDS). Each centre block is three products per column,
+            // B operands: object 16c + l16, features 32q + 8g .. 32q + 8g + 7,
+            // split into bf16 hi and lo; A likewise (table in LDS, zero past M).
+            // Each centre block is three products per column,
             // lo(A) hi(B) + hi(A) lo(B) + hi(A) hi(B), on top of |c|^2.
+            // Past M the A operands are zero, so the B values there only need
+            // to be finite: with M >= 16 the tile's zero slack covers the last
+            // row's reads past M and the rows are read straight through (the
+            // next object's features), else the reads are clamped to the row;
+            // |x|^2 masks them out.
             {
+                constexpr bool kClampReads = M < 16;
                 uint32_t bh[kCols][KC][4], bl[kCols][KC][4];
 #pragma unroll
                 for (int c = 0; c < kCols; ++c) {
@@ -436,10 +470,11 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
 #pragma unroll
                         for (int e = 0; e < 8; ++e) {
                             const int f = 32 * qc + 8 * g + e;
-                            // (the read stays inside the row; the value past M is 0)
-                            const float x = row[f < M ? f : M - 1];
-                            v[e] = f < M ? x : 0.f;
-                            acc = __builtin_fmaf(v[e], v[e], acc);
+                            v[e] = kClampReads ? row[f < M ? f : M - 1] : row[f];
+                            // in range for every lane group: no mask needed
+                            const bool always = 32 * qc + 24 + e < M;
+                            const float m = (always || f < M) ? v[e] : 0.f;
+                            acc = __builtin_fmaf(m, m, acc);
                         }
                         split_bf16x8(v, bh[c][qc], bl[c][qc]);
                     }
@@ -480,20 +515,82 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
                                 as_bf8(o.ah[qc]), as_bf8(bh[c][qc]), d[c], 0, 0, 0);
                     }
                 };
+                // Scan with packed keys: a score with its low 8 bits replaced by
+                // the centre's index within its group of 256 centres (16
+                // blocks), so that min / med3 / min keep the best and second
+                // best keys and the label comes with the best one. Per group
+                // the four lanes of an object merge their keys, and the group
+                // folds into a running (best, second, label) per column.
+                float g1[kCols], g2[kCols];
+                int gl[kCols];
+                float k1[kCols], k2[kCols];
+#pragma unroll
+                for (int c = 0; c < kCols; ++c) {
+                    g1[c] = INFINITY;
+                    g2[c] = INFINITY;
+                    gl[c] = 0;
+                }
+                int kt0 = 0;
+                auto scan_key = [&](int tt, const f4v (&d)[kCols]) {
+                    const uint32_t i0 = (uint32_t)((tt - kt0) * 16 + 4 * g);
+#pragma unroll
+                    for (int c = 0; c < kCols; ++c)
+#pragma unroll
+                        for (int r = 0; r < 4; r += 2) {
+                            const float s1 = __uint_as_float(
+                                (__float_as_uint(d[c][r]) & 0xFFFFFF00u) | (i0 + r));
+                            const float s2 = __uint_as_float(
+                                (__float_as_uint(d[c][r + 1]) & 0xFFFFFF00u) | (i0 + r + 1));
+                            const float n2 = fminf(k2[c], __builtin_amdgcn_fmed3f(k1[c], s1, s2));
+                            k1[c] = fminf(fminf(k1[c], s1), s2);
+                            k2[c] = n2;
+                        }
+                };
                 OpsH oA, oB;
-                reset();
-                blocks(oA, oB, load_h, chain_h);
-                finish();
+                for (; kt0 < KT; kt0 += kKeyBlocks) {
+                    const int kt1 = KT - kt0 < kKeyBlocks ? KT : kt0 + kKeyBlocks;
+#pragma unroll
+                    for (int c = 0; c < kCols; ++c) {
+                        k1[c] = INFINITY;
+                        k2[c] = INFINITY;
+                    }
+                    blocks(kt0, kt1, oA, oB, load_h, chain_h, scan_key);
+#pragma unroll
+                    for (int c = 0; c < kCols; ++c) {
+                        merge_keys<16>(k1[c], k2[c]);
+                        merge_keys<32>(k1[c], k2[c]);
+                        const int lab = kt0 * 16 + (int)(__float_as_uint(k1[c]) & 0xFFu);
+                        const bool take = k1[c] < g1[c];
+                        g2[c] = second_of(g1[c], g2[c], k1[c], k2[c]);
+                        g1[c] = take ? k1[c] : g1[c];
+                        gl[c] = take ? lab : gl[c];
+                    }
+                }
+                mb1 = g1[0];
+                mb2 = g2[0];
+                mx = xsq[0];
+                ml = gl[0];
+#pragma unroll
+                for (int c = 1; c < kCols; ++c) {
+                    const bool mine = g == c;
+                    mb1 = mine ? g1[c] : mb1;
+                    mb2 = mine ? g2[c] : mb2;
+                    mx = mine ? xsq[c] : mx;
+                    ml = mine ? gl[c] : ml;
+                }
             }
             // Error of a pass-1 score against the exact score |c|^2 - 2 x.c:
             // the dropped terms lo(A) lo(B), and the parts' truncation, are
             // below 3.02 * 2^-14 |2 c_j x_j| per feature; the fp32 sums of the
             // 96 KC + 1 exact terms add gamma_{96 KC + 2}; |c|^2 in fp32 adds
             // gamma_M |c|^2. With 2|c_j x_j| <= c_j^2 + x_j^2 each score is
-            // within E (|x|^2 + 3|c|^2), E = 3.02 * 2^-14 + 1.03 gamma, so the
-            // label stands when the two best scores differ by more than twice
-            // that (with margins).
-            constexpr float kE1 = 3.02f * 6.1035156e-05f + 1.03f * (float)(96 * KC + 2) * 5.9604645e-8f;
+            // within E (|x|^2 + 3|c|^2), E = 3.02 * 2^-14 + 1.03 gamma; a packed
+            // key moves its score by less than 2^-15 of the score's magnitude,
+            // itself below (1 + E)(|x|^2 + 3|c|^2). So the label stands when the
+            // two best keys differ by more than twice E + 1.01 * 2^-15 (with
+            // margins).
+            constexpr float kE1 = 3.02f * 6.1035156e-05f + 1.03f * (float)(96 * KC + 2) * 5.9604645e-8f +
+                                  1.01f * 3.0517578e-05f;
             const float thr1 = 2.02f * kE1 * (3.02f * cmax + 1.0001f * mx) + 1e-30f;
             bool ok = (K == 1) || (mb2 - mb1 > thr1);
 
@@ -535,12 +632,15 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
                 };
                 Ops oA, oB;
                 reset();
-                blocks(oA, oB, load_ops, chain);
+                blocks(0, KT, oA, oB, load_ops, chain, scan);
                 finish();
                 const float thr = kGuard * (3.02f * cmax + 1.0001f * mx) + 1e-30f;
                 ok = (K == 1) || (mb2 - mb1 > thr);
                 if (ctl != nullptr && lane == 0) ++nrerun;
             }
+            // a padding centre (index >= K, |c|^2 = FLT_MAX) wins only when
+            // every real score overflows; keep such a label in range
+            ml = ml < K ? ml : K - 1;
             float dmin = 0.f;
             if (valid && !ok) {
                 double bd;
@@ -569,29 +669,33 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
             if (have)
                 accumulate_tile<M, PA, kFullTile && MODE != kAccumLabels, kShared>(
                     valid ? my_lab : -1, tile, offs, wslabs, K, lane);
-        } else if (kAcc == kAccRing) {
-            // This wave's turn of the step (every wave takes it, with or
-            // without objects): lane l adds object l's features and count to
-            // its cluster's row of the workgroup slab. The features are read
-            // from the wave's own tile before the wait.
+        } else if (kAcc == kAccRing || kAcc == kAccLane) {
+            // Lane l adds object l's features and count to its cluster's row:
+            // of the workgroup slab in this wave's turn of the step (ring;
+            // every wave takes its turn, with or without objects), or of the
+            // wave's own slab (lane form). The features are read from the
+            // wave's tile first (before the wait).
             const bool adds = valid && my_lab >= 0;
             float xv[M];
 #pragma unroll
             for (int j = 0; j < M; ++j) xv[j] = tile[lane * M + j];
             const uint32_t want =
                 __builtin_amdgcn_readfirstlane(ring_seq * (uint32_t)W + (uint32_t)wave);
-            if (ring_ok) ring_ok = ring_wait(turn, want);
+            if (kAcc == kAccRing && ring_ok) ring_ok = ring_wait(turn, want);
             if (adds) {
                 constexpr int RS = ring_row(M);
-                double *row = reinterpret_cast<double *>(smem + L.slab) + (int64_t)my_lab * RS;
+                double *row = reinterpret_cast<double *>(smem + L.slab) +
+                              ((kAcc == kAccLane ? (int64_t)wave * K : 0) + my_lab) * RS;
 #pragma unroll
                 for (int j = 0; j < M; ++j)
                     __hip_atomic_fetch_add(row + j, (double)xv[j], __ATOMIC_RELAXED,
                                            __HIP_MEMORY_SCOPE_WORKGROUP);
                 __hip_atomic_fetch_add(row + M, 1.0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
             }
-            ring_pass(turn, want + 1);
-            ++ring_seq;
+            if (kAcc == kAccRing) {
+                ring_pass(turn, want + 1);
+                ++ring_seq;
+            }
         }
     };
 
@@ -618,14 +722,20 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
         write_wave_partials<M, PA, kShared>(reinterpret_cast<const double *>(smem + L.slab), W, K,
                                part_sums + (int64_t)blockIdx.x * K * M,
                                part_counts + (int64_t)blockIdx.x * K);
-    } else if (kAcc == kAccRing) {
+    } else if (kAcc == kAccRing || kAcc == kAccLane) {
+        // (lane form: the waves' slabs added in wave order)
         __syncthreads();
         constexpr int RS = ring_row(M);
+        const int nslab = kAcc == kAccLane ? W : 1;
         const double *slab = reinterpret_cast<const double *>(smem + L.slab);
         double *out = part_sums + (int64_t)blockIdx.x * K * M;
-        for (int e = tid; e < K * M; e += blockDim.x) out[e] = slab[(e / M) * RS + e % M];
-        for (int k = tid; k < K; k += blockDim.x)
-            part_counts[(int64_t)blockIdx.x * K + k] = (int32_t)slab[k * RS + M];
+        for (int e = tid; e < K * (M + 1); e += blockDim.x) {
+            const int k = e / (M + 1), j = e % (M + 1);
+            double v = slab[k * RS + j];
+            for (int w = 1; w < nslab; ++w) v = v + slab[((int64_t)w * K + k) * RS + j];
+            if (j < M) out[(int64_t)k * M + j] = v;
+            else part_counts[(int64_t)blockIdx.x * K + k] = (int32_t)v;
+        }
     }
 }
 
@@ -648,11 +758,13 @@ hipError_t launch_m(const StepArgs &a, Mode mode, const AccumPlan &p, hipStream_
     case kAssignAccum:
         if (p.accum == kAccWave) LLOYD_MFMA_LAUNCH(kAssignAccum, kAccWave);
         else if (p.accum == kAccWave1) LLOYD_MFMA_LAUNCH(kAssignAccum, kAccWave1);
+        else if (p.accum == kAccLane) LLOYD_MFMA_LAUNCH(kAssignAccum, kAccLane);
         else LLOYD_MFMA_LAUNCH(kAssignAccum, kAccRing);
         break;
     case kAccumLabels:
         if (p.accum == kAccWave) LLOYD_MFMA_LAUNCH(kAccumLabels, kAccWave);
         else if (p.accum == kAccWave1) LLOYD_MFMA_LAUNCH(kAccumLabels, kAccWave1);
+        else if (p.accum == kAccLane) LLOYD_MFMA_LAUNCH(kAccumLabels, kAccLane);
         else LLOYD_MFMA_LAUNCH(kAccumLabels, kAccRing);
         break;
     }
