@@ -201,6 +201,11 @@ def main():
         "kernel_avg_us": round(assign_avg_s * 1e6, 3),
         "iteration_avg_us": round(step_avg_s * 1e6, 3),
         "assign_launches_timed": tm.assign_samples,
+        # close calls of the timed run, per iteration: 64-object tiles whose
+        # split-precision scores were recomputed with fp32 products (tile
+        # kernel), objects re-decided in fp64 (both kernels)
+        "reruns_per_iteration": round(km.ctl_reruns(ws) / args.steps, 2),
+        "fallbacks_per_iteration": round(km.ctl_fallbacks(ws) / args.steps, 2),
         "roofline": {
             "bound": "hbm",
             "achieved": round(achieved, 1),

@@ -62,7 +62,12 @@ namespace {
 typedef float f4v __attribute__((ext_vector_type(4)));
 
 constexpr int kCols = 4;      // 16-object columns per wave tile (64 objects)
-constexpr int kKeyBlocks = 16; // centre blocks per packed-key group (256 centres, 8 index bits)
+// Index bits of a packed key: enough for the (padded) centres, at most 8;
+// a group of 2^bits centres shares one running best / second best.
+__host__ __device__ inline int key_bits(int KT)
+{
+    return KT <= 2 ? 5 : KT <= 4 ? 6 : KT <= 8 ? 7 : 8;
+}
 constexpr int kAccWave = 1;    // per-wave slabs, WaveAcc<M>::Pmax objects per step
 constexpr int kAccRing = 2;    // one slab per workgroup, waves add in turn
 constexpr int kAccWave1 = 3;   // one slab per wave, WaveAcc<M>::Pmax objects per step (less LDS)
@@ -184,22 +189,31 @@ __device__ inline float sum_rows(float v)
     return __uint_as_float(s[0]) + __uint_as_float(s[1]);
 }
 
-// Split eight fp32 values v into bf16 parts by truncation: hi = the top 16
-// bits of v, lo = the top 16 bits of the exact remainder v - hi. Then
-// |v - hi| < 2^-7 |v| and |v - hi - lo| < 2^-14 |v| (v finite). Parts are
-// packed two per dword, element 2e in the low half of dword e, as the bf16
-// operands of v_mfma_f32_16x16x32_bf16 expect (v_perm_b32 takes the top two
-// bytes of each of the pair).
+typedef __bf16 bf2v __attribute__((ext_vector_type(2)));
+typedef float f2v __attribute__((ext_vector_type(2)));
+
+// Two fp32 values rounded to nearest-even bf16 (v_cvt_pk_bf16_f32), packed
+// with the first in the low half.
+__device__ inline uint32_t bf16x2_rne(float a, float b)
+{
+    const f2v v = {a, b};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf2v));
+}
+
+// Split eight fp32 values v into bf16 parts rounded to nearest: hi = bf16(v),
+// lo = bf16(v - hi), the remainder being exact (hi is within a factor 2 of v).
+// With the bf16 unit roundoff 2^-8, |v - hi| <= 2^-8 |v| and
+// |v - hi - lo| <= 2^-16 |v| (v finite and below the bf16 overflow
+// threshold). Parts are packed two per dword, element 2e in the low half of
+// dword e, as the bf16 operands of v_mfma_f32_16x16x32_bf16 expect.
 __device__ inline void split_bf16x8(const float (&v)[8], uint32_t (&hi)[4], uint32_t (&lo)[4])
 {
-    constexpr uint32_t kTopHalves = 0x07060302u;   // bytes 2, 3 of the second, then of the first
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-        const uint32_t u0 = __float_as_uint(v[2 * e]), u1 = __float_as_uint(v[2 * e + 1]);
-        const uint32_t l0 = __float_as_uint(v[2 * e] - __uint_as_float(u0 & 0xFFFF0000u));
-        const uint32_t l1 = __float_as_uint(v[2 * e + 1] - __uint_as_float(u1 & 0xFFFF0000u));
-        hi[e] = __builtin_amdgcn_perm(u1, u0, kTopHalves);
-        lo[e] = __builtin_amdgcn_perm(l1, l0, kTopHalves);
+        const uint32_t h = bf16x2_rne(v[2 * e], v[2 * e + 1]);
+        hi[e] = h;
+        lo[e] = bf16x2_rne(v[2 * e] - __uint_as_float(h << 16),
+                           v[2 * e + 1] - __uint_as_float(h & 0xFFFF0000u));
     }
 }
 
@@ -252,6 +266,7 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int tid = threadIdx.x;
     const int KT = centre_blocks(K);       // even
+    const int kbits = key_bits(KT);        // index bits of the packed keys
 
     if (MODE == kAssignAccum && stop_before(ctl, t, fixed)) return;
 
@@ -515,12 +530,14 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
                                 as_bf8(o.ah[qc]), as_bf8(bh[c][qc]), d[c], 0, 0, 0);
                     }
                 };
-                // Scan with packed keys: a score with its low 8 bits replaced by
-                // the centre's index within its group of 256 centres (16
-                // blocks), so that min / med3 / min keep the best and second
+                // Scan with packed keys: a score with its low `bits` bits
+                // replaced by the centre's index within its group of 2^bits
+                // centres, so that min / med3 / min keep the best and second
                 // best keys and the label comes with the best one. Per group
                 // the four lanes of an object merge their keys, and the group
                 // folds into a running (best, second, label) per column.
+                const int gblocks = (1 << kbits) / 16;            // even
+                const uint32_t kmask = ~((1u << kbits) - 1u);
                 float g1[kCols], g2[kCols];
                 int gl[kCols];
                 float k1[kCols], k2[kCols];
@@ -538,17 +555,17 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
 #pragma unroll
                         for (int r = 0; r < 4; r += 2) {
                             const float s1 = __uint_as_float(
-                                (__float_as_uint(d[c][r]) & 0xFFFFFF00u) | (i0 + r));
+                                (__float_as_uint(d[c][r]) & kmask) | (i0 + r));
                             const float s2 = __uint_as_float(
-                                (__float_as_uint(d[c][r + 1]) & 0xFFFFFF00u) | (i0 + r + 1));
+                                (__float_as_uint(d[c][r + 1]) & kmask) | (i0 + r + 1));
                             const float n2 = fminf(k2[c], __builtin_amdgcn_fmed3f(k1[c], s1, s2));
                             k1[c] = fminf(fminf(k1[c], s1), s2);
                             k2[c] = n2;
                         }
                 };
                 OpsH oA, oB;
-                for (; kt0 < KT; kt0 += kKeyBlocks) {
-                    const int kt1 = KT - kt0 < kKeyBlocks ? KT : kt0 + kKeyBlocks;
+                for (; kt0 < KT; kt0 += gblocks) {
+                    const int kt1 = KT - kt0 < gblocks ? KT : kt0 + gblocks;
 #pragma unroll
                     for (int c = 0; c < kCols; ++c) {
                         k1[c] = INFINITY;
@@ -559,7 +576,7 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
                     for (int c = 0; c < kCols; ++c) {
                         merge_keys<16>(k1[c], k2[c]);
                         merge_keys<32>(k1[c], k2[c]);
-                        const int lab = kt0 * 16 + (int)(__float_as_uint(k1[c]) & 0xFFu);
+                        const int lab = kt0 * 16 + (int)(__float_as_uint(k1[c]) & ~kmask);
                         const bool take = k1[c] < g1[c];
                         g2[c] = second_of(g1[c], g2[c], k1[c], k2[c]);
                         g1[c] = take ? k1[c] : g1[c];
@@ -580,18 +597,21 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
                 }
             }
             // Error of a pass-1 score against the exact score |c|^2 - 2 x.c:
-            // the dropped terms lo(A) lo(B), and the parts' truncation, are
-            // below 3.02 * 2^-14 |2 c_j x_j| per feature; the fp32 sums of the
-            // 96 KC + 1 exact terms add gamma_{96 KC + 2}; |c|^2 in fp32 adds
-            // gamma_M |c|^2. With 2|c_j x_j| <= c_j^2 + x_j^2 each score is
-            // within E (|x|^2 + 3|c|^2), E = 3.02 * 2^-14 + 1.03 gamma; a packed
-            // key moves its score by less than 2^-15 of the score's magnitude,
-            // itself below (1 + E)(|x|^2 + 3|c|^2). So the label stands when the
-            // two best keys differ by more than twice E + 1.01 * 2^-15 (with
-            // margins).
-            constexpr float kE1 = 3.02f * 6.1035156e-05f + 1.03f * (float)(96 * KC + 2) * 5.9604645e-8f +
-                                  1.01f * 3.0517578e-05f;
-            const float thr1 = 2.02f * kE1 * (3.02f * cmax + 1.0001f * mx) + 1e-30f;
+            // with a = ah + al + ea, b = bh + bl + eb (|ea| <= 2^-16 |a|, |al|
+            // <= 2^-8 (1 + 2^-8) |a|, likewise b) the dropped terms
+            // (a - ea) eb + al bl + ea b are below 3.02 * 2^-16 |a b| per
+            // feature; the products are exact in fp32 and their fp32 sums with
+            // |c|^2 add gamma_{96 KC + 2} of the terms' magnitudes; |c|^2 in
+            // fp32 adds gamma_M |c|^2. With 2|c_j x_j| <= c_j^2 + x_j^2 each
+            // score is within E (|x|^2 + 3|c|^2), E = 3.02 * 2^-16 + 1.03 gamma.
+            // A packed key moves its score by less than 2^(bits - 23) of the
+            // score's magnitude, itself below (1 + E)(|x|^2 + 3|c|^2). So the
+            // label stands when the two best keys differ by more than twice
+            // E + 1.01 * 2^(bits - 23) (with margins).
+            const float key_rel = __uint_as_float((uint32_t)(127 - 23 + kbits) << 23);   // 2^(bits-23)
+            const float e1 = 3.02f * 1.5258789e-05f + 1.03f * (float)(96 * KC + 2) * 5.9604645e-8f +
+                             1.01f * key_rel;
+            const float thr1 = 2.02f * e1 * (3.02f * cmax + 1.0001f * mx) + 1e-30f;
             bool ok = (K == 1) || (mb2 - mb1 > thr1);
 
             // ---- pass 2 (tiles with a call too close for pass 1): the fp32
