@@ -127,9 +127,13 @@ lloyd_lane_kernel(const float *__restrict__ X, int64_t n, const float *__restric
 
     // Full tiles (all 64 objects present) are streamed in the main loop; the
     // last, partial tile (if n is not a multiple of 64) is handled after it.
+    // Wave w of workgroup b takes tiles w*G + b, then every G*W-th: the
+    // waves with one tile more than the others are then waves 0, 1, ... of
+    // every workgroup, which sit on different SIMDs, rather than every wave
+    // of the first workgroups.
     const int64_t nfull = n / kWave;
     const int64_t stride = (int64_t)gridDim.x * W;
-    const int64_t q0 = (int64_t)blockIdx.x * W + wave;
+    const int64_t q0 = (int64_t)wave * gridDim.x + blockIdx.x;
 
     // tiles in flight per wave: two ahead, or one where the matrix-core
     // operands take the registers
