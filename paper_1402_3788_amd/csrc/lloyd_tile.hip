@@ -280,21 +280,23 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
     uint32_t *turn = reinterpret_cast<uint32_t *>(smem + L.misc + 4);
     double *wslabs = reinterpret_cast<double *>(smem + L.slab) + (size_t)wave * kP * K * (M + 1);
 
-    // A block tile is the W wave tiles bt*W .. bt*W+W-1 of one workgroup step.
-    // Block tiles whose wave tiles are all full (64 objects present) are
-    // streamed in the main loop; the one block tile after them (partial tiles
-    // or tiles past the end) is handled after it.
+    // The grid works in rounds of G*W wave tiles; in round r, wave w of
+    // workgroup b takes tile r*G*W + w*G + b. Rounds whose tiles are all full
+    // (64 objects present) are streamed in the main loop; the one round after
+    // them (the remaining tiles, fewer than G*W, the ragged one included) is
+    // handled after it, its tiles going to waves 0, 1, ... of every
+    // workgroup. Every workgroup runs the same rounds.
     const int64_t nq = (n + kWave - 1) / kWave;
     const int64_t nfull = n / kWave;
-    const int64_t nbt_main = nfull / W;
-    const int64_t nbt = (nq + W - 1) / W;
     const int64_t G = gridDim.x;
+    const int64_t R = G * W;                   // tiles per round
+    const int64_t nr_main = nfull / R;
+    const int64_t qw = (int64_t)wave * G + blockIdx.x;   // this wave's tile in round 0
 
     // the first two tiles' loads go out before the prologue
     float4 buf[2][V];   // register buffers, selected by compile-time index
-    const int64_t bt0 = blockIdx.x;
-    if (bt0 < nbt_main) load_tile<M>(X, bt0 * W + wave, lane, buf[0]);
-    if (bt0 + G < nbt_main) load_tile<M>(X, (bt0 + G) * W + wave, lane, buf[1]);
+    if (nr_main > 0) load_tile<M>(X, qw, lane, buf[0]);
+    if (nr_main > 1) load_tile<M>(X, R + qw, lane, buf[1]);
 
     // ---- prologue: split A operands (-2C, bf16 hi and lo, in lane order),
     // centre norms, slabs
@@ -368,17 +370,17 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
 
     // One wave tile: stage it in LDS, put the loads of the tile two strides
     // ahead in flight in the same registers, assign, accumulate.
-    // full: a block tile of the main loop (every wave tile present and full;
-    // the loads two strides ahead are issued here) rather than the last one
-    auto step = [&](int64_t b, auto bi, auto full) {
+    // full: a round of the main loop (every wave tile present and full; the
+    // loads two rounds ahead are issued here) rather than the last one
+    auto step = [&](int64_t r, auto bi, auto full) {
         constexpr bool kFullTile = decltype(full)::value;
         constexpr bool prefetch = kFullTile;
         float4 (&bb)[V] = buf[decltype(bi)::value];
-        const int64_t q = b * W + wave;
+        const int64_t q = r * R + qw;
         const bool have = kFullTile || q < nq;
         if (have) store_tile<M>(tile, lane, bb);
         __builtin_amdgcn_wave_barrier();
-        if (prefetch && b + 2 * G < nbt_main) load_tile<M>(X, (b + 2 * G) * W + wave, lane, bb);
+        if (prefetch && r + 2 < nr_main) load_tile<M>(X, q + 2 * R, lane, bb);
         const int64_t i = q * kWave + lane;
         const bool valid = kFullTile || (have && i < n);
         int my_lab = -1;
@@ -719,18 +721,18 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
         }
     };
 
-    // Block tiles are taken in strides of the grid; the register buffers
-    // alternate. Every wave of a workgroup runs the same steps (the ring form
-    // needs every wave's turn in every step).
-    for (int64_t bt = bt0; bt < nbt_main; bt += 2 * G) {
-        step(bt, std::integral_constant<int, 0>{}, std::true_type{});
-        if (bt + G < nbt_main) step(bt + G, std::integral_constant<int, 1>{}, std::true_type{});
+    // The register buffers alternate between rounds. Every wave of a
+    // workgroup runs the same steps (the ring form needs every wave's turn in
+    // every step).
+    for (int64_t r = 0; r < nr_main; r += 2) {
+        step(r, std::integral_constant<int, 0>{}, std::true_type{});
+        if (r + 1 < nr_main) step(r + 1, std::integral_constant<int, 1>{}, std::true_type{});
     }
-    if (nbt_main < nbt && nbt_main >= bt0 && (nbt_main - bt0) % G == 0) {
-        const int64_t q = nbt_main * W + wave;
+    if (nr_main * R < nq) {
+        const int64_t q = nr_main * R + qw;
         if (q < nfull) load_tile<M>(X, q, lane, buf[0]);
         else if (q < nq) load_tail_tile<M>(X, n, q, lane, buf[0]);
-        step(nbt_main, std::integral_constant<int, 0>{}, std::false_type{});
+        step(nr_main, std::integral_constant<int, 0>{}, std::false_type{});
     }
 
     if (ctl != nullptr && lane == 0 && nfallback > 0) atomicAdd(&ctl->fallbacks, nfallback);
