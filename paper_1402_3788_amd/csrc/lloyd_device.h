@@ -1,6 +1,7 @@
-// Device helpers shared by the distance kernels: streaming a 64-object tile of
-// X through registers into LDS, the per-wave fp64 accumulation of Eq. (1)'s
-// sums, and the fp64 re-decision of close calls.
+// Device helpers shared by the distance kernels: bf16 operand splitting,
+// streaming a 64-object tile of X through registers into LDS, the per-wave
+// fp64 accumulation of Eq. (1)'s sums, and the fp64 re-decision of close
+// calls.
 #pragma once
 
 #include "lloyd.h"
@@ -8,6 +9,47 @@
 #include <math.h>
 
 namespace lloyd {
+
+// ---------------------------------------------------------------------------
+// Split-precision operands of the bf16 matrix products (both distance kernels).
+
+typedef __bf16 bf2v __attribute__((ext_vector_type(2)));
+typedef float f2v __attribute__((ext_vector_type(2)));
+
+// Two fp32 values rounded to nearest-even bf16 (v_cvt_pk_bf16_f32), packed
+// with the first in the low half.
+__device__ inline uint32_t bf16x2_rne(float a, float b)
+{
+    const f2v v = {a, b};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf2v));
+}
+
+// Split eight fp32 values v into bf16 parts rounded to nearest: hi = bf16(v),
+// lo = bf16(v - hi), the remainder being exact (hi is within a factor 2 of v).
+// With the bf16 unit roundoff 2^-8, |v - hi| <= 2^-8 |v| and
+// |v - hi - lo| <= 2^-16 |v| (v finite and below the bf16 overflow
+// threshold). Parts are packed two per dword, element 2e in the low half of
+// dword e, as the bf16 operands of v_mfma_f32_16x16x32_bf16 expect.
+__device__ inline void split_bf16x8(const float (&v)[8], uint32_t (&hi)[4], uint32_t (&lo)[4])
+{
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const uint32_t h = bf16x2_rne(v[2 * e], v[2 * e + 1]);
+        hi[e] = h;
+        lo[e] = bf16x2_rne(v[2 * e] - __uint_as_float(h << 16),
+                           v[2 * e + 1] - __uint_as_float(h & 0xFFFF0000u));
+    }
+}
+
+typedef __bf16 bf8v __attribute__((ext_vector_type(8)));
+
+// Four packed dwords as the eight bf16 of a matrix operand.
+__device__ inline bf8v as_bf8(const uint32_t (&u)[4])
+{
+    typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+    const u4v w = {u[0], u[1], u[2], u[3]};
+    return __builtin_bit_cast(bf8v, w);
+}
 
 template <int M>
 struct TileGeom {

@@ -14,18 +14,19 @@
 //          distances are called in fp32 only when their gap exceeds
 //          4 gamma_{M+2} of the second;
 //        DIST = kDistMfma: the expanded form score = |c|^2 - 2 x.c on the
-//          matrix cores with v_mfma_f32_16x16x4f32: A = -2C for 16 centres
-//          by 4 feature columns (plus the |c|^2 column, which meets B = 1),
-//          held in registers for the whole launch (K <= 16); B = 4 features
-//          of 16 objects, read from the tile. The four 16-object blocks of a
-//          tile are four independent chains of ceil((M+1)/4) products. Each
-//          lane ends with 4 scores of one object; they go back into the slot
+//          bf16 matrix cores (v_mfma_f32_16x16x32_bf16) in split precision:
+//          A = -2C for 16 centres by 32 features and B = 32 features of 16
+//          objects (read from the tile), each split into bf16 hi and lo
+//          parts rounded to nearest, three products per 16-object block
+//          (lo(A) hi(B) + hi(A) lo(B) + hi(A) hi(B)) on top of |c|^2; A and
+//          |c|^2 stay in registers for the whole launch (K <= 16). Each lane
+//          ends with 4 scores of one object; they go back into the slot
 //          (which is no longer needed) as one row of 16 scores per object, so
 //          that each lane again scans the K scores of its own object with no
-//          cross-lane merge. The expanded form's fp32 error is bounded by
-//          gamma_{M+2} (3|c|^2 + |x|^2) whatever the summation order, so a
-//          label is accepted only if the two best scores differ by more than
-//          2.5 times that bound;
+//          cross-lane merge. A score is within E (3|c|^2 + |x|^2) of the
+//          exact one, E = 3.02 * 2^-16 + 1.03 gamma_98, so a label is
+//          accepted only if the two best scores differ by more than 2.02 E
+//          (3 max|c|^2 + |x|^2);
 //      either way, a lane whose call is too close recomputes all K distances
 //      in fp64 in the oracle's operation order and takes the lowest-index
 //      minimum, so the label is the exact-arithmetic argmin;
@@ -167,18 +168,31 @@ lloyd_lane_kernel(const float *__restrict__ X, int64_t n, const float *__restric
         __syncthreads();
         for (int k = 0; k < K; ++k) cmax = fmaxf(cmax, atab[k * FP + M]);
     }
-    // A operands of the 16x16x4 products for the whole launch: k-step s covers
-    // table columns 4s .. 4s+3; lane l holds row l % 16 (centre), column
-    // 4s + l / 16.
-    constexpr int kKS = FP / 4;
-    float aop[kKS];
+    // A operands of the bf16 products for the whole launch: lane l holds
+    // features 8(l/16) .. 8(l/16)+7 of centre l % 16 (-2c, zero past M),
+    // split into bf16 hi and lo, and the |c|^2 seeds of centres
+    // 4(l/16) .. 4(l/16)+3 (the rows of the result it holds).
+    uint32_t ah[4], al[4];
+    f4v cseed;
+    {
+        float a[8];
 #pragma unroll
-    for (int ks = 0; ks < kKS; ++ks)
-        aop[ks] = (kMfma && MODE != kAccumLabels) ? atab[(lane % 16) * FP + 4 * ks + lane / 16] : 0.f;
+        for (int e = 0; e < 8; ++e) {
+            const int f = 8 * (lane / 16) + e;
+            a[e] = (kMfma && MODE != kAccumLabels && f < M) ? atab[(lane % 16) * FP + f] : 0.f;
+        }
+        split_bf16x8(a, ah, al);
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            cseed[r] = (kMfma && MODE != kAccumLabels) ? atab[(4 * (lane / 16) + r) * FP + M] : 0.f;
+    }
 
-    // fp32 call thresholds (see the header comment)
+    // call thresholds (see the header comment): the direct form in fp32; the
+    // split-precision scores, within E (|x|^2 + 3|c|^2) of the exact ones with
+    // E = 3.02 * 2^-16 + 1.03 gamma_98 (the bf16 split of both operands, the
+    // fp32 sums of 96 exact products and |c|^2, and |c|^2 itself in fp32)
     constexpr float kTau = 4.0f * (float)(M + 2) * 5.9604645e-8f;
-    constexpr float kGuard = 2.5f * 1.01f * (float)(M + 2) * 5.9604645e-8f;
+    constexpr float kE1 = 3.02f * 1.5258789e-05f + 1.03f * 98.0f * 5.9604645e-8f;
     int nfallback = 0;
 
     // A tile's labels (and distances) are stored at the start of the next step,
@@ -224,41 +238,48 @@ lloyd_lane_kernel(const float *__restrict__ X, int64_t n, const float *__restric
             lab = 0;
             bool ok;
             if constexpr (kMfma) {
-                // v_mfma_f32_16x16x4f32 on four blocks of 16 objects: A = the
-                // operand table (16 centres x 4 columns, in aop), B = 4
-                // features x 16 objects read from the tile, the |c|^2 column
-                // meeting B = 1. Lane l ends with the scores of centres
+                // Split-precision products on the bf16 matrix cores
+                // (v_mfma_f32_16x16x32_bf16) for four blocks of 16 objects:
+                // A = -2C (16 centres x 32 features, in ah / al), B = features
+                // 8(l/16) .. 8(l/16)+7 of object 16b + l%16 read from the tile
+                // (zero past M; the reads stay inside the wave's slot) and split
+                // likewise; per block lo(A) hi(B) + hi(A) lo(B) + hi(A) hi(B)
+                // on top of |c|^2. Lane l ends with the scores of centres
                 // 4(l/16) .. 4(l/16)+3 for object 16b + l%16 of block b; it
                 // also sums the squares of the features it read (a quarter
                 // of |x|^2). The four blocks are four independent chains.
                 const int g = lane / 16, o16 = lane % 16;
                 f4v d[4];
                 float xp[4];
-                float bv[4][kKS];
+                uint32_t bh[4][4], bl[4][4];
 #pragma unroll
                 for (int b = 0; b < 4; ++b) {
-                    d[b] = f4v{0.f, 0.f, 0.f, 0.f};
-                    xp[b] = 0.f;
+                    const float *row = tile + (16 * b + o16) * M + 8 * g;
+                    float v[8];
+                    float acc = 0.f;
 #pragma unroll
-                    for (int ks = 0; ks < kKS; ++ks) {
-                        const float v = tile[(16 * b + o16) * M + 4 * ks + g];
-                        if (4 * ks + 3 < M) {
-                            bv[b][ks] = v;
-                            xp[b] = __builtin_fmaf(v, v, xp[b]);
-                        } else {
-                            const int f = 4 * ks + g;
-                            const float xv = f < M ? v : 0.f;
-                            bv[b][ks] = f < M ? v : (f == M ? 1.0f : 0.f);
-                            xp[b] = __builtin_fmaf(xv, xv, xp[b]);
-                        }
+                    for (int e = 0; e < 8; ++e) {
+                        // every read is made (in range for every lane group
+                        // where 24 + e < M), and the bits past M are masked
+                        const bool always = 24 + e < M;
+                        const uint32_t keep = (always || 8 * g + e < M) ? ~0u : 0u;
+                        v[e] = __uint_as_float(__float_as_uint(row[e]) & keep);
+                        acc = __builtin_fmaf(v[e], v[e], acc);
                     }
+                    xp[b] = acc;
+                    split_bf16x8(v, bh[b], bl[b]);
                 }
 #pragma unroll
-                for (int ks = 0; ks < kKS; ++ks) {
+                for (int b = 0; b < 4; ++b) d[b] = cseed;
 #pragma unroll
-                    for (int b = 0; b < 4; ++b)
-                        d[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(aop[ks], bv[b][ks], d[b], 0, 0, 0);
-                }
+                for (int b = 0; b < 4; ++b)
+                    d[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf8(al), as_bf8(bh[b]), d[b], 0, 0, 0);
+#pragma unroll
+                for (int b = 0; b < 4; ++b)
+                    d[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf8(ah), as_bf8(bl[b]), d[b], 0, 0, 0);
+#pragma unroll
+                for (int b = 0; b < 4; ++b)
+                    d[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf8(ah), as_bf8(bh[b]), d[b], 0, 0, 0);
                 // every read of the tile (features above, accumulation values
                 // before) precedes these writes in program order, and a wave's
                 // LDS operations complete in order: the score rows may reuse
@@ -287,7 +308,7 @@ lloyd_lane_kernel(const float *__restrict__ X, int64_t n, const float *__restric
                         lab = lt ? 4 * qq + r : lab;
                     }
                 }
-                const float thr = kGuard * (3.02f * cmax + 1.0001f * xsq) + 1e-30f;
+                const float thr = 2.02f * kE1 * (3.02f * cmax + 1.0001f * xsq) + 1e-30f;
                 ok = (K == 1) || (b2 - b1 > thr);
             } else {
                 float x[M];
