@@ -197,6 +197,32 @@ def test_split_precision_rerun_parity(K, M):
     assert reruns > 0
 
 
+@pytest.mark.parametrize("K,M", [(16, 25), (9, 27), (12, 7)])
+def test_lane_split_band_parity(K, M):
+    # The one-object-per-lane kernel (K <= 16) scores with split-precision
+    # bf16 products and sends every call inside its guard band straight to
+    # the fp64 re-decision: half of the objects lie within 1e-4 (relative) of
+    # a bisector, so many of them must take that path, and labels, counts and
+    # centres must still equal the oracle's.
+    _say(f"[lane band] K={K} M={M}")
+    rng = np.random.default_rng(100 + K + M)
+    n = 20_000
+    C = rng.uniform(-50, 50, (K, M)).astype(np.float32)
+    a, b = rng.integers(0, K, n), rng.integers(0, K, n)
+    t = rng.uniform(0.4999, 0.5001, (n, 1))
+    X = (C[a] * t + C[b] * (1 - t)).astype(np.float32)
+    X[n // 2:] = rng.uniform(-50, 50, (n - n // 2, M)).astype(np.float32)
+    ws = km.workspace(n, M, K, DEV, km.KMEANS_PATH_MFMA)
+    lab, Cn, cnt, it = km.kmeans_run(_gpu(X), K, _gpu(C), 2, fixed_iters=True, path="mfma", ws=ws)
+    olab, oC, ocnt, oit = oracle.run(X, K, C, 2, fixed=True)
+    assert np.array_equal(lab.cpu().numpy(), olab)
+    assert np.array_equal(cnt.cpu().numpy(), ocnt)
+    check_centers(Cn.cpu().numpy(), oC)
+    fb = km.ctl_fallbacks(ws)
+    _say(f"[lane band] K={K}: {fb} objects re-decided in fp64")
+    assert fb > 0
+
+
 @pytest.mark.parametrize("n,M,K", [(1, 2, 1), (1000, 3, 7), (65_537, 25, 16), (33_333, 64, 100),
                                    (10_000, 10, 1024)])
 def test_update_parity(n, M, K):
