@@ -38,7 +38,7 @@ METRIC = "Lloyd iters/sec and points·iters/sec at n=2e6,M=25,K=16; % of HBM pea
 # kernel that does the work of a step on each distance path, and the sources
 # it is built from (a committed counter summary is used only while they match)
 KERNELS = {
-    "lane-mfma": ("lloyd_lane_kernel<M, assign+accumulate, dist=mfma 16x16x4>",
+    "lane-mfma": ("lloyd_lane_kernel<M, assign+accumulate, dist=mfma, split bf16 products>",
                   ["lloyd_lane.hip", "lloyd_device.h", "lloyd.h"]),
     "direct": ("lloyd_lane_kernel<M, assign+accumulate, dist=valu>",
                ["lloyd_lane.hip", "lloyd_device.h", "lloyd.h"]),
@@ -225,12 +225,16 @@ def main():
         Xc = torch.from_numpy(rng.uniform(-50, 50, (nc, M)).astype(np.float32)).to(dev)
         Cc = Xc[:K].clone()
         km.kmeans_run(Xc, K, Cc, 5, fixed_iters=True, path=path)
+        wsc = km.workspace(nc, M, K, dev, flags)
         _, _, _, _, tmc = km.kmeans_run(Xc, K, Cc, 50, fixed_iters=True, path=path,
-                                        timing=True, sample_every=1)
+                                        timing=True, sample_every=1, ws=wsc)
         avg = tmc.assign_ms / 1e3 / tmc.assign_samples
         result["control_n8m_uniform"] = {
             "kernel_avg_us": round(avg * 1e6, 2),
             "achieved_GBps": round(nc * bytes_per_point / avg / 1e9, 1),
+            # uniform objects sit near bisectors far more often than clustered
+            # ones: the fp64 re-decisions are part of this launch's time
+            "fallbacks_per_iteration": round(km.ctl_fallbacks(wsc) / 50, 1),
         }
         del Xc
         result["copy_GBps_torch_1GiB"] = round(copy_bandwidth(torch), 1)
