@@ -71,7 +71,6 @@ __host__ __device__ inline int key_bits(int KT)
 constexpr int kAccWave = 1;    // per-wave slabs, WaveAcc<M>::Pmax objects per step
 constexpr int kAccRing = 2;    // one slab per workgroup, waves add in turn
 constexpr int kAccWave1 = 3;   // one slab per wave, WaveAcc<M>::Pmax objects per step (less LDS)
-constexpr int kAccLane = 4;    // one slab per wave, one lane per object
 constexpr int kMaxWaves = 8;
 [[maybe_unused]] constexpr int kMinWaveForm = 4;   // fewest waves the wave form is used with
 
@@ -117,8 +116,6 @@ __host__ __device__ inline MfmaLds mfma_lds(int M, int K, int W, int acc)
         L.slab = o;    o = al16(o + (size_t)W * wave_acc_p(M, acc) * K * (M + 1) * 8);
     } else if (acc == kAccRing) {
         L.slab = o;    o = al16(o + (size_t)K * ring_row(M) * 8);
-    } else if (acc == kAccLane) {
-        L.slab = o;    o = al16(o + (size_t)W * K * ring_row(M) * 8);
     }
     L.total = o;
     return L;
@@ -290,10 +287,9 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
     if (kWaveForm) {
         double *slabs = reinterpret_cast<double *>(smem + L.slab);
         for (int i = tid; i < W * kP * K * (M + 1); i += blockDim.x) slabs[i] = 0.0;
-    } else if (kAcc == kAccRing || kAcc == kAccLane) {
+    } else if (kAcc == kAccRing) {
         double *slab = reinterpret_cast<double *>(smem + L.slab);
-        const int rows = kAcc == kAccLane ? W * K : K;
-        for (int i = tid; i < rows * ring_row(M); i += blockDim.x) slab[i] = 0.0;
+        for (int i = tid; i < K * ring_row(M); i += blockDim.x) slab[i] = 0.0;
         if (tid == 0) *turn = 0u;
     }
     __syncthreads();
@@ -655,33 +651,29 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
             if (have)
                 accumulate_tile<M, PA, kFullTile && MODE != kAccumLabels, kShared>(
                     valid ? my_lab : -1, tile, offs, wslabs, K, lane);
-        } else if (kAcc == kAccRing || kAcc == kAccLane) {
-            // Lane l adds object l's features and count to its cluster's row:
-            // of the workgroup slab in this wave's turn of the step (ring;
-            // every wave takes its turn, with or without objects), or of the
-            // wave's own slab (lane form). The features are read from the
-            // wave's tile first (before the wait).
+        } else if (kAcc == kAccRing) {
+            // This wave's turn of the step (every wave takes it, with or
+            // without objects): lane l adds object l's features and count to
+            // its cluster's row of the workgroup slab. The features are read
+            // from the wave's own tile before the wait.
             const bool adds = valid && my_lab >= 0;
             float xv[M];
 #pragma unroll
             for (int j = 0; j < M; ++j) xv[j] = tile[lane * M + j];
             const uint32_t want =
                 __builtin_amdgcn_readfirstlane(ring_seq * (uint32_t)W + (uint32_t)wave);
-            if (kAcc == kAccRing && ring_ok) ring_ok = ring_wait(turn, want);
+            if (ring_ok) ring_ok = ring_wait(turn, want);
             if (adds) {
                 constexpr int RS = ring_row(M);
-                double *row = reinterpret_cast<double *>(smem + L.slab) +
-                              ((kAcc == kAccLane ? (int64_t)wave * K : 0) + my_lab) * RS;
+                double *row = reinterpret_cast<double *>(smem + L.slab) + (int64_t)my_lab * RS;
 #pragma unroll
                 for (int j = 0; j < M; ++j)
                     __hip_atomic_fetch_add(row + j, (double)xv[j], __ATOMIC_RELAXED,
                                            __HIP_MEMORY_SCOPE_WORKGROUP);
                 __hip_atomic_fetch_add(row + M, 1.0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
             }
-            if (kAcc == kAccRing) {
-                ring_pass(turn, want + 1);
-                ++ring_seq;
-            }
+            ring_pass(turn, want + 1);
+            ++ring_seq;
         }
     };
 
@@ -708,17 +700,14 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
         write_wave_partials<M, PA, kShared>(reinterpret_cast<const double *>(smem + L.slab), W, K,
                                part_sums + (int64_t)blockIdx.x * K * M,
                                part_counts + (int64_t)blockIdx.x * K);
-    } else if (kAcc == kAccRing || kAcc == kAccLane) {
-        // (lane form: the waves' slabs added in wave order)
+    } else if (kAcc == kAccRing) {
         __syncthreads();
         constexpr int RS = ring_row(M);
-        const int nslab = kAcc == kAccLane ? W : 1;
         const double *slab = reinterpret_cast<const double *>(smem + L.slab);
         double *out = part_sums + (int64_t)blockIdx.x * K * M;
         for (int e = tid; e < K * (M + 1); e += blockDim.x) {
             const int k = e / (M + 1), j = e % (M + 1);
-            double v = slab[k * RS + j];
-            for (int w = 1; w < nslab; ++w) v = v + slab[((int64_t)w * K + k) * RS + j];
+            const double v = slab[k * RS + j];
             if (j < M) out[(int64_t)k * M + j] = v;
             else part_counts[(int64_t)blockIdx.x * K + k] = (int32_t)v;
         }
@@ -744,13 +733,11 @@ hipError_t launch_m(const StepArgs &a, Mode mode, const AccumPlan &p, hipStream_
     case kAssignAccum:
         if (p.accum == kAccWave) LLOYD_MFMA_LAUNCH(kAssignAccum, kAccWave);
         else if (p.accum == kAccWave1) LLOYD_MFMA_LAUNCH(kAssignAccum, kAccWave1);
-        else if (p.accum == kAccLane) LLOYD_MFMA_LAUNCH(kAssignAccum, kAccLane);
         else LLOYD_MFMA_LAUNCH(kAssignAccum, kAccRing);
         break;
     case kAccumLabels:
         if (p.accum == kAccWave) LLOYD_MFMA_LAUNCH(kAccumLabels, kAccWave);
         else if (p.accum == kAccWave1) LLOYD_MFMA_LAUNCH(kAccumLabels, kAccWave1);
-        else if (p.accum == kAccLane) LLOYD_MFMA_LAUNCH(kAccumLabels, kAccLane);
         else LLOYD_MFMA_LAUNCH(kAccumLabels, kAccRing);
         break;
     }
