@@ -186,21 +186,41 @@ __device__ inline float sum_rows(float v)
     return __uint_as_float(s[0]) + __uint_as_float(s[1]);
 }
 
-// Merge the packed (best, second) keys of lanes l and l ^ 16 (ROW = 16) or
-// l and l ^ 32 (ROW = 32); keys of different centres never compare equal.
-template <int ROW>
-__device__ inline void merge_keys(float &k1, float &k2)
+// Packed (best, second) keys of object `lane` (column lane / 16 of the tile's
+// 16-object columns) from the per-column keys (k1[c], k2[c]) of the four lanes
+// l16 + 16 g' that hold its centre rows. Two exchange stages: with lane l ^ 32
+// (the lower half keeps columns 0, 1 and sends 2, 3; the upper half the
+// reverse), then with lane l ^ 16 (a lane keeps its own column and sends the
+// other); each received pair is merged into the kept one. Keys of different
+// centres never compare equal, so the order of a merge does not matter.
+__device__ inline void own_column_keys(const float (&k1)[4], const float (&k2)[4], int lane,
+                                       float &b1, float &b2)
 {
-    auto swap = [](uint32_t v) {
-        if (ROW == 16) return __builtin_amdgcn_permlane16_swap(v, v, false, false);
-        return __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    const bool up = lane >= 32;
+    const bool odd = (lane >> 4) & 1;
+    // the partner's value out of a swap's pair (see merge_rows)
+    auto other32 = [up](uint32_t v) {
+        const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+        return __uint_as_float(up ? r[0] : r[1]);
     };
-    const auto s1 = swap(__float_as_uint(k1));
-    const auto s2 = swap(__float_as_uint(k2));
-    const float f1 = __uint_as_float(s1[0]), g1 = __uint_as_float(s1[1]);
-    const float f2 = __uint_as_float(s2[0]), g2 = __uint_as_float(s2[1]);
-    k2 = second_of(f1, f2, g1, g2);
-    k1 = fminf(f1, g1);
+    auto other16 = [odd](uint32_t v) {
+        const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+        return __uint_as_float(odd ? r[0] : r[1]);
+    };
+    float m1[2], m2[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const float o1 = up ? k1[2 + i] : k1[i], o2 = up ? k2[2 + i] : k2[i];   // kept
+        const float s1 = up ? k1[i] : k1[2 + i], s2 = up ? k2[i] : k2[2 + i];   // sent
+        const float p1 = other32(__float_as_uint(s1)), p2 = other32(__float_as_uint(s2));
+        m2[i] = second_of(o1, o2, p1, p2);
+        m1[i] = fminf(o1, p1);
+    }
+    const float o1 = odd ? m1[1] : m1[0], o2 = odd ? m2[1] : m2[0];
+    const float s1 = odd ? m1[0] : m1[1], s2 = odd ? m2[0] : m2[1];
+    const float p1 = other16(__float_as_uint(s1)), p2 = other16(__float_as_uint(s2));
+    b2 = second_of(o1, o2, p1, p2);
+    b1 = fminf(o1, p1);
 }
 
 
@@ -496,19 +516,14 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
                 // replaced by the centre's index within its group of 2^bits
                 // centres, so that min / med3 / min keep the best and second
                 // best keys and the label comes with the best one. Per group
-                // the four lanes of an object merge their keys, and the group
-                // folds into a running (best, second, label) per column.
+                // each lane gathers the keys of its own object from the four
+                // lanes that hold its centre rows, and the group folds into
+                // the lane's running (best, second, label).
                 const int gblocks = (1 << kbits) / 16;            // even
                 const uint32_t kmask = ~((1u << kbits) - 1u);
-                float g1[kCols], g2[kCols];
-                int gl[kCols];
+                float g1 = INFINITY, g2 = INFINITY;
+                int gl = 0;
                 float k1[kCols], k2[kCols];
-#pragma unroll
-                for (int c = 0; c < kCols; ++c) {
-                    g1[c] = INFINITY;
-                    g2[c] = INFINITY;
-                    gl[c] = 0;
-                }
                 int kt0 = 0;
                 auto scan_key = [&](int tt, const f4v (&d)[kCols]) {
                     const uint32_t i0 = (uint32_t)((tt - kt0) * 16 + 4 * g);
@@ -534,29 +549,20 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
                         k2[c] = INFINITY;
                     }
                     blocks(kt0, kt1, oA, oB, load_h, chain_h, scan_key);
-#pragma unroll
-                    for (int c = 0; c < kCols; ++c) {
-                        merge_keys<16>(k1[c], k2[c]);
-                        merge_keys<32>(k1[c], k2[c]);
-                        const int lab = kt0 * 16 + (int)(__float_as_uint(k1[c]) & ~kmask);
-                        const bool take = k1[c] < g1[c];
-                        g2[c] = second_of(g1[c], g2[c], k1[c], k2[c]);
-                        g1[c] = take ? k1[c] : g1[c];
-                        gl[c] = take ? lab : gl[c];
-                    }
+                    float b1, b2;
+                    own_column_keys(k1, k2, lane, b1, b2);
+                    const int lab = kt0 * 16 + (int)(__float_as_uint(b1) & ~kmask);
+                    const bool take = b1 < g1;
+                    g2 = second_of(g1, g2, b1, b2);
+                    g1 = take ? b1 : g1;
+                    gl = take ? lab : gl;
                 }
-                mb1 = g1[0];
-                mb2 = g2[0];
+                mb1 = g1;
+                mb2 = g2;
+                ml = gl;
                 mx = xsq[0];
-                ml = gl[0];
 #pragma unroll
-                for (int c = 1; c < kCols; ++c) {
-                    const bool mine = g == c;
-                    mb1 = mine ? g1[c] : mb1;
-                    mb2 = mine ? g2[c] : mb2;
-                    mx = mine ? xsq[c] : mx;
-                    ml = mine ? gl[c] : ml;
-                }
+                for (int c = 1; c < kCols; ++c) mx = g == c ? xsq[c] : mx;
             }
             // Error of a pass-1 score against the exact score |c|^2 - 2 x.c:
             // with a = ah + al + ea, b = bh + bl + eb (|ea| <= 2^-16 |a|, |al|
