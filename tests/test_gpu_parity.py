@@ -170,13 +170,14 @@ def test_assign_near_ties_are_exact():
             assert np.array_equal(lab, oracle.assign(X, CC)), path
 
 
-@pytest.mark.parametrize("K,M", [(64, 25), (256, 25), (40, 40)])
+@pytest.mark.parametrize("K,M", [(64, 25), (256, 25), (40, 40), (300, 25)])
 def test_split_precision_rerun_parity(K, M):
     # Half of the objects lie within 1e-4 (relative) of the bisector of two
     # centres: the tile kernel's split-precision pass cannot call them, so
     # their tiles are recomputed with fp32 products and the closest calls
     # re-decided in fp64. Labels, counts and centres must still equal the
     # oracle's, and the control block must show that tiles were recomputed.
+    # (K = 300: two groups of centres, 256 and 44, whose packed keys are folded.)
     _say(f"[rerun] K={K} M={M}")
     rng = np.random.default_rng(K + M)
     n = 20_000
