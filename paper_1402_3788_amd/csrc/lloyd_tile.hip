@@ -4,29 +4,36 @@
 // Expanded form of the squared distance of Eq. (2): for object x and centre c,
 //     |x - c|^2 = |x|^2 + score,   score = |c|^2 - 2 x.c,
 // and |x|^2 is the same for every centre, so the nearest centre is the one with
-// the smallest score. For 16 centres and 16 objects the scores are one
-// v_mfma_f32_16x16x4f32 chain over the features (4 per step, zero-padded):
-//     D[centre][object] = |c|^2 + sum_j (-2 c_j) x_j,
-// with A = -2C (16 x 4 per step, built once per workgroup in LDS, already in
-// the lane order the instruction wants), B = X^T (4 x 16 per step, read from
-// the LDS tile) and the accumulator seeded with |c|^2.
+// the smallest score. For 16 centres and 16 objects the scores are one matrix
+// product D[centre][object] = |c|^2 + sum_j (-2 c_j) x_j with A = -2C (built
+// once per workgroup in LDS, in the lane order the instruction wants), B = X^T
+// (read from the LDS tile) and the accumulator seeded with |c|^2, in up to
+// three stages:
+//   pass 1 (every tile): split precision on the bf16 matrix cores, three
+//     v_mfma_f32_16x16x32_bf16 per block on operands split into bf16 hi and
+//     lo parts rounded to nearest; each score is within E (3|c|^2 + |x|^2) of
+//     the exact one (E = 3.02 * 2^-16 + 1.03 gamma_{96 ceil(M/32) + 2}); the
+//     scores are scanned as packed (score, index) keys, and a label is
+//     accepted when the two best keys differ by more than twice that bound
+//     plus the keys' truncation (with |c|^2 bounded by the largest centre
+//     norm and margins);
+//   pass 2 (tiles with a call too close for pass 1): fp32 products, a
+//     v_mfma_f32_16x16x4f32 chain over the features, whose error is bounded by
+//     gamma_{M+2} (3|c|^2 + |x|^2); a label is accepted at 2.5 times that;
+//   the objects still too close are re-decided with fp64 distances in the
+//   fixed operation order, over all centres, lowest index on ties.
 //
-// Layout of v_mfma_f32_16x16x4f32 (64 lanes): A[i][k] is in lane i + 16k,
-// B[k][j] in lane j + 16k, and D[i][j] in lane j + 16(i/4), register i%4. So
-// after a chain every lane holds the scores of 4 centres for one object; a lane
-// keeps a running best / second-best over its centres, and two row swaps
-// (v_permlane16_swap, v_permlane32_swap) merge the four lanes that share an
-// object.
+// Layout of the 16x16 products (64 lanes): D[i][j] is in lane j + 16(i/4),
+// register i%4; A[i][k] in lane i + 16k (16x16x4) or lane i + 16(k/8), element
+// k%8 (16x16x32), and B[k][j] likewise with j. So every lane holds the scores
+// of 4 centres for the four objects it sees in the tile's four 16-object
+// columns, and the four lanes that hold an object's centre rows exchange their
+// results with row swaps (v_permlane16_swap, v_permlane32_swap).
 //
-// The expanded form cancels: its fp32 error is bounded by
-// gamma_{M+2} (3|c|^2 + |x|^2), so a label is accepted only if the two best
-// scores differ by more than 2.5 times that bound (with |c|^2 bounded by the
-// largest centre norm). Other objects are re-decided with fp64 distances in the
-// fixed operation order, over all centres, lowest index on ties.
-//
-// Each wavefront streams 64-object tiles: the next two tiles' loads are in
-// flight in registers while the current tile is staged in the wave's LDS slot;
-// the ragged last tile (n not a multiple of 64) is handled after the loop.
+// Each wavefront streams 64-object tiles (in wave-major rounds of the grid):
+// the next two tiles' loads are in flight in registers while the current tile
+// is staged in the wave's LDS slot; the round with the ragged last tile (n not
+// a multiple of 64) is handled after the loop.
 //
 // Accumulation (the sums of Eq. (1)) has two forms, both with every addition in
 // an order fixed by the problem shape (and the hardware's lane order):
