@@ -2,7 +2,8 @@
 
 TEST INFRASTRUCTURE ONLY: the oracle is the slow, obviously correct statement
 of Algorithm 1's Lloyd iteration (assign by Eq. (2), centres of gravity by
-Eq. (1), stop on congruent centres) that the GPU library is checked against.
+Eq. (1), stop on congruent centres) and of its step 1 (farthest-point initial
+centres) that the GPU library is checked against.
 Only the tests, the smoke check and the benchmark's CPU-baseline leg use it;
 the GPU library never imports, links or calls it.
 """
@@ -41,6 +42,8 @@ def _bind(path: str):
     lib.oracle_run.restype = ctypes.c_int
     lib.oracle_sse.argtypes = [p, i64, i32, p, p, i32]
     lib.oracle_sse.restype = ctypes.c_double
+    lib.oracle_init_farthest.argtypes = [p, i64, i32, i32, p]
+    lib.oracle_init_farthest.restype = ctypes.c_int
     return lib
 
 
@@ -140,6 +143,20 @@ def sse(X, labels, C) -> float:
     labels = np.ascontiguousarray(labels, dtype=np.int32)
     return float(_load().oracle_sse(_ptr(X), X.shape[0], X.shape[1], _ptr(labels),
                                     _ptr(C), C.shape[0]))
+
+
+def init_farthest(X, K: int):
+    """Algorithm 1 step 1, read as farthest-point traversal from object 0:
+    idx[0] = 0, idx[m] = the not-yet-chosen object whose smallest squared
+    distance to the chosen ones is largest (lowest index on ties).
+    Returns idx (int32 [K]); the initial centres are X[idx]. Needs K <= n."""
+    X = _f32(X)
+    n, M = X.shape
+    idx = np.empty(int(K), np.int32)
+    rc = _load().oracle_init_farthest(_ptr(X), n, M, int(K), _ptr(idx))
+    if rc:
+        raise ValueError(f"oracle_init_farthest failed ({rc})")
+    return idx
 
 
 def gap_rel(d1, d2):

@@ -199,3 +199,52 @@ double oracle_sse(const float *X, int64_t n, int32_t M, const int32_t *labels,
     }
     return s;
 }
+
+/*
+ * Initial centres, Algorithm 1 step 1 ("K objects far away from each other";
+ * the paper leaves the method open). Reading: farthest-point traversal from
+ * object 0 --
+ *   idx[0] = 0;
+ *   idx[m] = the object i not among idx[0..m-1] whose smallest squared
+ *            distance (Eq. (2), normative fp64 order above) to the objects
+ *            idx[0..m-1] is largest, the lowest such i on ties.
+ * The centres are the rows X[idx[m]]. Requires 1 <= K <= n.
+ */
+int oracle_init_farthest(const float *X, int64_t n, int32_t M, int32_t K, int32_t *idx)
+{
+    if (!X || !idx || n < 1 || M < 1 || K < 1 || (int64_t)K > n)
+        return ORACLE_EINVAL;
+    double *nearest = (double *)malloc((size_t)n * sizeof(double));
+    unsigned char *chosen = (unsigned char *)calloc((size_t)n, 1);
+    if (!nearest || !chosen) {
+        free(nearest);
+        free(chosen);
+        return ORACLE_ENOMEM;
+    }
+    for (int64_t i = 0; i < n; ++i)
+        nearest[i] = INFINITY;
+    idx[0] = 0;
+    chosen[0] = 1;
+    for (int32_t m = 1; m < K; ++m) {
+        /* fold the newest centre into every object's nearest distance */
+        const float *c = X + (int64_t)idx[m - 1] * M;
+        for (int64_t i = 0; i < n; ++i) {
+            double d = sqdist(X + i * (int64_t)M, c, M);
+            if (d < nearest[i])
+                nearest[i] = d;
+        }
+        /* the farthest object not yet chosen, lowest index on ties */
+        int64_t far = -1;
+        for (int64_t i = 0; i < n; ++i) {
+            if (chosen[i])
+                continue;
+            if (far < 0 || nearest[i] > nearest[far])
+                far = i;
+        }
+        idx[m] = (int32_t)far;
+        chosen[far] = 1;
+    }
+    free(nearest);
+    free(chosen);
+    return 0;
+}

@@ -1,5 +1,6 @@
 """Plant plausible mistakes in a copy of the oracle source and check that the
-oracle's pins (tests/test_oracle.py) catch every one of them.
+oracle's pins (tests/test_oracle.py for the Lloyd iteration,
+tests/test_oracle_init.py for the initial centres) catch every one of them.
 
 Each mutant is a textual edit of oracle/kmeans_oracle.c compiled into a
 temporary library; the pin suite then runs against it in a subprocess (through
@@ -39,6 +40,22 @@ MUTANTS = {
     "count_off_by_one": ("cnt[l] += 1;", "cnt[l] += (i > 0);"),
 }
 
+# mistakes in the initial-centre traversal, caught by tests/test_oracle_init.py
+INIT_MUTANTS = {
+    "init_ties_to_highest_index": ("nearest[i] > nearest[far]", "nearest[i] >= nearest[far]"),
+    "init_chosen_not_excluded": ("if (chosen[i])\n                continue;",
+                                 "if (0 && chosen[i])\n                continue;"),
+    "init_newest_centre_only": ("if (d < nearest[i])\n                nearest[i] = d;",
+                                "nearest[i] = d;"),
+    "init_nearest_as_max": ("if (d < nearest[i])\n                nearest[i] = d;",
+                            "if (nearest[i] == INFINITY || d > nearest[i])\n"
+                            "                nearest[i] = d;"),
+    "init_starts_at_last_object": ("idx[0] = 0;\n    chosen[0] = 1;",
+                                   "idx[0] = (int32_t)(n - 1);\n    chosen[n - 1] = 1;"),
+    "init_drops_last_feature": ("double d = sqdist(X + i * (int64_t)M, c, M);",
+                                "double d = sqdist(X + i * (int64_t)M, c, M > 1 ? M - 1 : M);"),
+}
+
 
 @pytest.fixture(scope="module")
 def source():
@@ -47,9 +64,10 @@ def source():
 
 
 @pytest.mark.slow
-@pytest.mark.parametrize("name", sorted(MUTANTS))
+@pytest.mark.parametrize("name", sorted(MUTANTS) + sorted(INIT_MUTANTS))
 def test_pins_catch_planted_mistake(name, source, tmp_path):
-    old, new = MUTANTS[name]
+    old, new = MUTANTS[name] if name in MUTANTS else INIT_MUTANTS[name]
+    pins = "test_oracle.py" if name in MUTANTS else "test_oracle_init.py"
     assert source.count(old) == 1, f"mutant {name} does not apply"
     src = tmp_path / "mutant.c"
     src.write_text(source.replace(old, new))
@@ -57,6 +75,6 @@ def test_pins_catch_planted_mistake(name, source, tmp_path):
     subprocess.check_call(["gcc", *oracle.CFLAGS, "-o", str(lib), str(src), "-lm"])
     env = dict(os.environ, KMEANS_ORACLE_LIB=str(lib))
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
-                        os.path.join(ROOT, "tests", "test_oracle.py")],
+                        "-m", "not slow", os.path.join(ROOT, "tests", pins)],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"mutant {name} survived the oracle pins:\n{r.stdout[-2000:]}"
