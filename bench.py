@@ -11,8 +11,12 @@ timed step does the full work (this workload converges after 2 passes; the
 passes after that repeat the same labels and centres). X is resident in device
 memory before the timed region starts.
 
+The JSON line also times the farthest-point initial centres of Algorithm 1
+step 1 (K passes over X) on the same workload ("init_farthest").
+
 python bench.py [--gpus 1] [--steps 1000] [--warmup 20] [--workload 3]
                 [--path auto|direct|mfma|tiles] [--no-cpu-baseline] [--no-control]
+                [--no-init]
 python bench.py --calibrate-copy   # plain device copy of known size (PMC scaling)
 
 Prints ONE JSON line.
@@ -56,6 +60,7 @@ def _parse():
     ap.add_argument("--path", default="auto", choices=["auto", "direct", "mfma", "tiles"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-control", action="store_true")
+    ap.add_argument("--no-init", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true")
     return ap.parse_args()
 
@@ -125,6 +130,40 @@ def copy_bandwidth(torch, nbytes=1 << 30, reps=20):
     return 2 * nbytes / sec / 1e9
 
 
+def init_bytes(n: int, M: int, K: int) -> int:
+    """Algorithmic bytes of the farthest-point traversal: pass p = 1 .. K-1
+    reads X, reads the fp64 nearest distances (p > 1) and writes them (when a
+    later pass reads them)."""
+    return sum(n * 4 * M + (8 * n if p > 1 else 0) + (8 * n if p + 1 < K else 0)
+               for p in range(1, K))
+
+
+def time_init(torch, km, Xg, K, stored, reps=5):
+    n, M = Xg.shape
+    ws = torch.empty(km.kmeans_init_workspace_bytes(n, M, K), dtype=torch.uint8,
+                     device=Xg.device)
+    idx, _ = km.kmeans_init_farthest(Xg, K, ws=ws)             # warm-up, and a check
+    torch.cuda.synchronize()
+    same = bool((idx.cpu().numpy() == stored).all())
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(reps):
+        km.kmeans_init_farthest(Xg, K, ws=ws)
+    e.record()
+    torch.cuda.synchronize()
+    sec = s.elapsed_time(e) / 1e3 / reps
+    nbytes = init_bytes(n, M, K)
+    return {
+        "ms": round(sec * 1e3, 3),
+        "launches": K,
+        "bytes": nbytes,
+        "achieved_GBps": round(nbytes / sec / 1e9, 1) if K > 1 else None,
+        "frac_hbm_peak": round(nbytes / sec / 1e9 / HBM_PEAK_GBPS, 4) if K > 1 else None,
+        "matches_stored_init": same,
+        "reps": reps,
+    }
+
+
 def main():
     args = _parse()
     if args.gpus != 1:
@@ -143,7 +182,7 @@ def main():
     import workloads
 
     w = workloads.get(args.workload)
-    X, _, _, init = workloads.load(args.workload)
+    X, _, init_idx, init = workloads.load(args.workload)
     dev = torch.device("cuda:0")
     Xg = torch.from_numpy(X).to(dev)
     Cg = torch.from_numpy(init).to(dev)
@@ -217,6 +256,9 @@ def main():
             "bytes_per_launch": launch_bytes,
         },
     }
+
+    if not args.no_init:
+        result["init_farthest"] = time_init(torch, km, Xg, K, init_idx)
 
     if not args.no_control:
         # same kernel on a point set larger than the 256 MB Infinity Cache

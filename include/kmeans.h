@@ -6,7 +6,8 @@
  * by K-means method": assign every object to the nearest centre (steps 2 and
  * 4, Euclidean distance of Eq. (2)), recompute each cluster's centre of gravity
  * (steps 3 and 5, Eq. (1)), and stop when the centres of the last two
- * iterations are congruent (steps 6 and 7).
+ * iterations are congruent (steps 6 and 7). It also picks the K initial
+ * centres of step 1 by farthest-point traversal.
  *
  * Conventions shared by every entry point
  *   - Array arguments are DEVICE pointers (hipMalloc'd or equivalent), owned by
@@ -94,6 +95,29 @@ size_t kmeans_workspace_bytes(int64_t n, int32_t M, int32_t K, uint32_t flags);
 
 /* Human-readable name of a status code (static storage). */
 const char *kmeans_strerror(int status);
+
+/* Bytes of device workspace that kmeans_init_farthest needs for this shape
+ * (one fp64 distance per object, n * 8 bytes plus a few KB). Returns 0 for
+ * shapes the library refuses, K > n included. Pure host computation. */
+size_t kmeans_init_workspace_bytes(int64_t n, int32_t M, int32_t K);
+
+/*
+ * Initial centres, Algorithm 1 step 1 ("K objects far away from each other";
+ * the paper leaves the method open), read as farthest-point traversal from
+ * object 0:
+ *   init_idx[0] = 0;
+ *   init_idx[m] = the object not among init_idx[0..m-1] whose smallest squared
+ *                 distance (Eq. (2)) to those objects is largest, the lowest
+ *                 such index on ties;
+ *   centers[m]  = X[init_idx[m]] (fp32 [K][M], copied bit for bit).
+ * The distances are formed in fp64 in the fixed order e = x_j - c_j,
+ * d = d + e*e (features ascending, each operation rounded), so the indices are
+ * exactly the ones that definition gives. Needs 1 <= K <= n (K > n:
+ * KMEANS_EINVAL). init_idx is an int32 [K] DEVICE array. Asynchronous on
+ * `stream`: K launches, each one pass over X (n * (4M + 16) bytes).
+ */
+int kmeans_init_farthest(const float *X, int64_t n, int32_t M, int32_t K, int32_t *init_idx,
+                         float *centers, void *workspace, size_t workspace_bytes, void *stream);
 
 /*
  * Assignment, Algorithm 1 steps 2 and 4, distance of Eq. (2):

@@ -10,7 +10,9 @@ Entry points (same names as the C ABI):
     kmeans_update(X, labels, K, prev_centers, out=None) -> (centers, counts)
     kmeans_run(X, K, init_centers, max_iter, fixed_iters=False, path=None,
                timing=False) -> (labels, centers, counts, iterations[, timing])
-    kmeans_workspace_bytes(n, M, K, flags=0), kmeans_strerror(code)
+    kmeans_init_farthest(X, K, ws=None) -> (init_idx, centers)
+    kmeans_workspace_bytes(n, M, K, flags=0), kmeans_init_workspace_bytes(n, M, K),
+    kmeans_strerror(code)
 """
 from __future__ import annotations
 
@@ -34,7 +36,7 @@ KMEANS_PATH_MFMA = 1 << 2
 KMEANS_PATH_TILES = 1 << 3
 
 EXPORTED = ("kmeans_workspace_bytes", "kmeans_strerror", "kmeans_assign", "kmeans_update",
-            "kmeans_run")
+            "kmeans_run", "kmeans_init_workspace_bytes", "kmeans_init_farthest")
 
 
 class KmeansTiming(ctypes.Structure):
@@ -66,6 +68,10 @@ def _load() -> ctypes.CDLL:
     lib.kmeans_run.argtypes = [p, i64, i32, i32, p, i32, u32, p, p, p, p, p, sz, p,
                                ctypes.POINTER(KmeansTiming)]
     lib.kmeans_run.restype = ctypes.c_int
+    lib.kmeans_init_workspace_bytes.argtypes = [i64, i32, i32]
+    lib.kmeans_init_workspace_bytes.restype = sz
+    lib.kmeans_init_farthest.argtypes = [p, i64, i32, i32, p, p, p, sz, p]
+    lib.kmeans_init_farthest.restype = ctypes.c_int
     return lib
 
 
@@ -81,6 +87,10 @@ kmeans_strerror = strerror
 
 def kmeans_workspace_bytes(n: int, M: int, K: int, flags: int = 0) -> int:
     return int(_lib.kmeans_workspace_bytes(int(n), int(M), int(K), int(flags)))
+
+
+def kmeans_init_workspace_bytes(n: int, M: int, K: int) -> int:
+    return int(_lib.kmeans_init_workspace_bytes(int(n), int(M), int(K)))
 
 
 def _stream_ptr(device) -> ctypes.c_void_p:
@@ -114,6 +124,30 @@ def workspace(n: int, M: int, K: int, device, flags: int = 0) -> torch.Tensor:
     if nbytes == 0:
         raise KmeansError("kmeans_workspace_bytes", KMEANS_EUNSUPPORTED)
     return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+def kmeans_init_farthest(X: torch.Tensor, K: int, ws: torch.Tensor | None = None, out=None):
+    """Algorithm 1 step 1 as farthest-point traversal from object 0.
+
+    Returns (init_idx int32 [K], centers float32 [K, M]) on X's device;
+    asynchronous on the current stream. `out` may supply both tensors."""
+    _check_x(X)
+    n, M = X.shape
+    if out is None:
+        idx = torch.empty(int(K), dtype=torch.int32, device=X.device)
+        centers = torch.empty((int(K), M), dtype=torch.float32, device=X.device)
+    else:
+        idx, centers = out
+    if ws is None:
+        nbytes = kmeans_init_workspace_bytes(n, M, K)
+        if nbytes == 0:
+            raise KmeansError("kmeans_init_workspace_bytes", KMEANS_EINVAL)
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=X.device)
+    rc = _lib.kmeans_init_farthest(_dev_ptr(X), n, M, int(K), _dev_ptr(idx), _dev_ptr(centers),
+                                   _dev_ptr(ws), ws.numel(), _stream_ptr(X.device))
+    if rc:
+        raise KmeansError("kmeans_init_farthest", rc)
+    return idx, centers
 
 
 def kmeans_assign(X: torch.Tensor, centers: torch.Tensor, with_min_d2: bool = False, path=None):

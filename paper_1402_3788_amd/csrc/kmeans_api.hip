@@ -1,5 +1,6 @@
 // C ABI of the Lloyd-iteration library: argument validation, workspace layout,
-// and the iteration control of Algorithm 1 (steps 2-7). See include/kmeans.h.
+// the initial centres of Algorithm 1 step 1 and the iteration control of its
+// steps 2-7. See include/kmeans.h.
 #include "../../include/kmeans.h"
 #include "lloyd.h"
 
@@ -88,6 +89,23 @@ void bind_workspace(StepArgs &a, const Layout &L, char *ws)
 
 int hip_status(hipError_t e) { return e == hipSuccess ? KMEANS_OK : KMEANS_EHIP; }
 
+// Workspace of the farthest-point traversal: [fp64 nearest distance per
+// object] [fp64 candidate distance 2*G] [int32 candidate index 2*G].
+struct InitLayout {
+    FarthestPlan plan;
+    size_t cand_v_off, cand_i_off, total;
+};
+
+InitLayout init_layout(int64_t n, int32_t M)
+{
+    InitLayout L{};
+    L.plan = plan_farthest(n, M);
+    L.cand_v_off = align_up((size_t)n * sizeof(double), 256);
+    L.cand_i_off = align_up(L.cand_v_off + 2 * (size_t)L.plan.groups * sizeof(double), 256);
+    L.total = align_up(L.cand_i_off + 2 * (size_t)L.plan.groups * sizeof(int32_t), 256);
+    return L;
+}
+
 }  // namespace
 
 extern "C" {
@@ -109,6 +127,32 @@ size_t kmeans_workspace_bytes(int64_t n, int32_t M, int32_t K, uint32_t flags)
     if (check_shape(n, M, K) != KMEANS_OK || (flags & ~kKnownFlags)) return 0;
     if (check_flags(flags) != KMEANS_OK || select_path(M, K, flags) < 0) return 0;
     return layout(n, M, K, flags).total;
+}
+
+size_t kmeans_init_workspace_bytes(int64_t n, int32_t M, int32_t K)
+{
+    if (check_shape(n, M, K) != KMEANS_OK || (int64_t)K > n) return 0;
+    return init_layout(n, M).total;
+}
+
+int kmeans_init_farthest(const float *X, int64_t n, int32_t M, int32_t K, int32_t *init_idx,
+                         float *centers, void *workspace, size_t workspace_bytes, void *stream)
+{
+    if (!X || !init_idx || !centers) return KMEANS_EINVAL;
+    int rc = check_shape(n, M, K);
+    if (rc) return rc;
+    if ((int64_t)K > n || !aligned16(X)) return KMEANS_EINVAL;
+    const InitLayout L = init_layout(n, M);
+    if (!workspace || workspace_bytes < L.total) return KMEANS_EWORKSPACE;
+    char *ws = static_cast<char *>(workspace);
+    FarthestArgs a{};
+    a.X = X; a.n = n; a.M = M; a.K = K;
+    a.nearest = reinterpret_cast<double *>(ws);
+    a.cand_v = reinterpret_cast<double *>(ws + L.cand_v_off);
+    a.cand_i = reinterpret_cast<int32_t *>(ws + L.cand_i_off);
+    a.idx = init_idx;
+    a.centers = centers;
+    return hip_status(launch_farthest(a, L.plan, static_cast<hipStream_t>(stream)));
 }
 
 int kmeans_assign(const float *X, int64_t n, int32_t M, const float *centers, int32_t K,

@@ -118,4 +118,27 @@ hipError_t launch_ctl_reset(Ctl *ctl, hipStream_t s);
 // accumulating launch with `groups` workgroups (lloyd_centres.hip).
 hipError_t launch_centres(const StepArgs &a, int groups, hipStream_t s);
 
+// Farthest-point initial centres (farthest.hip).
+struct FarthestPlan {
+    int waves;          // wavefronts per workgroup
+    int groups;         // persistent workgroups of each pass
+    size_t lds_bytes;   // dynamic LDS per workgroup (one tile slot per wave)
+};
+
+struct FarthestArgs {
+    const float *X;
+    int64_t n;
+    int M;
+    int K;              // 1 <= K <= n
+    double *nearest;    // [n] fp64 nearest-centre distances (-1 = chosen)
+    double *cand_v;     // [2][groups] farthest distance per workgroup and pass parity
+    int32_t *cand_i;    // [2][groups] its object index
+    int32_t *idx;       // out: [K] chosen objects
+    float *centers;     // out: [K][M] their rows
+};
+
+FarthestPlan plan_farthest(int64_t n, int M);
+// Enqueues the K launches of the traversal on s.
+hipError_t launch_farthest(const FarthestArgs &a, const FarthestPlan &plan, hipStream_t s);
+
 }  // namespace lloyd

@@ -130,6 +130,31 @@ def test_run_validation(kw, code):
     assert _run(**kw) == code
 
 
+def test_init_workspace_bytes():
+    assert km.kmeans_init_workspace_bytes(2_000_000, 25, 16) >= 2_000_000 * 8
+    assert km.kmeans_init_workspace_bytes(10, 2, 11) == 0       # K > n
+    assert km.kmeans_init_workspace_bytes(10, 65, 4) == 0
+    assert km.kmeans_init_workspace_bytes(0, 2, 1) == 0
+    assert km.kmeans_init_workspace_bytes(1, 1, 1) > 0
+
+
+def _init(X=FAKE, n=100, M=4, K=3, idx=FAKE, C=FAKE, ws=FAKE, wsb=None):
+    wsb = km.kmeans_init_workspace_bytes(n, M, K) if wsb is None else wsb
+    return km._lib.kmeans_init_farthest(X, n, M, K, idx, C, ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(X=None), km.KMEANS_EINVAL), (dict(idx=None), km.KMEANS_EINVAL),
+    (dict(C=None), km.KMEANS_EINVAL), (dict(n=0), km.KMEANS_EINVAL),
+    (dict(K=0), km.KMEANS_EINVAL), (dict(n=5, K=6), km.KMEANS_EINVAL),
+    (dict(M=65), km.KMEANS_EUNSUPPORTED), (dict(K=1025), km.KMEANS_EUNSUPPORTED),
+    (dict(X=FAKE_MISALIGNED), km.KMEANS_EINVAL), (dict(ws=None), km.KMEANS_EWORKSPACE),
+    (dict(wsb=100 * 8), km.KMEANS_EWORKSPACE),
+])
+def test_init_validation(kw, code):
+    assert _init(**kw) == code
+
+
 def test_run_null_iterations_pointer():
     it_null = ctypes.POINTER(ctypes.c_int32)()
     assert _run(iters=it_null) == km.KMEANS_EINVAL

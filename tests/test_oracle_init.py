@@ -114,8 +114,9 @@ def test_rejects_k_above_n():
 
 
 @pytest.mark.slow
-def test_stored_workload_init_matches():
-    """The initial centres stored for the 2*10^6 x 25, K = 16 workload (written
-    by the numpy recipe) are the oracle's."""
-    X, _, idx, _ = workloads.load("aniso25d-n2m-k16")
-    assert np.array_equal(oracle.init_farthest(X, 16), idx)
+@pytest.mark.parametrize("name", ["aniso25d-n2m-k16", "blobs25d-n2m-k256"])
+def test_stored_workload_init_matches(name):
+    """The initial centres stored for the 2*10^6 x 25 workloads (written by the
+    numpy recipe) are the oracle's."""
+    X, _, idx, _ = workloads.load(name)
+    assert np.array_equal(oracle.init_farthest(X, workloads.get(name).K), idx)
