@@ -19,14 +19,21 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(_HERE, "kmeans_oracle.c")
 LIB = os.path.join(_HERE, "libkmeans_oracle.so")
 CFLAGS = ["-std=c99", "-O2", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared"]
+# the multi-threaded CPU regime (Algorithm 3), a baseline checked against the oracle
+ALG3_SRC = os.path.join(_HERE, "kmeans_alg3.c")
+ALG3_LIB = os.path.join(_HERE, "libkmeans_alg3.so")
+ALG3_CFLAGS = ["-std=c99", "-O3", "-fopenmp", "-ffp-contract=off", "-fno-fast-math", "-fPIC",
+               "-shared"]
 
 
 def build(force: bool = True) -> str:
-    """Compile the oracle with gcc (no fused multiply-add, no fast-math)."""
-    if force or not os.path.exists(LIB):
-        tmp = LIB + ".tmp"
-        subprocess.check_call(["gcc", *CFLAGS, "-o", tmp, SRC, "-lm"])
-        os.replace(tmp, LIB)
+    """Compile the oracle with gcc (no fused multiply-add, no fast-math), and
+    the Algorithm 3 baseline beside it."""
+    for src, lib, flags in ((SRC, LIB, CFLAGS), (ALG3_SRC, ALG3_LIB, ALG3_CFLAGS)):
+        if force or not os.path.exists(lib):
+            tmp = lib + ".tmp"
+            subprocess.check_call(["gcc", *flags, "-o", tmp, src, "-lm"])
+            os.replace(tmp, lib)
     return LIB
 
 
@@ -157,6 +164,43 @@ def init_farthest(X, K: int):
     if rc:
         raise ValueError(f"oracle_init_farthest failed ({rc})")
     return idx
+
+
+_alg3 = None
+
+
+def _load_alg3():
+    global _alg3
+    if _alg3 is None:
+        if not os.path.exists(ALG3_LIB):
+            build(force=False)
+        lib = ctypes.CDLL(ALG3_LIB)
+        p, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
+        lib.alg3_run.argtypes = [p, i64, i32, i32, p, i32, i32, i32, p, p, p, p, p]
+        lib.alg3_run.restype = ctypes.c_int
+        _alg3 = lib
+    return _alg3
+
+
+def alg3_run(X, K: int, init, max_iter: int, fixed: bool = False, threads: int = 0):
+    """The multi-threaded CPU regime (Algorithm 3, steps 4-9) from the given
+    initial centres: each of `threads` threads (0 = all OpenMP threads)
+    assigns and sums its 1/N of the objects. Returns (labels, centers, counts,
+    iterations, threads used)."""
+    X, init = _f32(X), _f32(init)
+    n, M = X.shape
+    if init.shape != (K, M):
+        raise ValueError("init shape mismatch")
+    labels = np.empty(n, np.int32)
+    centers = np.empty((K, M), np.float32)
+    counts = np.empty(K, np.int32)
+    iters, used = ctypes.c_int32(0), ctypes.c_int32(0)
+    rc = _load_alg3().alg3_run(_ptr(X), n, M, int(K), _ptr(init), int(max_iter),
+                               int(bool(fixed)), int(threads), _ptr(labels), _ptr(centers),
+                               _ptr(counts), ctypes.byref(iters), ctypes.byref(used))
+    if rc:
+        raise ValueError(f"alg3_run failed ({rc})")
+    return labels, centers, counts, int(iters.value), int(used.value)
 
 
 def gap_rel(d1, d2):
