@@ -3,7 +3,8 @@
 TEST INFRASTRUCTURE ONLY: the oracle is the slow, obviously correct statement
 of Algorithm 1's Lloyd iteration (assign by Eq. (2), centres of gravity by
 Eq. (1), stop on congruent centres) and of its step 1 (farthest-point initial
-centres) that the GPU library is checked against.
+centres, and Algorithm 2's steps 1-2: diameter of Eq. (3) and the centre of
+gravity of the whole set) that the GPU library is checked against.
 Only the tests, the smoke check and the benchmark's CPU-baseline leg use it;
 the GPU library never imports, links or calls it.
 """
@@ -51,6 +52,10 @@ def _bind(path: str):
     lib.oracle_sse.restype = ctypes.c_double
     lib.oracle_init_farthest.argtypes = [p, i64, i32, i32, p]
     lib.oracle_init_farthest.restype = ctypes.c_int
+    lib.oracle_centroid.argtypes = [p, i64, i32, p]
+    lib.oracle_centroid.restype = ctypes.c_int
+    lib.oracle_diameter.argtypes = [p, i64, i32, p, p, p]
+    lib.oracle_diameter.restype = ctypes.c_int
     return lib
 
 
@@ -164,6 +169,33 @@ def init_farthest(X, K: int):
     if rc:
         raise ValueError(f"oracle_init_farthest failed ({rc})")
     return idx
+
+
+def centroid(X):
+    """Centre of gravity of the whole set (Algorithm 2 step 2): fp32 of the
+    fp64 mean, objects summed in ascending order."""
+    X = _f32(X)
+    n, M = X.shape
+    c = np.empty(M, np.float32)
+    rc = _load().oracle_centroid(_ptr(X), n, M, _ptr(c))
+    if rc:
+        raise ValueError(f"oracle_centroid failed ({rc})")
+    return c
+
+
+def diameter(X):
+    """Eq. (3), squared (Algorithm 2 step 1): (d2, k, l) with d2 the largest
+    squared distance over pairs k < l (fp64) and (k, l) the lexicographically
+    smallest pair reaching it; (0.0, 0, 0) when n == 1. O(n^2 M)."""
+    X = _f32(X)
+    n, M = X.shape
+    d2 = ctypes.c_double(0.0)
+    k, l = ctypes.c_int32(0), ctypes.c_int32(0)
+    rc = _load().oracle_diameter(_ptr(X), n, M, ctypes.byref(d2), ctypes.byref(k),
+                                 ctypes.byref(l))
+    if rc:
+        raise ValueError(f"oracle_diameter failed ({rc})")
+    return float(d2.value), int(k.value), int(l.value)
 
 
 _alg3 = None

@@ -248,3 +248,52 @@ int oracle_init_farthest(const float *X, int64_t n, int32_t M, int32_t K, int32_
     free(chosen);
     return 0;
 }
+
+/*
+ * Centre of gravity of the whole set (Algorithm 2 step 2):
+ *   centroid[j] = fp32( (sum over i ascending of (double)x_ij) / n ).
+ */
+int oracle_centroid(const float *X, int64_t n, int32_t M, float *centroid)
+{
+    if (!X || !centroid || n < 1 || M < 1)
+        return ORACLE_EINVAL;
+    for (int32_t j = 0; j < M; ++j) {
+        double s = 0.0;
+        for (int64_t i = 0; i < n; ++i)
+            s = s + (double)X[i * (int64_t)M + j];
+        centroid[j] = (float)(s / (double)n);
+    }
+    return 0;
+}
+
+/*
+ * Diameter of the set, Eq. (3) (Algorithm 2 step 1: "find two objects with
+ * the largest distance between them"), squared:
+ *   d2 = max over pairs k < l of |x_k - x_l|^2 (normative fp64 order above),
+ *   (k, l) = the lexicographically smallest pair reaching it.
+ * With n = 1 there is no pair: d2 = 0 and k = l = 0. The diameter is sqrt(d2).
+ */
+int oracle_diameter(const float *X, int64_t n, int32_t M, double *d2, int32_t *k_out,
+                    int32_t *l_out)
+{
+    if (!X || !d2 || !k_out || !l_out || n < 1 || M < 1)
+        return ORACLE_EINVAL;
+    double best = 0.0;
+    int64_t bk = 0, bl = n > 1 ? 1 : 0;
+    int have = 0;
+    for (int64_t k = 0; k < n; ++k) {
+        for (int64_t l = k + 1; l < n; ++l) {
+            double d = sqdist(X + k * (int64_t)M, X + l * (int64_t)M, M);
+            if (!have || d > best) {
+                best = d;
+                bk = k;
+                bl = l;
+                have = 1;
+            }
+        }
+    }
+    *d2 = best;
+    *k_out = (int32_t)bk;
+    *l_out = (int32_t)bl;
+    return 0;
+}

@@ -1,6 +1,7 @@
 """Plant plausible mistakes in a copy of the oracle source and check that the
 oracle's pins (tests/test_oracle.py for the Lloyd iteration,
-tests/test_oracle_init.py for the initial centres) catch every one of them.
+tests/test_oracle_init.py for the initial centres, tests/test_oracle_diameter.py
+for the diameter and the centre of gravity) catch every one of them.
 
 Each mutant is a textual edit of oracle/kmeans_oracle.c compiled into a
 temporary library; the pin suite then runs against it in a subprocess (through
@@ -40,6 +41,22 @@ MUTANTS = {
     "count_off_by_one": ("cnt[l] += 1;", "cnt[l] += (i > 0);"),
 }
 
+# mistakes in the diameter and the centre of gravity of the whole set, caught by
+# tests/test_oracle_diameter.py
+DIAM_MUTANTS = {
+    "diam_ties_to_last_pair": ("if (!have || d > best) {", "if (!have || d >= best) {"),
+    "diam_self_pairs": ("for (int64_t l = k + 1; l < n; ++l) {", "for (int64_t l = k; l < n; ++l) {"),
+    "diam_drops_last_feature": ("double d = sqdist(X + k * (int64_t)M, X + l * (int64_t)M, M);",
+                                "double d = sqdist(X + k * (int64_t)M, X + l * (int64_t)M, "
+                                "M > 1 ? M - 1 : M);"),
+    "diam_skips_last_object": ("for (int64_t l = k + 1; l < n; ++l) {",
+                               "for (int64_t l = k + 1; l < n - 1; ++l) {"),
+    "centroid_divides_by_n_minus_1": ("centroid[j] = (float)(s / (double)n);",
+                                      "centroid[j] = (float)(s / (double)(n > 1 ? n - 1 : 1));"),
+    "centroid_skips_first_object": ("for (int64_t i = 0; i < n; ++i)\n            s = s + (double)X",
+                                    "for (int64_t i = 1; i < n; ++i)\n            s = s + (double)X"),
+}
+
 # mistakes in the initial-centre traversal, caught by tests/test_oracle_init.py
 INIT_MUTANTS = {
     "init_ties_to_highest_index": ("nearest[i] > nearest[far]", "nearest[i] >= nearest[far]"),
@@ -64,10 +81,13 @@ def source():
 
 
 @pytest.mark.slow
-@pytest.mark.parametrize("name", sorted(MUTANTS) + sorted(INIT_MUTANTS))
+@pytest.mark.parametrize("name", sorted(MUTANTS) + sorted(INIT_MUTANTS) + sorted(DIAM_MUTANTS))
 def test_pins_catch_planted_mistake(name, source, tmp_path):
-    old, new = MUTANTS[name] if name in MUTANTS else INIT_MUTANTS[name]
-    pins = "test_oracle.py" if name in MUTANTS else "test_oracle_init.py"
+    for table, pins in ((MUTANTS, "test_oracle.py"), (INIT_MUTANTS, "test_oracle_init.py"),
+                        (DIAM_MUTANTS, "test_oracle_diameter.py")):
+        if name in table:
+            old, new = table[name]
+            break
     assert source.count(old) == 1, f"mutant {name} does not apply"
     src = tmp_path / "mutant.c"
     src.write_text(source.replace(old, new))
