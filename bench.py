@@ -11,12 +11,14 @@ timed step does the full work (this workload converges after 2 passes; the
 passes after that repeat the same labels and centres). X is resident in device
 memory before the timed region starts.
 
-The JSON line also times the farthest-point initial centres of Algorithm 1
-step 1 (K passes over X) on the same workload ("init_farthest").
+The JSON line also times, on the same workload, the farthest-point initial
+centres of Algorithm 1 step 1 (K passes over X, "init_farthest") and the
+diameter of Eq. (3) with the centre of gravity (Algorithm 2 steps 1-2, two
+passes over all pairs on the bf16 matrix cores, "diameter").
 
 python bench.py [--gpus 1] [--steps 1000] [--warmup 20] [--workload 3]
                 [--path auto|direct|mfma|tiles] [--no-cpu-baseline] [--no-control]
-                [--no-init]
+                [--no-init] [--no-diameter]
 python bench.py --calibrate-copy   # plain device copy of known size (PMC scaling)
 
 Prints ONE JSON line.
@@ -61,6 +63,7 @@ def _parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-control", action="store_true")
     ap.add_argument("--no-init", action="store_true")
+    ap.add_argument("--no-diameter", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true")
     return ap.parse_args()
 
@@ -164,6 +167,39 @@ def time_init(torch, km, Xg, K, stored, reps=5):
     }
 
 
+BF16_PEAK_TFLOPS = 2500.0       # MI355X dense bf16 matrix peak
+
+
+def time_diameter(torch, km, Xg, reps=2):
+    """Two passes over the n(n-1)/2 pairs; each pair costs three bf16 matrix
+    products over 32 ceil((M+2)/32) features per pass."""
+    n, M = Xg.shape
+    ws = torch.empty(km.kmeans_diameter_workspace_bytes(n, M), dtype=torch.uint8,
+                     device=Xg.device)
+    d2a, paira, _ = km.kmeans_diameter(Xg, ws=ws)             # warm-up
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(reps):
+        d2, pair, _ = km.kmeans_diameter(Xg, ws=ws)
+    e.record()
+    torch.cuda.synchronize()
+    sec = s.elapsed_time(e) / 1e3 / reps
+    P = 32 * ((M + 2 + 31) // 32)
+    pairs = n * (n - 1) // 2
+    flops = 2 * pairs * 3 * 2 * P
+    return {
+        "ms": round(sec * 1e3, 2),
+        "d2": float(d2.item()),
+        "pair": [int(v) for v in pair.cpu().numpy()],
+        "repeatable": bool(d2.item() == d2a.item() and torch.equal(pair, paira)),
+        "pairs_per_s": round(2 * pairs / sec, 1),
+        "bf16_matrix_TFLOPs": round(flops / sec / 1e12, 1),
+        "frac_bf16_peak": round(flops / sec / 1e12 / BF16_PEAK_TFLOPS, 4),
+        "reps": reps,
+    }
+
+
 def main():
     args = _parse()
     if args.gpus != 1:
@@ -259,6 +295,9 @@ def main():
 
     if not args.no_init:
         result["init_farthest"] = time_init(torch, km, Xg, K, init_idx)
+
+    if not args.no_diameter:
+        result["diameter"] = time_diameter(torch, km, Xg)
 
     if not args.no_control:
         # same kernel on a point set larger than the 256 MB Infinity Cache

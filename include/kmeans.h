@@ -7,7 +7,9 @@
  * 4, Euclidean distance of Eq. (2)), recompute each cluster's centre of gravity
  * (steps 3 and 5, Eq. (1)), and stop when the centres of the last two
  * iterations are congruent (steps 6 and 7). It also picks the K initial
- * centres of step 1 by farthest-point traversal.
+ * centres of step 1 by farthest-point traversal, and computes the diameter
+ * (Eq. (3)) and the centre of gravity of the whole set (Algorithm 2 steps
+ * 1-2).
  *
  * Conventions shared by every entry point
  *   - Array arguments are DEVICE pointers (hipMalloc'd or equivalent), owned by
@@ -118,6 +120,45 @@ size_t kmeans_init_workspace_bytes(int64_t n, int32_t M, int32_t K);
  */
 int kmeans_init_farthest(const float *X, int64_t n, int32_t M, int32_t K, int32_t *init_idx,
                          float *centers, void *workspace, size_t workspace_bytes, void *stream);
+
+/* Bytes of device workspace that kmeans_centroid needs (one fp64 row of
+ * partial sums per workgroup, a few KB). 0 for refused shapes. Pure host. */
+size_t kmeans_centroid_workspace_bytes(int64_t n, int32_t M);
+
+/*
+ * Centre of gravity of the whole set, Algorithm 2 step 2 (and Algorithm 4's
+ * coordinate sums): centroid[j] = fp32(fp64 sum of x_ij over all i / n),
+ * fp32 [M] DEVICE array. The sums are formed in an order fixed by the shape
+ * (deterministic). Asynchronous on `stream`: two launches, one pass over X.
+ */
+int kmeans_centroid(const float *X, int64_t n, int32_t M, float *centroid, void *workspace,
+                    size_t workspace_bytes, void *stream);
+
+/* Bytes of device workspace that kmeans_diameter needs: the centre of gravity
+ * and its partials, four bf16 operand arrays of n * 32 ceil((M+2)/32) values
+ * each (n rounded up to 8192), and 16 bytes per (512-object block, 8192-object
+ * chunk) pair. 0 for refused shapes (also when n needs more than 65535 column
+ * chunks). Pure host computation. */
+size_t kmeans_diameter_workspace_bytes(int64_t n, int32_t M);
+
+/*
+ * Diameter of the set, Eq. (3) (Algorithm 2 step 1, "find two objects with
+ * the largest distance between them"), squared:
+ *   *d2     = max over pairs k < l of |x_k - x_l|^2 (DEVICE fp64 [1]), the
+ *             fp64 value formed as e = x_j - c_j, d = d + e*e (features
+ *             ascending, each operation rounded), so exactly that pair's value;
+ *   pair    = (k, l), the lexicographically smallest pair reaching it
+ *             (DEVICE int32 [2]);
+ *   centroid (may be NULL) = the centre of gravity, as kmeans_centroid.
+ * With n = 1 there is no pair: *d2 = 0 and pair = (0, 0). The diameter is
+ * sqrt(*d2). The pairs are screened with split-precision bf16 matrix
+ * products under a proven error bound and the close ones re-evaluated in
+ * fp64, so the result is exact; the cost is two passes over all n(n-1)/2
+ * pairs (O(n^2 M): about half a second per pass at n = 2*10^6, M = 25).
+ * Asynchronous on `stream`.
+ */
+int kmeans_diameter(const float *X, int64_t n, int32_t M, double *d2, int32_t *pair,
+                    float *centroid, void *workspace, size_t workspace_bytes, void *stream);
 
 /*
  * Assignment, Algorithm 1 steps 2 and 4, distance of Eq. (2):

@@ -11,6 +11,8 @@ Entry points (same names as the C ABI):
     kmeans_run(X, K, init_centers, max_iter, fixed_iters=False, path=None,
                timing=False) -> (labels, centers, counts, iterations[, timing])
     kmeans_init_farthest(X, K, ws=None) -> (init_idx, centers)
+    kmeans_centroid(X, ws=None) -> centroid
+    kmeans_diameter(X, ws=None) -> (d2, pair, centroid)
     kmeans_workspace_bytes(n, M, K, flags=0), kmeans_init_workspace_bytes(n, M, K),
     kmeans_strerror(code)
 """
@@ -36,7 +38,9 @@ KMEANS_PATH_MFMA = 1 << 2
 KMEANS_PATH_TILES = 1 << 3
 
 EXPORTED = ("kmeans_workspace_bytes", "kmeans_strerror", "kmeans_assign", "kmeans_update",
-            "kmeans_run", "kmeans_init_workspace_bytes", "kmeans_init_farthest")
+            "kmeans_run", "kmeans_init_workspace_bytes", "kmeans_init_farthest",
+            "kmeans_centroid_workspace_bytes", "kmeans_centroid",
+            "kmeans_diameter_workspace_bytes", "kmeans_diameter")
 
 
 class KmeansTiming(ctypes.Structure):
@@ -72,6 +76,14 @@ def _load() -> ctypes.CDLL:
     lib.kmeans_init_workspace_bytes.restype = sz
     lib.kmeans_init_farthest.argtypes = [p, i64, i32, i32, p, p, p, sz, p]
     lib.kmeans_init_farthest.restype = ctypes.c_int
+    lib.kmeans_centroid_workspace_bytes.argtypes = [i64, i32]
+    lib.kmeans_centroid_workspace_bytes.restype = sz
+    lib.kmeans_centroid.argtypes = [p, i64, i32, p, p, sz, p]
+    lib.kmeans_centroid.restype = ctypes.c_int
+    lib.kmeans_diameter_workspace_bytes.argtypes = [i64, i32]
+    lib.kmeans_diameter_workspace_bytes.restype = sz
+    lib.kmeans_diameter.argtypes = [p, i64, i32, p, p, p, p, sz, p]
+    lib.kmeans_diameter.restype = ctypes.c_int
     return lib
 
 
@@ -148,6 +160,52 @@ def kmeans_init_farthest(X: torch.Tensor, K: int, ws: torch.Tensor | None = None
     if rc:
         raise KmeansError("kmeans_init_farthest", rc)
     return idx, centers
+
+
+def kmeans_centroid_workspace_bytes(n: int, M: int) -> int:
+    return int(_lib.kmeans_centroid_workspace_bytes(int(n), int(M)))
+
+
+def kmeans_diameter_workspace_bytes(n: int, M: int) -> int:
+    return int(_lib.kmeans_diameter_workspace_bytes(int(n), int(M)))
+
+
+def _ws(nbytes: int, device, fn: str) -> torch.Tensor:
+    if nbytes == 0:
+        raise KmeansError(fn, KMEANS_EUNSUPPORTED)
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+def kmeans_centroid(X: torch.Tensor, ws: torch.Tensor | None = None):
+    """Algorithm 2 step 2: the centre of gravity of all objects (float32 [M])."""
+    _check_x(X)
+    n, M = X.shape
+    c = torch.empty(M, dtype=torch.float32, device=X.device)
+    if ws is None:
+        ws = _ws(kmeans_centroid_workspace_bytes(n, M), X.device, "kmeans_centroid_workspace_bytes")
+    rc = _lib.kmeans_centroid(_dev_ptr(X), n, M, _dev_ptr(c), _dev_ptr(ws), ws.numel(),
+                              _stream_ptr(X.device))
+    if rc:
+        raise KmeansError("kmeans_centroid", rc)
+    return c
+
+
+def kmeans_diameter(X: torch.Tensor, ws: torch.Tensor | None = None):
+    """Eq. (3), Algorithm 2 step 1: (d2 float64 [1], pair int32 [2], centroid
+    float32 [M]) on X's device; the diameter is sqrt(d2), reached by the
+    lexicographically smallest pair. Asynchronous on the current stream."""
+    _check_x(X)
+    n, M = X.shape
+    d2 = torch.empty(1, dtype=torch.float64, device=X.device)
+    pair = torch.empty(2, dtype=torch.int32, device=X.device)
+    c = torch.empty(M, dtype=torch.float32, device=X.device)
+    if ws is None:
+        ws = _ws(kmeans_diameter_workspace_bytes(n, M), X.device, "kmeans_diameter_workspace_bytes")
+    rc = _lib.kmeans_diameter(_dev_ptr(X), n, M, _dev_ptr(d2), _dev_ptr(pair), _dev_ptr(c),
+                              _dev_ptr(ws), ws.numel(), _stream_ptr(X.device))
+    if rc:
+        raise KmeansError("kmeans_diameter", rc)
+    return d2, pair, c
 
 
 def kmeans_assign(X: torch.Tensor, centers: torch.Tensor, with_min_d2: bool = False, path=None):

@@ -18,7 +18,8 @@ LIB = os.path.join(HERE, "libkmeans_mi355x.so")
 # part of the feature-count range so the template instantiations build in parallel
 PARTS = 4
 SOURCES = ([("kmeans_api.hip", [], "kmeans_api.o"), ("lloyd_ctl.hip", [], "lloyd_ctl.o"),
-            ("lloyd_centres.hip", [], "lloyd_centres.o"), ("farthest.hip", [], "farthest.o")]
+            ("lloyd_centres.hip", [], "lloyd_centres.o"), ("farthest.hip", [], "farthest.o"),
+            ("diameter.hip", [], "diameter.o")]
            + [(f, [f"-DLLOYD_PART={p}"], f.replace(".hip", f"_part{p}.o"))
               for f in ("lloyd_tile.hip", "lloyd_lane.hip") for p in range(PARTS)])
 ARCH = "gfx950"

@@ -106,6 +106,40 @@ InitLayout init_layout(int64_t n, int32_t M)
     return L;
 }
 
+// Workspace of the centroid and diameter launches: [counters 256 B]
+// [fp32 centroid, M] [fp64 partials G*M] then, for the diameter, the four
+// split operand arrays [npad][4 ks] x 16 B and the item slots.
+struct DiamLayout {
+    CentroidPlan cplan;
+    DiameterPlan dplan;
+    size_t centroid_off, part_off, ops_off, ops_bytes, slots_off, total;
+};
+
+DiamLayout diam_layout(int64_t n, int32_t M, bool diameter)
+{
+    DiamLayout L{};
+    L.cplan = plan_centroid(n, M);
+    L.centroid_off = 256;
+    L.part_off = align_up(L.centroid_off + (size_t)M * sizeof(float), 256);
+    L.ops_off = align_up(L.part_off + (size_t)L.cplan.groups * M * sizeof(double), 256);
+    L.total = L.ops_off;
+    if (diameter) {
+        L.dplan = plan_diameter(n, M);
+        L.ops_bytes = align_up((size_t)L.dplan.npad * 4 * L.dplan.ks * 16, 256);
+        L.slots_off = L.ops_off + 4 * L.ops_bytes;
+        L.total = align_up(L.slots_off + (size_t)L.dplan.row_blocks * L.dplan.chunks *
+                                             sizeof(DiamBest), 256);
+    }
+    return L;
+}
+
+// Grid limits of the diameter passes (row blocks in x, column chunks in y).
+bool diameter_fits(int64_t n, int32_t M)
+{
+    const DiameterPlan p = plan_diameter(n, M);
+    return p.chunks <= 65535 && p.row_blocks <= INT32_MAX;
+}
+
 }  // namespace
 
 extern "C" {
@@ -153,6 +187,62 @@ int kmeans_init_farthest(const float *X, int64_t n, int32_t M, int32_t K, int32_
     a.idx = init_idx;
     a.centers = centers;
     return hip_status(launch_farthest(a, L.plan, static_cast<hipStream_t>(stream)));
+}
+
+size_t kmeans_centroid_workspace_bytes(int64_t n, int32_t M)
+{
+    if (check_shape(n, M, 1) != KMEANS_OK) return 0;
+    return diam_layout(n, M, false).total;
+}
+
+int kmeans_centroid(const float *X, int64_t n, int32_t M, float *centroid, void *workspace,
+                    size_t workspace_bytes, void *stream)
+{
+    if (!X || !centroid) return KMEANS_EINVAL;
+    int rc = check_shape(n, M, 1);
+    if (rc) return rc;
+    if (!aligned16(X)) return KMEANS_EINVAL;
+    const DiamLayout L = diam_layout(n, M, false);
+    if (!workspace || workspace_bytes < L.total) return KMEANS_EWORKSPACE;
+    char *ws = static_cast<char *>(workspace);
+    return hip_status(launch_centroid(X, n, M, reinterpret_cast<double *>(ws + L.part_off),
+                                      nullptr, centroid, nullptr, L.cplan,
+                                      static_cast<hipStream_t>(stream)));
+}
+
+size_t kmeans_diameter_workspace_bytes(int64_t n, int32_t M)
+{
+    if (check_shape(n, M, 1) != KMEANS_OK || !diameter_fits(n, M)) return 0;
+    return diam_layout(n, M, true).total;
+}
+
+int kmeans_diameter(const float *X, int64_t n, int32_t M, double *d2, int32_t *pair,
+                    float *centroid, void *workspace, size_t workspace_bytes, void *stream)
+{
+    if (!X || !d2 || !pair) return KMEANS_EINVAL;
+    int rc = check_shape(n, M, 1);
+    if (rc) return rc;
+    if (!aligned16(X)) return KMEANS_EINVAL;
+    if (!diameter_fits(n, M)) return KMEANS_EUNSUPPORTED;
+    const DiamLayout L = diam_layout(n, M, true);
+    if (!workspace || workspace_bytes < L.total) return KMEANS_EWORKSPACE;
+    char *ws = static_cast<char *>(workspace);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    DiameterArgs a{};
+    a.X = X; a.n = n; a.M = M;
+    a.counters = reinterpret_cast<uint32_t *>(ws);
+    a.centroid_ws = reinterpret_cast<float *>(ws + L.centroid_off);
+    a.ah = reinterpret_cast<uint4 *>(ws + L.ops_off);
+    a.al = reinterpret_cast<uint4 *>(ws + L.ops_off + L.ops_bytes);
+    a.bh = reinterpret_cast<uint4 *>(ws + L.ops_off + 2 * L.ops_bytes);
+    a.bl = reinterpret_cast<uint4 *>(ws + L.ops_off + 3 * L.ops_bytes);
+    a.slots = reinterpret_cast<DiamBest *>(ws + L.slots_off);
+    a.d2 = d2;
+    a.pair = pair;
+    rc = hip_status(launch_centroid(X, n, M, reinterpret_cast<double *>(ws + L.part_off),
+                                    a.centroid_ws, centroid, a.counters, L.cplan, s));
+    if (rc) return rc;
+    return hip_status(launch_diameter(a, L.dplan, s));
 }
 
 int kmeans_assign(const float *X, int64_t n, int32_t M, const float *centers, int32_t K,
