@@ -45,7 +45,9 @@
 // operands of 64 rows in registers; the workgroup stages 64 columns of B at a
 // time in LDS (row stride padded by 16 bytes so the 16-byte reads of a
 // 16-object column block spread over the banks), and each wave forms 4 x 4
-// blocks of 16 x 16 pairs per step.
+// blocks of 16 x 16 pairs per step. The next step's operands are loaded into
+// registers while the current step is computed, and written to the other of
+// two LDS buffers after it: one barrier per step.
 #include "lloyd_device.h"
 
 #include <climits>
@@ -193,6 +195,22 @@ __device__ inline float diam_threshold(const uint32_t *counters, int M)
     return t;
 }
 
+// fp64 squared distance of objects i and j in the fixed operation order (the
+// rare exact re-evaluation of pass 2, kept out of line so that the matrix
+// loop's registers are not sized for it).
+__device__ __attribute__((noinline)) double diam_exact_d2(const float *__restrict__ X, int M,
+                                                          int64_t i, int64_t j)
+{
+    const float *xi = X + i * M, *xj = X + j * M;
+    double d = 0.0;
+    for (int f = 0; f < M; ++f) {
+        const double e = (double)xi[f] - (double)xj[f];
+        const double sq = e * e;
+        d = d + sq;
+    }
+    return d;
+}
+
 template <int KS, bool kExact>
 __global__ void __launch_bounds__(kDiamThreads)
 diam_pass_kernel(const uint4 *__restrict__ ah, const uint4 *__restrict__ al,
@@ -202,7 +220,11 @@ diam_pass_kernel(const uint4 *__restrict__ ah, const uint4 *__restrict__ al,
 {
     constexpr int G4 = 4 * KS;                        // 16-byte groups per operand row
     constexpr int kLdsRow = G4 + 1;                   // uint4 per LDS row (16 bytes padding)
-    __shared__ uint4 sbh[64 * kLdsRow], sbl[64 * kLdsRow];
+    constexpr int kQuads = 64 * G4;                   // 16-byte groups per step and array
+    constexpr int kPer = 2 * kQuads / kDiamThreads;   // groups each thread copies (= KS)
+    static_assert(2 * kQuads == kPer * kDiamThreads, "copy split");
+    // two buffers (the step computed and the step being staged), hi and lo
+    __shared__ uint4 sb[2][2][64 * kLdsRow];
     __shared__ float wmax[kDiamWaves];
     __shared__ DiamBest wbest[kDiamWaves];
 
@@ -235,20 +257,37 @@ diam_pass_kernel(const uint4 *__restrict__ ah, const uint4 *__restrict__ al,
             a_lo[rb][ks][0] = l.x; a_lo[rb][ks][1] = l.y; a_lo[rb][ks][2] = l.z; a_lo[rb][ks][3] = l.w;
         }
 
+    // staging: thread t copies groups q = t + 512 u of the hi array, then the lo array
+    uint4 pf[kPer];
+    auto fetch = [&](int64_t s) {
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+            const int q = threadIdx.x + kDiamThreads * u;
+            const int qq = q < kQuads ? q : q - kQuads;
+            pf[u] = (q < kQuads ? bh : bl)[(s * 64 + qq / G4) * G4 + qq % G4];
+        }
+    };
+    auto stage = [&](int buf) {
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+            const int q = threadIdx.x + kDiamThreads * u;
+            const int qq = q < kQuads ? q : q - kQuads;
+            sb[buf][q < kQuads ? 0 : 1][(qq / G4) * kLdsRow + qq % G4] = pf[u];
+        }
+    };
+
     float vmax = -INFINITY;
     double bd = -1.0;
     int bk = INT_MAX, bl_ = INT_MAX;
 
+    fetch(s_lo);
+    stage(0);
+    __syncthreads();
     for (int64_t s = s_lo; s < s_hi; ++s) {
-        // stage the 64 columns' operands (each thread copies 16-byte groups)
-        const int64_t c0 = s * 64;
-        __syncthreads();                              // the previous step's reads are done
-        for (int q = threadIdx.x; q < 64 * G4; q += kDiamThreads) {
-            const int o = q / G4, g = q % G4;
-            sbh[o * kLdsRow + g] = bh[(c0 + o) * G4 + g];
-            sbl[o * kLdsRow + g] = bl[(c0 + o) * G4 + g];
-        }
-        __syncthreads();
+        const int buf = (int)((s - s_lo) & 1);
+        const bool more = s + 1 < s_hi;
+        if (more) fetch(s + 1);                       // in flight during this step
+        const uint4 *lh = sb[buf][0], *ll = sb[buf][1];
 
         f4v acc[4][4];
 #pragma unroll
@@ -261,8 +300,8 @@ diam_pass_kernel(const uint4 *__restrict__ ah, const uint4 *__restrict__ al,
 #pragma unroll
             for (int cb = 0; cb < 4; ++cb) {
                 const int o = 16 * cb + lane % 16;
-                const uint4 h = sbh[o * kLdsRow + ks * 4 + lane / 16];
-                const uint4 l = sbl[o * kLdsRow + ks * 4 + lane / 16];
+                const uint4 h = lh[o * kLdsRow + ks * 4 + lane / 16];
+                const uint4 l = ll[o * kLdsRow + ks * 4 + lane / 16];
                 b_hi[cb][0] = h.x; b_hi[cb][1] = h.y; b_hi[cb][2] = h.z; b_hi[cb][3] = h.w;
                 b_lo[cb][0] = l.x; b_lo[cb][1] = l.y; b_lo[cb][2] = l.z; b_lo[cb][3] = l.w;
             }
@@ -286,40 +325,42 @@ diam_pass_kernel(const uint4 *__restrict__ ah, const uint4 *__restrict__ al,
                         as_bf8(a_hi[rb][ks]), as_bf8(b_hi[cb]), acc[rb][cb], 0, 0, 0);
         }
 
+        // the step's largest value in this lane (padding rows and columns give
+        // exactly 0, never above a real pair's value by more than the bound;
+        // pairs i >= j repeat pairs i < j)
+        float smax = -INFINITY;
+#pragma unroll
+        for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+            for (int cb = 0; cb < 4; ++cb)
+                smax = fmaxf(fmaxf(smax, fmaxf(acc[rb][cb][0], acc[rb][cb][1])),
+                             fmaxf(acc[rb][cb][2], acc[rb][cb][3]));
         if constexpr (!kExact) {
-            // padding rows and columns give exactly 0, never above a real pair's
-            // value by more than the bound; pairs i >= j repeat pairs i < j
-#pragma unroll
-            for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-                for (int cb = 0; cb < 4; ++cb)
-                    vmax = fmaxf(fmaxf(vmax, fmaxf(acc[rb][cb][0], acc[rb][cb][1])),
-                                 fmaxf(acc[rb][cb][2], acc[rb][cb][3]));
-        } else {
+            vmax = fmaxf(vmax, smax);
+        } else if (__builtin_amdgcn_ballot_w64(smax >= thr) != 0) {
+            // rare: some pair of this wave's step reaches the threshold
+            const int64_t c0 = s * 64;
 #pragma unroll
             for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
                 for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
-                        if (acc[rb][cb][r] < thr) continue;
                         const int64_t i = r0 + 16 * rb + 4 * (lane / 16) + r;
                         const int64_t j = c0 + 16 * cb + lane % 16;
-                        if (i >= j || j >= n) continue;
-                        const float *xi = X + i * M, *xj = X + j * M;
-                        double d = 0.0;
-                        for (int f = 0; f < M; ++f) {
-                            const double e = (double)xi[f] - (double)xj[f];
-                            const double sq = e * e;
-                            d = d + sq;
-                        }
-                        if (diam_better(d, (int)i, (int)j, bd, bk, bl_)) {
-                            bd = d;
-                            bk = (int)i;
-                            bl_ = (int)j;
+                        if (acc[rb][cb][r] >= thr && i < j && j < n) {
+                            const double d = diam_exact_d2(X, M, i, j);
+                            if (diam_better(d, (int)i, (int)j, bd, bk, bl_)) {
+                                bd = d;
+                                bk = (int)i;
+                                bl_ = (int)j;
+                            }
                         }
                     }
         }
+
+        if (more) stage(buf ^ 1);                     // the other buffer: nobody reads it now
+        __syncthreads();
     }
 
     if constexpr (!kExact) {
