@@ -24,9 +24,12 @@
 //   pass 1  every pair block is three v_mfma_f32_16x16x32_bf16 per 32
 //           features (lo.hi, hi.lo, hi.hi), exact products summed in fp32;
 //           the maximum approximate value d~* over all pairs is kept (integer
-//           atomic max of an order-preserving key: order-free);
-//   pass 2  the same products again; every pair k < l with
-//           d~ >= d~* - 2B is re-evaluated in fp64 in the fixed operation order
+//           atomic max of an order-preserving key: order-free), and each
+//           work item's own maximum goes to its result slot;
+//   pass 2  items whose maximum is below the threshold d~* - 2B write an
+//           empty result at once; the others form the same products again,
+//           and every pair k < l with d~ >= d~* - 2B is re-evaluated in fp64
+//           in the fixed operation order
 //           e = x_j - c_j, d = d + e*e (features ascending, each operation
 //           rounded) and the lexicographic best (largest d, then lowest k,
 //           then lowest l) is kept.
@@ -236,12 +239,21 @@ diam_pass_kernel(const uint4 *__restrict__ ah, const uint4 *__restrict__ al,
     int64_t s_hi = (J0 + kChunk) / 64;
     if (s_hi > nsteps_total) s_hi = nsteps_total;
     if (s_lo >= s_hi) {                               // wholly below the diagonal or past n
-        if (kExact && threadIdx.x == 0) slots[slot] = DiamBest{-1.0, INT_MAX, INT_MAX};
+        if (threadIdx.x == 0) slots[slot] = DiamBest{kExact ? -1.0 : -INFINITY, INT_MAX, INT_MAX};
         return;
     }
 
     float thr = 0.f;
-    if constexpr (kExact) thr = diam_threshold<KS>(counters, M);
+    if constexpr (kExact) {
+        // pass 1 left this item's largest value in its slot: an item with no
+        // value at the threshold has no candidate pair
+        thr = diam_threshold<KS>(counters, M);
+        if (!(slots[slot].d >= (double)thr)) {
+            __syncthreads();                          // every thread has read the slot
+            if (threadIdx.x == 0) slots[slot] = DiamBest{-1.0, INT_MAX, INT_MAX};
+            return;
+        }
+    }
 
     // A operands of this wave's 64 rows: 4 row blocks x KS steps of 32 features
     uint32_t a_hi[4][KS][4], a_lo[4][KS][4];
@@ -372,6 +384,7 @@ diam_pass_kernel(const uint4 *__restrict__ ah, const uint4 *__restrict__ al,
             float m = wmax[0];
             for (int k = 1; k < kDiamWaves; ++k) m = fmaxf(m, wmax[k]);
             atomicMax(&counters[1], float_key(m));
+            slots[slot] = DiamBest{(double)m, INT_MAX, INT_MAX};   // read by pass 2
         }
     } else {
 #pragma unroll
