@@ -215,11 +215,11 @@ __device__ __attribute__((noinline)) double diam_exact_d2(const float *__restric
 }
 
 template <int KS, bool kExact>
-__global__ void __launch_bounds__(kDiamThreads)
-diam_pass_kernel(const uint4 *__restrict__ ah, const uint4 *__restrict__ al,
-                 const uint4 *__restrict__ bh, const uint4 *__restrict__ bl, int64_t n,
-                 int64_t nsteps_total, const float *__restrict__ X, int M,
-                 uint32_t *__restrict__ counters, DiamBest *__restrict__ slots)
+__device__ __forceinline__ void
+diam_pass_body(const uint4 *__restrict__ ah, const uint4 *__restrict__ al,
+               const uint4 *__restrict__ bh, const uint4 *__restrict__ bl, int64_t n,
+               int64_t nsteps_total, const float *__restrict__ X, int M,
+               uint32_t *__restrict__ counters, DiamBest *__restrict__ slots)
 {
     constexpr int G4 = 4 * KS;                        // 16-byte groups per operand row
     constexpr int kLdsRow = G4 + 1;                   // uint4 per LDS row (16 bytes padding)
@@ -301,74 +301,86 @@ diam_pass_kernel(const uint4 *__restrict__ ah, const uint4 *__restrict__ al,
         if (more) fetch(s + 1);                       // in flight during this step
         const uint4 *lh = sb[buf][0], *ll = sb[buf][1];
 
-        f4v acc[4][4];
+        // the step's 64 columns in two halves of 32 (2 column blocks): with 32
+        // accumulator registers per half, 32 features fit 4 waves per SIMD
+        // (two workgroups per compute unit)
 #pragma unroll
-        for (int rb = 0; rb < 4; ++rb)
+        for (int half = 0; half < 2; ++half) {
+            f4v acc[4][2];
 #pragma unroll
-            for (int cb = 0; cb < 4; ++cb) acc[rb][cb] = f4v{0.f, 0.f, 0.f, 0.f};
+            for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            uint32_t b_hi[4][4], b_lo[4][4];
+                for (int cc = 0; cc < 2; ++cc) acc[rb][cc] = f4v{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int cb = 0; cb < 4; ++cb) {
-                const int o = 16 * cb + lane % 16;
-                const uint4 h = lh[o * kLdsRow + ks * 4 + lane / 16];
-                const uint4 l = ll[o * kLdsRow + ks * 4 + lane / 16];
-                b_hi[cb][0] = h.x; b_hi[cb][1] = h.y; b_hi[cb][2] = h.z; b_hi[cb][3] = h.w;
-                b_lo[cb][0] = l.x; b_lo[cb][1] = l.y; b_lo[cb][2] = l.z; b_lo[cb][3] = l.w;
+            for (int ks = 0; ks < KS; ++ks) {
+                // one operand set at a time: the hi parts of B with both parts
+                // of A, then the lo parts of B with hi(A)
+                uint32_t b[2][4];
+#pragma unroll
+                for (int cc = 0; cc < 2; ++cc) {
+                    const int o = 16 * (2 * half + cc) + lane % 16;
+                    const uint4 h = lh[o * kLdsRow + ks * 4 + lane / 16];
+                    b[cc][0] = h.x; b[cc][1] = h.y; b[cc][2] = h.z; b[cc][3] = h.w;
+                }
+#pragma unroll
+                for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+                    for (int cc = 0; cc < 2; ++cc)
+                        acc[rb][cc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                            as_bf8(a_lo[rb][ks]), as_bf8(b[cc]), acc[rb][cc], 0, 0, 0);
+#pragma unroll
+                for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+                    for (int cc = 0; cc < 2; ++cc)
+                        acc[rb][cc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                            as_bf8(a_hi[rb][ks]), as_bf8(b[cc]), acc[rb][cc], 0, 0, 0);
+#pragma unroll
+                for (int cc = 0; cc < 2; ++cc) {
+                    const int o = 16 * (2 * half + cc) + lane % 16;
+                    const uint4 l = ll[o * kLdsRow + ks * 4 + lane / 16];
+                    b[cc][0] = l.x; b[cc][1] = l.y; b[cc][2] = l.z; b[cc][3] = l.w;
+                }
+#pragma unroll
+                for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+                    for (int cc = 0; cc < 2; ++cc)
+                        acc[rb][cc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                            as_bf8(a_hi[rb][ks]), as_bf8(b[cc]), acc[rb][cc], 0, 0, 0);
             }
-#pragma unroll
-            for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-                for (int cb = 0; cb < 4; ++cb)
-                    acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        as_bf8(a_lo[rb][ks]), as_bf8(b_hi[cb]), acc[rb][cb], 0, 0, 0);
-#pragma unroll
-            for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-                for (int cb = 0; cb < 4; ++cb)
-                    acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        as_bf8(a_hi[rb][ks]), as_bf8(b_lo[cb]), acc[rb][cb], 0, 0, 0);
-#pragma unroll
-            for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-                for (int cb = 0; cb < 4; ++cb)
-                    acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        as_bf8(a_hi[rb][ks]), as_bf8(b_hi[cb]), acc[rb][cb], 0, 0, 0);
-        }
 
-        // the step's largest value in this lane (padding rows and columns give
-        // exactly 0, never above a real pair's value by more than the bound;
-        // pairs i >= j repeat pairs i < j)
-        float smax = -INFINITY;
-#pragma unroll
-        for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-            for (int cb = 0; cb < 4; ++cb)
-                smax = fmaxf(fmaxf(smax, fmaxf(acc[rb][cb][0], acc[rb][cb][1])),
-                             fmaxf(acc[rb][cb][2], acc[rb][cb][3]));
-        if constexpr (!kExact) {
-            vmax = fmaxf(vmax, smax);
-        } else if (__builtin_amdgcn_ballot_w64(smax >= thr) != 0) {
-            // rare: some pair of this wave's step reaches the threshold
-            const int64_t c0 = s * 64;
+            // the largest value of the half in this lane (padding rows and
+            // columns give exactly 0, never above a real pair's value by more
+            // than the bound; pairs i >= j repeat pairs i < j)
+            float smax = -INFINITY;
 #pragma unroll
             for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
-                for (int cb = 0; cb < 4; ++cb)
+                for (int cc = 0; cc < 2; ++cc)
+                    smax = fmaxf(fmaxf(smax, fmaxf(acc[rb][cc][0], acc[rb][cc][1])),
+                                 fmaxf(acc[rb][cc][2], acc[rb][cc][3]));
+            if constexpr (!kExact) {
+                vmax = fmaxf(vmax, smax);
+            } else if (__builtin_amdgcn_ballot_w64(smax >= thr) != 0) {
+                // rare: some pair of this wave's half step reaches the threshold
+                const int64_t c0 = s * 64 + 32 * half;
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const int64_t i = r0 + 16 * rb + 4 * (lane / 16) + r;
-                        const int64_t j = c0 + 16 * cb + lane % 16;
-                        if (acc[rb][cb][r] >= thr && i < j && j < n) {
-                            const double d = diam_exact_d2(X, M, i, j);
-                            if (diam_better(d, (int)i, (int)j, bd, bk, bl_)) {
-                                bd = d;
-                                bk = (int)i;
-                                bl_ = (int)j;
+                for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+                    for (int cc = 0; cc < 2; ++cc)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const int64_t i = r0 + 16 * rb + 4 * (lane / 16) + r;
+                            const int64_t j = c0 + 16 * cc + lane % 16;
+                            if (acc[rb][cc][r] >= thr && i < j && j < n) {
+                                const double d = diam_exact_d2(X, M, i, j);
+                                if (diam_better(d, (int)i, (int)j, bd, bk, bl_)) {
+                                    bd = d;
+                                    bk = (int)i;
+                                    bl_ = (int)j;
+                                }
                             }
                         }
-                    }
+            }
         }
 
         if (more) stage(buf ^ 1);                     // the other buffer: nobody reads it now
@@ -406,6 +418,16 @@ diam_pass_kernel(const uint4 *__restrict__ ah, const uint4 *__restrict__ al,
             slots[slot] = b;
         }
     }
+}
+
+template <int KS, bool kExact>
+__global__ void __launch_bounds__(kDiamThreads)
+diam_pass_kernel(const uint4 *__restrict__ ah, const uint4 *__restrict__ al,
+                 const uint4 *__restrict__ bh, const uint4 *__restrict__ bl, int64_t n,
+                 int64_t nsteps_total, const float *__restrict__ X, int M,
+                 uint32_t *__restrict__ counters, DiamBest *__restrict__ slots)
+{
+    diam_pass_body<KS, kExact>(ah, al, bh, bl, n, nsteps_total, X, M, counters, slots);
 }
 
 // The lexicographic best of all item slots. With n = 1 there is no pair:
@@ -459,11 +481,13 @@ hipError_t diam_launch_ks(const DiameterArgs &a, const DiameterPlan &pl, hipStre
     if (e != hipSuccess) return e;
     const dim3 grid((unsigned)pl.row_blocks, (unsigned)pl.chunks);
     const int64_t nsteps = pl.npad / 64;
-    hipLaunchKernelGGL((diam_pass_kernel<KS, false>), grid, dim3(kDiamThreads), 0, s, a.ah,
-                       a.al, a.bh, a.bl, a.n, nsteps, a.X, a.M, a.counters, a.slots);
+    auto pass1 = diam_pass_kernel<KS, false>;
+    auto pass2 = diam_pass_kernel<KS, true>;
+    hipLaunchKernelGGL(pass1, grid, dim3(kDiamThreads), 0, s, a.ah, a.al, a.bh, a.bl, a.n,
+                       nsteps, a.X, a.M, a.counters, a.slots);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL((diam_pass_kernel<KS, true>), grid, dim3(kDiamThreads), 0, s, a.ah,
-                       a.al, a.bh, a.bl, a.n, nsteps, a.X, a.M, a.counters, a.slots);
+    hipLaunchKernelGGL(pass2, grid, dim3(kDiamThreads), 0, s, a.ah, a.al, a.bh, a.bl, a.n,
+                       nsteps, a.X, a.M, a.counters, a.slots);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(diam_final_kernel, dim3(1), dim3(1024), 0, s, a.slots,
                        (int64_t)pl.row_blocks * pl.chunks, a.n, a.d2, a.pair);
