@@ -155,6 +155,50 @@ def test_init_validation(kw, code):
     assert _init(**kw) == code
 
 
+def test_centroid_and_diameter_workspace_bytes():
+    assert km.kmeans_centroid_workspace_bytes(2_000_000, 25) > 0
+    assert km.kmeans_centroid_workspace_bytes(0, 25) == 0
+    assert km.kmeans_centroid_workspace_bytes(10, 65) == 0
+    # four bf16 operand arrays of 32 ceil((M+2)/32) values per object (n padded to 8192)
+    assert km.kmeans_diameter_workspace_bytes(2_000_000, 25) >= 4 * 2_000_000 * 32 * 2
+    assert (km.kmeans_diameter_workspace_bytes(10_000, 40)
+            > km.kmeans_diameter_workspace_bytes(10_000, 30))
+    assert km.kmeans_diameter_workspace_bytes(1, 1) > 0
+    assert km.kmeans_diameter_workspace_bytes(0, 3) == 0
+    assert km.kmeans_diameter_workspace_bytes(2**31 - 1, 4) == 0     # too many column chunks
+
+
+def _centroid(X=FAKE, n=100, M=4, C=FAKE, ws=FAKE, wsb=None):
+    wsb = km.kmeans_centroid_workspace_bytes(n, M) if wsb is None else wsb
+    return km._lib.kmeans_centroid(X, n, M, C, ws, wsb, None)
+
+
+def _diameter(X=FAKE, n=100, M=4, d2=FAKE, pair=FAKE, C=FAKE, ws=FAKE, wsb=None):
+    wsb = km.kmeans_diameter_workspace_bytes(n, M) if wsb is None else wsb
+    return km._lib.kmeans_diameter(X, n, M, d2, pair, C, ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(X=None), km.KMEANS_EINVAL), (dict(C=None), km.KMEANS_EINVAL),
+    (dict(n=0), km.KMEANS_EINVAL), (dict(M=0), km.KMEANS_EINVAL),
+    (dict(M=65), km.KMEANS_EUNSUPPORTED), (dict(X=FAKE_MISALIGNED), km.KMEANS_EINVAL),
+    (dict(ws=None), km.KMEANS_EWORKSPACE), (dict(wsb=8), km.KMEANS_EWORKSPACE),
+])
+def test_centroid_validation(kw, code):
+    assert _centroid(**kw) == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(X=None), km.KMEANS_EINVAL), (dict(d2=None), km.KMEANS_EINVAL),
+    (dict(pair=None), km.KMEANS_EINVAL), (dict(n=0), km.KMEANS_EINVAL),
+    (dict(M=65), km.KMEANS_EUNSUPPORTED), (dict(n=2**31 - 1), km.KMEANS_EUNSUPPORTED),
+    (dict(X=FAKE_MISALIGNED), km.KMEANS_EINVAL), (dict(ws=None), km.KMEANS_EWORKSPACE),
+    (dict(wsb=4096), km.KMEANS_EWORKSPACE),
+])
+def test_diameter_validation(kw, code):
+    assert _diameter(**kw) == code
+
+
 def test_run_null_iterations_pointer():
     it_null = ctypes.POINTER(ctypes.c_int32)()
     assert _run(iters=it_null) == km.KMEANS_EINVAL
