@@ -104,7 +104,7 @@ const char *kmeans_strerror(int status);
 size_t kmeans_init_workspace_bytes(int64_t n, int32_t M, int32_t K);
 
 /*
- * Initial centres, Algorithm 1 step 1 ("K objects far away from each other";
+ * Initial centres, Algorithm 1 step 1 (K objects lying far apart;
  * the paper leaves the method open), read as farthest-point traversal from
  * object 0:
  *   init_idx[0] = 0;
@@ -142,8 +142,8 @@ int kmeans_centroid(const float *X, int64_t n, int32_t M, float *centroid, void 
 size_t kmeans_diameter_workspace_bytes(int64_t n, int32_t M);
 
 /*
- * Diameter of the set, Eq. (3) (Algorithm 2 step 1, "find two objects with
- * the largest distance between them"), squared:
+ * Diameter of the set, Eq. (3) (Algorithm 2 step 1: the pair of objects that
+ * lie farthest apart), squared:
  *   *d2     = max over pairs k < l of |x_k - x_l|^2 (DEVICE fp64 [1]), the
  *             fp64 value formed as e = x_j - c_j, d = d + e*e (features
  *             ascending, each operation rounded), so exactly that pair's value;

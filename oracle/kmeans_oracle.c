@@ -201,7 +201,7 @@ double oracle_sse(const float *X, int64_t n, int32_t M, const int32_t *labels,
 }
 
 /*
- * Initial centres, Algorithm 1 step 1 ("K objects far away from each other";
+ * Initial centres, Algorithm 1 step 1 (K objects lying far apart;
  * the paper leaves the method open). Reading: farthest-point traversal from
  * object 0 --
  *   idx[0] = 0;
@@ -267,8 +267,8 @@ int oracle_centroid(const float *X, int64_t n, int32_t M, float *centroid)
 }
 
 /*
- * Diameter of the set, Eq. (3) (Algorithm 2 step 1: "find two objects with
- * the largest distance between them"), squared:
+ * Diameter of the set, Eq. (3) (Algorithm 2 step 1: the pair of objects that
+ * lie farthest apart), squared:
  *   d2 = max over pairs k < l of |x_k - x_l|^2 (normative fp64 order above),
  *   (k, l) = the lexicographically smallest pair reaching it.
  * With n = 1 there is no pair: d2 = 0 and k = l = 0. The diameter is sqrt(d2).

@@ -1,4 +1,4 @@
-// Initial centres of Algorithm 1 step 1 ("K objects far away from each other",
+// Initial centres of Algorithm 1 step 1 (K objects lying far apart,
 // method left open), taken as farthest-point traversal from object 0:
 //   idx[0] = 0, and idx[m] = the not-yet-chosen object whose smallest squared
 //   distance (Eq. (2)) to the objects idx[0..m-1] is largest, lowest index on
