@@ -48,6 +48,10 @@ def _bind(path: str):
     lib.oracle_update.restype = ctypes.c_int
     lib.oracle_run.argtypes = [p, i64, i32, i32, p, i32, i32, p, p, p, p, p, p]
     lib.oracle_run.restype = ctypes.c_int
+    lib.oracle_assign_l1.argtypes = [p, i64, i32, p, i32, p, p, p]
+    lib.oracle_assign_l1.restype = ctypes.c_int
+    lib.oracle_run_l1.argtypes = [p, i64, i32, i32, p, i32, i32, p, p, p, p, p, p]
+    lib.oracle_run_l1.restype = ctypes.c_int
     lib.oracle_sse.argtypes = [p, i64, i32, p, p, i32]
     lib.oracle_sse.restype = ctypes.c_double
     lib.oracle_init_farthest.argtypes = [p, i64, i32, i32, p]
@@ -87,11 +91,20 @@ def _ptr(a):
     return ctypes.c_void_p(a.ctypes.data) if a is not None else None
 
 
-def assign(X, C, with_dist: bool = False):
+def _metric_fn(metric: str, l2_name: str, l1_name: str):
+    if metric == "l2":
+        return getattr(_load(), l2_name)
+    if metric == "l1":
+        return getattr(_load(), l1_name)
+    raise ValueError(f"unknown metric {metric!r}")
+
+
+def assign(X, C, with_dist: bool = False, metric: str = "l2"):
     """Algorithm 1 steps 2/4: nearest centre per object (lowest index on ties).
 
-    Returns labels (int32 [n]); with_dist also returns the best and second-best
-    squared distances (fp64 [n]); second-best is +inf when K == 1.
+    metric "l2": squared Euclidean distance (Eq. (2)); "l1": city-block
+    distance. Returns labels (int32 [n]); with_dist also returns the best and
+    second-best distances (fp64 [n]); second-best is +inf when K == 1.
     """
     X, C = _f32(X), _f32(C)
     n, M = X.shape
@@ -101,7 +114,8 @@ def assign(X, C, with_dist: bool = False):
     labels = np.empty(n, np.int32)
     d1 = np.empty(n, np.float64) if with_dist else None
     d2 = np.empty(n, np.float64) if with_dist else None
-    rc = _load().oracle_assign(_ptr(X), n, M, _ptr(C), K, _ptr(labels), _ptr(d1), _ptr(d2))
+    fn = _metric_fn(metric, "oracle_assign", "oracle_assign_l1")
+    rc = fn(_ptr(X), n, M, _ptr(C), K, _ptr(labels), _ptr(d1), _ptr(d2))
     if rc:
         raise ValueError(f"oracle_assign failed ({rc})")
     return (labels, d1, d2) if with_dist else labels
@@ -124,8 +138,10 @@ def update(X, labels, K: int, prev):
     return centers, counts
 
 
-def run(X, K: int, init, max_iter: int, fixed: bool = False, with_dist: bool = False):
-    """Algorithm 1 steps 2-7 from the given initial centres.
+def run(X, K: int, init, max_iter: int, fixed: bool = False, with_dist: bool = False,
+        metric: str = "l2"):
+    """Algorithm 1 steps 2-7 from the given initial centres (assignment by
+    the metric: "l2" as Eq. (2), or "l1").
 
     Returns (labels, centers, counts, iterations) and, with with_dist, the last
     assignment's best / second-best squared distances.
@@ -140,9 +156,10 @@ def run(X, K: int, init, max_iter: int, fixed: bool = False, with_dist: bool = F
     iters = ctypes.c_int32(0)
     d1 = np.empty(n, np.float64) if with_dist else None
     d2 = np.empty(n, np.float64) if with_dist else None
-    rc = _load().oracle_run(_ptr(X), n, M, K, _ptr(init), int(max_iter), int(bool(fixed)),
-                            _ptr(labels), _ptr(centers), _ptr(counts),
-                            ctypes.byref(iters), _ptr(d1), _ptr(d2))
+    fn = _metric_fn(metric, "oracle_run", "oracle_run_l1")
+    rc = fn(_ptr(X), n, M, K, _ptr(init), int(max_iter), int(bool(fixed)),
+            _ptr(labels), _ptr(centers), _ptr(counts),
+            ctypes.byref(iters), _ptr(d1), _ptr(d2))
     if rc:
         raise ValueError(f"oracle_run failed ({rc})")
     out = (labels, centers, counts, int(iters.value))

@@ -142,6 +142,51 @@ static int congruent(const float *a, const float *b, int64_t count)
 }
 
 /*
+ * Another metric for the assignment (the paper allows one in place of
+ * Eq. (2)): the L1 (city-block) distance sum_j |x_j - c_j|, in fp64 as
+ *     e = (double)x_j - (double)c_j ;  d = d + |e|
+ * for j ascending, each operation rounded. Only the assignment changes; the
+ * centres stay the centres of gravity of Eq. (1).
+ */
+static double l1dist(const float *x, const float *c, int32_t M)
+{
+    double sum = 0.0;
+    for (int32_t f = 0; f < M; ++f) {
+        double diff = (double)x[f] - (double)c[f];
+        sum = sum + fabs(diff);
+    }
+    return sum;
+}
+
+/* Assignment by the L1 distance: the same rule as oracle_assign (lowest k on
+ * ties, optional best and second-best distances). */
+int oracle_assign_l1(const float *X, int64_t n, int32_t M, const float *C, int32_t K,
+                     int32_t *labels, double *d1, double *d2)
+{
+    if (!X || !C || !labels || n < 0 || M < 1 || K < 1)
+        return ORACLE_EINVAL;
+    for (int64_t obj = 0; obj < n; ++obj) {
+        const float *row = X + obj * (int64_t)M;
+        double nearest = INFINITY, runner_up = INFINITY;
+        int32_t choice = 0;
+        for (int32_t k = 0; k < K; ++k) {
+            double dk = l1dist(row, C + (int64_t)k * M, M);
+            if (dk < nearest) {
+                runner_up = nearest;
+                nearest = dk;
+                choice = k;
+            } else if (dk < runner_up) {
+                runner_up = dk;
+            }
+        }
+        labels[obj] = choice;
+        if (d1) d1[obj] = nearest;
+        if (d2) d2[obj] = runner_up;
+    }
+    return 0;
+}
+
+/*
  * The whole loop, Algorithm 1 steps 2-7 from the given initial centres:
  *   for t = 1 .. max_iter:
  *     labels_t = assign(C_{t-1});  C_t = update(labels_t, C_{t-1});
@@ -150,9 +195,10 @@ static int congruent(const float *a, const float *b, int64_t count)
  * assignment passes executed. d1/d2 (nullable) receive the final pass's best
  * and second-best squared distances per object.
  */
-int oracle_run(const float *X, int64_t n, int32_t M, int32_t K, const float *init,
-               int32_t max_iter, int32_t fixed, int32_t *labels, float *centers,
-               int32_t *counts, int32_t *iterations, double *d1, double *d2)
+static int run_loop(const float *X, int64_t n, int32_t M, int32_t K, const float *init,
+                    int32_t max_iter, int32_t fixed, int32_t l1, int32_t *labels,
+                    float *centers, int32_t *counts, int32_t *iterations, double *d1,
+                    double *d2)
 {
     if (!X || !init || !labels || !centers || !counts || !iterations || n < 0 ||
         M < 1 || K < 1 || max_iter < 1)
@@ -169,7 +215,10 @@ int oracle_run(const float *X, int64_t n, int32_t M, int32_t K, const float *ini
     int32_t t = 0;
     int rc = 0;
     for (t = 1; t <= max_iter; ++t) {
-        rc = oracle_assign(X, n, M, prev, K, labels, d1, d2);
+        if (l1)
+            rc = oracle_assign_l1(X, n, M, prev, K, labels, d1, d2);
+        else
+            rc = oracle_assign(X, n, M, prev, K, labels, d1, d2);
         if (rc) break;
         rc = oracle_update(X, n, M, labels, K, prev, cur, counts);
         if (rc) break;
@@ -185,6 +234,23 @@ int oracle_run(const float *X, int64_t n, int32_t M, int32_t K, const float *ini
     free(prev);
     free(cur);
     return rc;
+}
+
+int oracle_run(const float *X, int64_t n, int32_t M, int32_t K, const float *init,
+               int32_t max_iter, int32_t fixed, int32_t *labels, float *centers,
+               int32_t *counts, int32_t *iterations, double *d1, double *d2)
+{
+    return run_loop(X, n, M, K, init, max_iter, fixed, 0, labels, centers, counts, iterations,
+                    d1, d2);
+}
+
+/* The same loop with the L1 assignment. */
+int oracle_run_l1(const float *X, int64_t n, int32_t M, int32_t K, const float *init,
+                  int32_t max_iter, int32_t fixed, int32_t *labels, float *centers,
+                  int32_t *counts, int32_t *iterations, double *d1, double *d2)
+{
+    return run_loop(X, n, M, K, init, max_iter, fixed, 1, labels, centers, counts, iterations,
+                    d1, d2);
 }
 
 /* Objective sum_i |x_i - c_{label_i}|^2 in fp64 (used by the invariant tests). */

@@ -1,7 +1,8 @@
 """Plant plausible mistakes in a copy of the oracle source and check that the
 oracle's pins (tests/test_oracle.py for the Lloyd iteration,
 tests/test_oracle_init.py for the initial centres, tests/test_oracle_diameter.py
-for the diameter and the centre of gravity) catch every one of them.
+for the diameter and the centre of gravity, tests/test_oracle_l1.py for the L1
+assignment) catch every one of them.
 
 Each mutant is a textual edit of oracle/kmeans_oracle.c compiled into a
 temporary library; the pin suite then runs against it in a subprocess (through
@@ -57,6 +58,16 @@ DIAM_MUTANTS = {
                                     "for (int64_t i = 1; i < n; ++i)\n            s = s + (double)X"),
 }
 
+# mistakes in the L1 assignment, caught by tests/test_oracle_l1.py
+L1_MUTANTS = {
+    "l1_squares_instead_of_abs": ("sum = sum + fabs(diff);", "sum = sum + diff * diff;"),
+    "l1_signed_difference": ("sum = sum + fabs(diff);", "sum = sum + diff;"),
+    "l1_ties_to_highest_index": ("if (dk < nearest) {", "if (dk <= nearest) {"),
+    "l1_drops_last_feature": ("for (int32_t f = 0; f < M; ++f) {\n        double diff",
+                              "for (int32_t f = 0; f < (M > 1 ? M - 1 : M); ++f) {\n        double diff"),
+    "l1_run_uses_l2": ("if (l1)\n            rc = oracle_assign_l1", "if (0)\n            rc = oracle_assign_l1"),
+}
+
 # mistakes in the initial-centre traversal, caught by tests/test_oracle_init.py
 INIT_MUTANTS = {
     "init_ties_to_highest_index": ("nearest[i] > nearest[far]", "nearest[i] >= nearest[far]"),
@@ -81,10 +92,12 @@ def source():
 
 
 @pytest.mark.slow
-@pytest.mark.parametrize("name", sorted(MUTANTS) + sorted(INIT_MUTANTS) + sorted(DIAM_MUTANTS))
+@pytest.mark.parametrize("name", sorted(MUTANTS) + sorted(INIT_MUTANTS) + sorted(DIAM_MUTANTS)
+                         + sorted(L1_MUTANTS))
 def test_pins_catch_planted_mistake(name, source, tmp_path):
     for table, pins in ((MUTANTS, "test_oracle.py"), (INIT_MUTANTS, "test_oracle_init.py"),
-                        (DIAM_MUTANTS, "test_oracle_diameter.py")):
+                        (DIAM_MUTANTS, "test_oracle_diameter.py"),
+                        (L1_MUTANTS, "test_oracle_l1.py")):
         if name in table:
             old, new = table[name]
             break
