@@ -14,11 +14,12 @@ memory before the timed region starts.
 The JSON line also times, on the same workload, the farthest-point initial
 centres of Algorithm 1 step 1 (K passes over X, "init_farthest") and the
 diameter of Eq. (3) with the centre of gravity (Algorithm 2 steps 1-2, two
-passes over all pairs on the bf16 matrix cores, "diameter").
+passes over all pairs on the bf16 matrix cores, "diameter"), and Lloyd
+iterations that assign by the L1 distance instead ("l1_metric").
 
 python bench.py [--gpus 1] [--steps 1000] [--warmup 20] [--workload 3]
                 [--path auto|direct|mfma|tiles] [--no-cpu-baseline] [--no-control]
-                [--no-init] [--no-diameter]
+                [--no-init] [--no-diameter] [--no-l1]
 python bench.py --calibrate-copy   # plain device copy of known size (PMC scaling)
 
 Prints ONE JSON line.
@@ -64,6 +65,7 @@ def _parse():
     ap.add_argument("--no-control", action="store_true")
     ap.add_argument("--no-init", action="store_true")
     ap.add_argument("--no-diameter", action="store_true")
+    ap.add_argument("--no-l1", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true")
     return ap.parse_args()
 
@@ -299,6 +301,22 @@ def main():
 
     if not args.no_diameter:
         result["diameter"] = time_diameter(torch, km, Xg)
+
+    if not args.no_l1:
+        # the other metric: an L1 assign launch, then the accumulate-from-labels
+        # and centres launches of the Euclidean path (three launches per step)
+        T = 200
+        km.kmeans_run(Xg, K, Cg, 5, fixed_iters=True, metric="l1", out=out, ws=ws)
+        torch.cuda.synchronize()
+        _, _, _, _, tml = km.kmeans_run(Xg, K, Cg, T, fixed_iters=True, metric="l1", timing=True,
+                                        out=out, ws=ws)
+        result["l1_metric"] = {
+            "iters_per_s": round(T / (tml.step_ms / 1e3), 1),
+            "iteration_avg_us": round(tml.step_ms * 1e3 / T, 2),
+            "assign_launch_avg_us": round(tml.assign_ms * 1e3 / tml.assign_samples, 2),
+            "fallbacks_per_iteration": round(km.ctl_fallbacks(ws) / T, 2),
+            "steps": T,
+        }
 
     if not args.no_control:
         # same kernel on a point set larger than the 256 MB Infinity Cache

@@ -62,6 +62,10 @@ extern "C" {
                                       /* tiles; KMEANS_EUNSUPPORTED when the tiles' per-workgroup     */
                                       /* state (centre operands, fp64 sums) does not fit in LDS       */
 #define KMEANS_PATH_TILES   (1u << 3) /* force the 64-object-tile matrix-core path (any K)           */
+#define KMEANS_METRIC_L1    (1u << 4) /* assign by the L1 (city-block) distance sum_j |x_j - c_j|      */
+                                      /* instead of Eq. (2) -- the paper allows another metric; the   */
+                                      /* centres stay the centres of gravity of Eq. (1). One form (one */
+                                      /* object per lane on the vector ALU): no path flag with it.     */
 /* Without a path flag: 64-object tiles on the matrix cores for K > 16, one
  * object per lane on the matrix cores for 5 <= K <= 16 (M <= 27), the vector
  * ALU otherwise. Every path gives the same labels, centres and counts. */
@@ -163,8 +167,9 @@ int kmeans_diameter(const float *X, int64_t n, int32_t M, double *d2, int32_t *p
 /*
  * Assignment, Algorithm 1 steps 2 and 4, distance of Eq. (2):
  *   labels[i] = argmin_k |X_i - centers_k|^2  (lowest k on ties), int32 [n].
- * min_d2 (may be NULL) receives fp32 [n] squared distances to the chosen centre.
- * flags: KMEANS_PATH_* only. Asynchronous on `stream`.
+ * min_d2 (may be NULL) receives fp32 [n] squared distances to the chosen centre
+ * (with KMEANS_METRIC_L1: the labels are by the L1 distance and min_d2 holds it).
+ * flags: KMEANS_PATH_* or KMEANS_METRIC_L1. Asynchronous on `stream`.
  */
 int kmeans_assign(const float *X, int64_t n, int32_t M, const float *centers, int32_t K,
                   int32_t *labels, float *min_d2, uint32_t flags, void *stream);

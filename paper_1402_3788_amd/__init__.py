@@ -6,10 +6,10 @@ library's HIP kernels. Importing this module fails loudly if the library has
 not been built (python paper_1402_3788_amd/build.py).
 
 Entry points (same names as the C ABI):
-    kmeans_assign(X, centers, with_min_d2=False, path=None) -> labels [, min_d2]
+    kmeans_assign(X, centers, with_min_d2=False, path=None, metric="l2") -> labels [, min_d2]
     kmeans_update(X, labels, K, prev_centers, out=None) -> (centers, counts)
     kmeans_run(X, K, init_centers, max_iter, fixed_iters=False, path=None,
-               timing=False) -> (labels, centers, counts, iterations[, timing])
+               timing=False, metric="l2") -> (labels, centers, counts, iterations[, timing])
     kmeans_init_farthest(X, K, ws=None) -> (init_idx, centers)
     kmeans_centroid(X, ws=None) -> centroid
     kmeans_diameter(X, ws=None) -> (d2, pair, centroid)
@@ -36,6 +36,7 @@ KMEANS_FIXED_ITERS = 1 << 0
 KMEANS_PATH_DIRECT = 1 << 1
 KMEANS_PATH_MFMA = 1 << 2
 KMEANS_PATH_TILES = 1 << 3
+KMEANS_METRIC_L1 = 1 << 4
 
 EXPORTED = ("kmeans_workspace_bytes", "kmeans_strerror", "kmeans_assign", "kmeans_update",
             "kmeans_run", "kmeans_init_workspace_bytes", "kmeans_init_farthest",
@@ -117,6 +118,14 @@ def _check_x(X: torch.Tensor):
 
 def _dev_ptr(t):
     return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def _metric(metric):
+    if metric == "l2":
+        return 0
+    if metric == "l1":
+        return KMEANS_METRIC_L1
+    raise ValueError(f"unknown metric {metric!r}")
 
 
 def _flags(path):
@@ -208,8 +217,11 @@ def kmeans_diameter(X: torch.Tensor, ws: torch.Tensor | None = None):
     return d2, pair, c
 
 
-def kmeans_assign(X: torch.Tensor, centers: torch.Tensor, with_min_d2: bool = False, path=None):
-    """Algorithm 1 steps 2/4: labels[i] = nearest centre (lowest index on ties)."""
+def kmeans_assign(X: torch.Tensor, centers: torch.Tensor, with_min_d2: bool = False, path=None,
+                  metric: str = "l2"):
+    """Algorithm 1 steps 2/4: labels[i] = nearest centre (lowest index on ties),
+    by the squared Euclidean distance of Eq. (2) or, with metric="l1", by the
+    city-block distance (min_d2 then holds that distance)."""
     _check_x(X)
     n, M = X.shape
     C = centers.contiguous()
@@ -217,7 +229,7 @@ def kmeans_assign(X: torch.Tensor, centers: torch.Tensor, with_min_d2: bool = Fa
     labels = torch.empty(n, dtype=torch.int32, device=X.device)
     d2 = torch.empty(n, dtype=torch.float32, device=X.device) if with_min_d2 else None
     rc = _lib.kmeans_assign(_dev_ptr(X), n, M, _dev_ptr(C), K, _dev_ptr(labels), _dev_ptr(d2),
-                            _flags(path), _stream_ptr(X.device))
+                            _flags(path) | _metric(metric), _stream_ptr(X.device))
     if rc:
         raise KmeansError("kmeans_assign", rc)
     return (labels, d2) if with_min_d2 else labels
@@ -243,8 +255,10 @@ def kmeans_update(X: torch.Tensor, labels: torch.Tensor, K: int, prev_centers: t
 
 def kmeans_run(X: torch.Tensor, K: int, init_centers: torch.Tensor, max_iter: int,
                fixed_iters: bool = False, path=None, timing: bool = False,
-               out=None, ws: torch.Tensor | None = None, sample_every: int = 0):
-    """Algorithm 1 steps 2-7 from init_centers (synchronous).
+               out=None, ws: torch.Tensor | None = None, sample_every: int = 0,
+               metric: str = "l2"):
+    """Algorithm 1 steps 2-7 from init_centers (synchronous); metric="l1"
+    assigns by the city-block distance (the centres stay centres of gravity).
 
     Returns (labels, centers, counts, iterations), plus a KmeansTiming when
     timing=True (events around the whole call and around the assign launch of
@@ -260,7 +274,7 @@ def kmeans_run(X: torch.Tensor, K: int, init_centers: torch.Tensor, max_iter: in
         counts = torch.empty(K, dtype=torch.int32, device=X.device)
     else:
         labels, centers, counts = out
-    flags = _flags(path) | (KMEANS_FIXED_ITERS if fixed_iters else 0)
+    flags = _flags(path) | _metric(metric) | (KMEANS_FIXED_ITERS if fixed_iters else 0)
     if ws is None:
         ws = workspace(n, M, K, X.device, flags)
     iters = ctypes.c_int32(0)

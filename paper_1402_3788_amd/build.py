@@ -19,7 +19,7 @@ LIB = os.path.join(HERE, "libkmeans_mi355x.so")
 PARTS = 4
 SOURCES = ([("kmeans_api.hip", [], "kmeans_api.o"), ("lloyd_ctl.hip", [], "lloyd_ctl.o"),
             ("lloyd_centres.hip", [], "lloyd_centres.o"), ("farthest.hip", [], "farthest.o"),
-            ("diameter.hip", [], "diameter.o")]
+            ("diameter.hip", [], "diameter.o"), ("lloyd_l1.hip", [], "lloyd_l1.o")]
            + [(f, [f"-DLLOYD_PART={p}"], f.replace(".hip", f"_part{p}.o"))
               for f in ("lloyd_tile.hip", "lloyd_lane.hip") for p in range(PARTS)])
 ARCH = "gfx950"

@@ -3,6 +3,7 @@
 // steps 2-7. See include/kmeans.h.
 #include "../../include/kmeans.h"
 #include "lloyd.h"
+#include "lloyd_l1.h"
 
 #include <vector>
 
@@ -10,8 +11,8 @@ using namespace lloyd;
 
 namespace {
 
-constexpr uint32_t kKnownFlags =
-    KMEANS_FIXED_ITERS | KMEANS_PATH_DIRECT | KMEANS_PATH_MFMA | KMEANS_PATH_TILES;
+constexpr uint32_t kKnownFlags = KMEANS_FIXED_ITERS | KMEANS_PATH_DIRECT | KMEANS_PATH_MFMA |
+                                  KMEANS_PATH_TILES | KMEANS_METRIC_L1;
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
@@ -28,6 +29,7 @@ int check_flags(uint32_t flags)
     if (flags & ~kKnownFlags) return KMEANS_EINVAL;
     const uint32_t paths = flags & (KMEANS_PATH_DIRECT | KMEANS_PATH_MFMA | KMEANS_PATH_TILES);
     if (paths & (paths - 1)) return KMEANS_EINVAL;          // at most one path flag
+    if ((flags & KMEANS_METRIC_L1) && paths) return KMEANS_EINVAL;   // L1 has one form
     return KMEANS_OK;
 }
 
@@ -254,11 +256,16 @@ int kmeans_assign(const float *X, int64_t n, int32_t M, const float *centers, in
     if ((rc = check_flags(flags)) || (flags & KMEANS_FIXED_ITERS)) return rc ? rc : KMEANS_EINVAL;
     if (!aligned16(X)) return KMEANS_EINVAL;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if (select_path(M, K, flags) < 0) return KMEANS_EUNSUPPORTED;
-    const AccumPlan plan = plan_for(select_path(M, K, flags), n, M, K, kAssign);
     StepArgs a{};
     a.X = X; a.n = n; a.M = M; a.C = centers; a.K = K;
     a.labels = labels; a.min_d2 = min_d2;
+    if (flags & KMEANS_METRIC_L1) {
+        const L1Plan p1 = plan_l1(n, M, K);
+        if (p1.waves < 1) return KMEANS_EUNSUPPORTED;
+        return hip_status(launch_l1(a, p1, s));
+    }
+    if (select_path(M, K, flags) < 0) return KMEANS_EUNSUPPORTED;
+    const AccumPlan plan = plan_for(select_path(M, K, flags), n, M, K, kAssign);
     return hip_status(launch_step(a, kAssign, plan, s));
 }
 
@@ -303,6 +310,9 @@ int kmeans_run(const float *X, int64_t n, int32_t M, int32_t K, const float *ini
 
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int fixed = (flags & KMEANS_FIXED_ITERS) ? 1 : 0;
+    const bool l1 = (flags & KMEANS_METRIC_L1) != 0;
+    const L1Plan p1 = l1 ? plan_l1(n, M, K) : L1Plan{};
+    if (l1 && p1.waves < 1) return KMEANS_EUNSUPPORTED;
 
     StepArgs a{};
     a.X = X; a.n = n; a.M = M; a.C = centers; a.K = K;
@@ -312,6 +322,7 @@ int kmeans_run(const float *X, int64_t n, int32_t M, int32_t K, const float *ini
     bind_workspace(a, L, static_cast<char *>(workspace));
     a.fixed = fixed;
     a.compare = 1;
+    a.labels_in = labels;        // the L1 form accumulates from the labels it wrote
     Ctl *ctl = a.ctl;
 
     if ((rc = hip_status(launch_ctl_reset(ctl, s)))) return rc;
@@ -351,8 +362,15 @@ int kmeans_run(const float *X, int64_t n, int32_t M, int32_t K, const float *ini
             a.t = tt;
             const bool sampled = every > 0 && (tt - 1) % every == 0;
             if (sampled) rc = mark();
-            if (!rc) rc = hip_status(launch_step(a, kAssignAccum, L.plan, s));
-            if (!rc && sampled) rc = mark();
+            if (!rc && l1) {
+                // L1: assign, then the sums of Eq. (1) from those labels
+                rc = hip_status(launch_l1(a, p1, s));
+                if (!rc && sampled) rc = mark();
+                if (!rc) rc = hip_status(launch_step(a, kAccumLabels, L.plan, s));
+            } else if (!rc) {
+                rc = hip_status(launch_step(a, kAssignAccum, L.plan, s));
+                if (!rc && sampled) rc = mark();
+            }
             if (!rc) rc = hip_status(launch_centres(a, L.plan.groups, s));
             ++launched;
         }

@@ -43,7 +43,7 @@ def test_header_constants_match_binding():
         m = re.search(rf"#define {name}\s+(-?\d+)", text)
         assert int(m.group(1)) == getattr(km, name)
     for name in ["KMEANS_FIXED_ITERS", "KMEANS_PATH_DIRECT", "KMEANS_PATH_MFMA",
-                 "KMEANS_PATH_TILES"]:
+                 "KMEANS_PATH_TILES", "KMEANS_METRIC_L1"]:
         m = re.search(rf"#define {name}\s+\(1u << (\d+)\)", text)
         assert (1 << int(m.group(1))) == getattr(km, name)
 
@@ -62,6 +62,8 @@ def test_workspace_bytes():
     assert km.kmeans_workspace_bytes(10, 64, 257) == 0          # K*M > 16384
     assert km.kmeans_workspace_bytes(2**31, 4, 4) == 0
     assert km.kmeans_workspace_bytes(10, 4, 4, 1 << 9) == 0     # unknown flag
+    assert km.kmeans_workspace_bytes(10**6, 25, 16, km.KMEANS_METRIC_L1) > 0
+    assert km.kmeans_workspace_bytes(10, 4, 4, km.KMEANS_METRIC_L1 | km.KMEANS_PATH_MFMA) == 0
     # partials grow with K*M; the control block is always there
     assert km.kmeans_workspace_bytes(10**6, 25, 256) > km.kmeans_workspace_bytes(10**6, 25, 16)
     assert km.kmeans_workspace_bytes(1, 1, 1) >= 256
@@ -97,6 +99,9 @@ def _run(X=FAKE, n=100, M=4, K=3, init=FAKE, max_iter=5, flags=0, labels=FAKE, C
     (dict(flags=km.KMEANS_PATH_TILES | km.KMEANS_PATH_DIRECT), km.KMEANS_EINVAL),
     (dict(flags=km.KMEANS_PATH_TILES, M=16, K=1024), km.KMEANS_EUNSUPPORTED),
     (dict(flags=1 << 7), km.KMEANS_EINVAL),
+    (dict(flags=km.KMEANS_METRIC_L1 | km.KMEANS_PATH_MFMA), km.KMEANS_EINVAL),
+    (dict(flags=km.KMEANS_METRIC_L1 | km.KMEANS_PATH_DIRECT), km.KMEANS_EINVAL),
+    (dict(flags=km.KMEANS_METRIC_L1, M=65), km.KMEANS_EUNSUPPORTED),
 ])
 def test_assign_validation(kw, code):
     assert _assign(**kw) == code
@@ -124,6 +129,7 @@ def test_update_validation(kw, code):
     (dict(flags=km.KMEANS_PATH_MFMA | km.KMEANS_PATH_TILES), km.KMEANS_EINVAL),
     (dict(flags=km.KMEANS_PATH_TILES, M=16, K=1024, wsb=1 << 30), km.KMEANS_EUNSUPPORTED),
     (dict(flags=1 << 5), km.KMEANS_EINVAL), (dict(ws=None), km.KMEANS_EWORKSPACE),
+    (dict(flags=km.KMEANS_METRIC_L1 | km.KMEANS_PATH_TILES), km.KMEANS_EINVAL),
     (dict(wsb=16), km.KMEANS_EWORKSPACE),
 ])
 def test_run_validation(kw, code):
