@@ -377,7 +377,7 @@ def main():
         t = time.perf_counter()
         oracle.alg3_run(X, K, init, T, fixed=True)
         alg3_s = time.perf_counter() - t
-        result["cpu_alg3"] = {
+        result["cpu_baseline"]["alg3"] = {
             "value": round(T / alg3_s, 4),
             "unit": "iters/s",
             "cores": used,
