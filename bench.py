@@ -209,8 +209,8 @@ def main():
     args = _parse()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (got --gpus {args.gpus}); "
-              "the multi-GPU sharding of the Lloyd iteration is described in DESIGN.md "
-              "but not built", file=sys.stderr)
+              "sharding the Lloyd iteration over several GPUs (one all-gather of the fp64 "
+              "partial sums per iteration) is designed but not built", file=sys.stderr)
         sys.exit(2)
     if args.calibrate_copy:
         calibrate_copy()
