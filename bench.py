@@ -208,7 +208,7 @@ def time_diameter(torch, km, Xg, reps=2):
 def main():
     args = _parse()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (got --gpus {args.gpus}); "
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); "
               "sharding the Lloyd iteration over several GPUs (one all-gather of the fp64 "
               "partial sums per iteration) is designed but not built", file=sys.stderr)
         sys.exit(2)
