@@ -60,7 +60,7 @@ def _case(n, M, kind, seed, offset=0.0):
     (1000, 25, "blobs", 0.0), (5000, 25, "uniform", 0.0), (3000, 64, "blobs", 0.0),
     (4097, 33, "dups", 0.0), (8193, 10, "line", 0.0), (5000, 10, "blobs", 1000.0),
     (2500, 30, "uniform", 0.0), (2500, 31, "uniform", 0.0), (600, 1, "line", 0.0),
-    (20_000, 25, "blobs", 0.0),
+    (20_000, 25, "blobs", 0.0), (8192, 4, "uniform", 0.0), (1024, 2, "line", 0.0),
 ])
 def test_diameter_parity(n, M, kind, offset):
     X = _case(n, M, kind, seed=n + M, offset=offset)
