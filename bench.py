@@ -298,6 +298,17 @@ def main():
         },
     }
 
+    if key == "tiles":
+        # the 64-object-tile kernel is matrix-bound for large K: its first pass
+        # issues three bf16 products per 16 x 16 block of (object, centre) pairs
+        # over 32 ceil(M/32) features (tiles with a close call add fp32 products)
+        flops = 3 * 2 * (64 * -(-n // 64)) * (16 * -(-K // 16)) * (32 * -(-M // 32))
+        tf = flops / assign_avg_s / 1e12
+        result["roofline_mfma"] = {"bound": "mfma", "achieved": round(tf, 1),
+                                   "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                                   "frac": round(tf / BF16_PEAK_TFLOPS, 4),
+                                   "flops_per_launch": flops}
+
     # the paper's own stopping rule (centres congruent): end-to-end latency of
     # one synchronous call from the initial centres, host clock
     km.kmeans_run(Xg, K, Cg, w.max_iter, path=path, out=out, ws=ws)
