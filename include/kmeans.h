@@ -140,7 +140,7 @@ int kmeans_centroid(const float *X, int64_t n, int32_t M, float *centroid, void 
 
 /* Bytes of device workspace that kmeans_diameter needs: the centre of gravity
  * and its partials, four bf16 operand arrays of n * 32 ceil((M+2)/32) values
- * each (n rounded up to 8192), and 16 bytes per (512-object block, 8192-object
+ * each (n rounded up to 16384), and 16 bytes per (512-object block, 16384-object
  * chunk) pair. 0 for refused shapes (also when n needs more than 65535 column
  * chunks). Pure host computation. */
 size_t kmeans_diameter_workspace_bytes(int64_t n, int32_t M);

@@ -42,7 +42,7 @@
 // true pair has d~ >= D2 - B >= d~* - 2B, so it is always re-evaluated, and
 // the result is exact whatever the split products round to.
 //
-// Work: pass items are (row block of 512 objects, column chunk of 8192);
+// Work: pass items are (row block of 512 objects, column chunk of 16384);
 // items wholly below the diagonal return at once, and within the diagonal
 // chunk the column steps start at the row block. Each of 8 waves holds the A
 // operands of 64 rows in registers; the workgroup stages 64 columns of B at a
@@ -64,7 +64,7 @@ typedef float f4v __attribute__((ext_vector_type(4)));
 constexpr int kDiamWaves = 8;
 constexpr int kDiamThreads = kDiamWaves * kWave;
 constexpr int kRowBlock = kDiamWaves * 64;       // objects per item's row block
-constexpr int kChunkSteps = 128;                 // 64-column steps per item
+constexpr int kChunkSteps = 256;                 // 64-column steps per item
 constexpr int kChunk = kChunkSteps * 64;         // columns per item
 constexpr int kCentroidGroups = 256;
 

@@ -165,7 +165,7 @@ def test_centroid_and_diameter_workspace_bytes():
     assert km.kmeans_centroid_workspace_bytes(2_000_000, 25) > 0
     assert km.kmeans_centroid_workspace_bytes(0, 25) == 0
     assert km.kmeans_centroid_workspace_bytes(10, 65) == 0
-    # four bf16 operand arrays of 32 ceil((M+2)/32) values per object (n padded to 8192)
+    # four bf16 operand arrays of 32 ceil((M+2)/32) values per object (n padded to 16384)
     assert km.kmeans_diameter_workspace_bytes(2_000_000, 25) >= 4 * 2_000_000 * 32 * 2
     assert (km.kmeans_diameter_workspace_bytes(10_000, 40)
             > km.kmeans_diameter_workspace_bytes(10_000, 30))
