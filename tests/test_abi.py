@@ -205,6 +205,19 @@ def test_diameter_validation(kw, code):
     assert _diameter(**kw) == code
 
 
+def test_plain_c_client(tmp_path):
+    """The header compiles as C and a gcc-built client links against the
+    library and gets the documented results from the host-side paths."""
+    exe = tmp_path / "abi_client"
+    subprocess.check_call(["gcc", "-std=c99", "-Wall", "-Werror", "-I", os.path.join(ROOT, "include"),
+                           os.path.join(ROOT, "tests", "abi_client.c"), "-o", str(exe),
+                           "-L", os.path.dirname(km.LIB_PATH), "-lkmeans_mi355x",
+                           f"-Wl,-rpath,{os.path.dirname(km.LIB_PATH)}"])
+    r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert r.stdout.count("ok  ") == 18
+
+
 def test_run_null_iterations_pointer():
     it_null = ctypes.POINTER(ctypes.c_int32)()
     assert _run(iters=it_null) == km.KMEANS_EINVAL
