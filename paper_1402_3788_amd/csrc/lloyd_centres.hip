@@ -26,7 +26,12 @@ centres_kernel(const double *__restrict__ part_sums, const int32_t *__restrict__
                int G, int K, int M, const float *prev, float *centers, int32_t *counts, Ctl *ctl,
                int t, int fixed, int compare)
 {
-    if (stop_before(ctl, t, fixed)) return;
+    // Iterations past convergence: the assign launch of this iteration found
+    // the centres congruent and recorded converged_at (its first workgroup);
+    // that launch has finished, so the value is settled here. (The change
+    // flags are not read: workgroup 0 of this launch clears one of them.)
+    // The test waits until the loads below are in flight.
+    const bool skip = !fixed && ctl != nullptr && ctl->converged_at != 0;
     extern __shared__ __align__(16) unsigned char smem[];
     const int k = blockIdx.x;
     const int MW = M + 1;                       // M sums, then the count
@@ -35,6 +40,8 @@ centres_kernel(const double *__restrict__ part_sums, const int32_t *__restrict__
     double *sub = reinterpret_cast<double *>(smem);           // [MW][NG] group sums
     int32_t *s_changed = reinterpret_cast<int32_t *>(sub + (size_t)MW * NG);
 
+    // this workgroup's previous centre (threads 0 .. M-1; blockDim.x > M)
+    const float old = threadIdx.x < M ? prev[(int64_t)k * M + threadIdx.x] : 0.f;
     if (threadIdx.x == 0) *s_changed = 0;
     for (int it = threadIdx.x; it < MW * NG; it += blockDim.x) {
         const int e = it % MW, q = it / MW;
@@ -61,18 +68,18 @@ centres_kernel(const double *__restrict__ part_sums, const int32_t *__restrict__
         sub[e * NG + q] = s;
     }
     __syncthreads();
+    if (skip) return;                           // uniform: every thread read the same value
 
     int32_t c = 0;
     for (int q = 0; q < NG; ++q) c += (int32_t)sub[M * NG + q];
     int changed = 0;
-    for (int e = threadIdx.x; e < M; e += blockDim.x) {
+    if (threadIdx.x < M) {
+        const int e = threadIdx.x;
         double s = sub[e * NG];
         for (int q = 1; q < NG; ++q) s = s + sub[e * NG + q];
-        const int64_t idx = (int64_t)k * M + e;
-        const float old = prev[idx];
         const float nv = c > 0 ? (float)(s / (double)c) : old;
-        changed |= (__float_as_uint(nv) != __float_as_uint(old)) ? 1 : 0;
-        centers[idx] = nv;
+        changed = (__float_as_uint(nv) != __float_as_uint(old)) ? 1 : 0;
+        centers[(int64_t)k * M + e] = nv;
     }
     if (threadIdx.x == 0) counts[k] = c;
     if (changed) *s_changed = 1;
