@@ -287,10 +287,15 @@ def _stepwise_at_scale(name, T, sample=20_000):
     """Full-size check without the full oracle trajectory: the GPU's labels of
     pass T are compared with the oracle's assignment (to the GPU's own centres
     of pass T-1) on a seeded sample of objects, and the GPU's centres of pass T
-    with the oracle's Eq. (1) over all objects with the GPU's labels."""
+    with the oracle's Eq. (1) over all objects with the GPU's labels. The GPU's
+    farthest-point initial centres are compared with the stored ones."""
     w = workloads.get(name)
-    X, _, _, init = workloads.load(name)
+    X, _, init_idx, init = workloads.load(name)
     Xg, Cg = _gpu(X), _gpu(init)
+    # the initial centres at this size: the GPU traversal gives the stored ones
+    gidx, gC = km.kmeans_init_farthest(Xg, w.K)
+    assert np.array_equal(gidx.cpu().numpy(), init_idx)
+    assert np.array_equal(gC.cpu().numpy().view(np.uint32), init.view(np.uint32))
     _say(f"[scale] {w.name}: GPU {T - 1} and {T} fixed iterations")
     _, Cprev, _, _ = km.kmeans_run(Xg, w.K, Cg, T - 1, fixed_iters=True)
     lab, C, cnt, it = km.kmeans_run(Xg, w.K, Cg, T, fixed_iters=True)
