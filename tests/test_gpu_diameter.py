@@ -51,6 +51,13 @@ def check_centroid(c, X):
 def _case(n, M, kind, seed, offset=0.0):
     if kind == "same":
         return np.full((n, M), 2.5, np.float32)
+    if kind == "corners":
+        # the 2^M corners of a cube, shuffled and repeated: every antipodal
+        # pair of copies ties exactly at the maximum, across many work items
+        rng = np.random.default_rng(seed)
+        corners = ((np.arange(2 ** M)[:, None] >> np.arange(M)) & 1).astype(np.float32)
+        return np.ascontiguousarray(corners[rng.integers(0, 2 ** M, n)] * 3 - 1.5
+                                    + np.float32(offset))
     X, _ = workloads.random_case(n, M, 1, seed, kind)
     return (X + np.float32(offset)).astype(np.float32)
 
@@ -61,6 +68,7 @@ def _case(n, M, kind, seed, offset=0.0):
     (4097, 33, "dups", 0.0), (8193, 10, "line", 0.0), (5000, 10, "blobs", 1000.0),
     (2500, 30, "uniform", 0.0), (2500, 31, "uniform", 0.0), (600, 1, "line", 0.0),
     (20_000, 25, "blobs", 0.0), (8192, 4, "uniform", 0.0), (1024, 2, "line", 0.0),
+    (24_000, 3, "corners", 0.0), (20_000, 5, "corners", 7.0),
 ])
 def test_diameter_parity(n, M, kind, offset):
     X = _case(n, M, kind, seed=n + M, offset=offset)
