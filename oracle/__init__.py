@@ -56,6 +56,8 @@ def _bind(path: str):
     lib.oracle_sse.restype = ctypes.c_double
     lib.oracle_init_farthest.argtypes = [p, i64, i32, i32, p]
     lib.oracle_init_farthest.restype = ctypes.c_int
+    lib.oracle_init_farthest_from.argtypes = [p, i64, i32, i32, p, i32, p]
+    lib.oracle_init_farthest_from.restype = ctypes.c_int
     lib.oracle_centroid.argtypes = [p, i64, i32, p]
     lib.oracle_centroid.restype = ctypes.c_int
     lib.oracle_diameter.argtypes = [p, i64, i32, p, p, p]
@@ -185,6 +187,22 @@ def init_farthest(X, K: int):
     rc = _load().oracle_init_farthest(_ptr(X), n, M, int(K), _ptr(idx))
     if rc:
         raise ValueError(f"oracle_init_farthest failed ({rc})")
+    return idx
+
+
+def init_farthest_from(X, K: int, seeds):
+    """Farthest-point traversal from the given seed objects: idx[:S] = seeds,
+    then each next object is the not-yet-chosen one farthest (smallest squared
+    distance largest, lowest index on ties) from those chosen. Returns idx
+    (int32 [K]). Needs 1 <= S <= K <= n and seeds in [0, n)."""
+    X = _f32(X)
+    n, M = X.shape
+    seeds = np.ascontiguousarray(seeds, dtype=np.int32)
+    idx = np.empty(int(K), np.int32)
+    rc = _load().oracle_init_farthest_from(_ptr(X), n, M, int(K), _ptr(seeds), len(seeds),
+                                           _ptr(idx))
+    if rc:
+        raise ValueError(f"oracle_init_farthest_from failed ({rc})")
     return idx
 
 

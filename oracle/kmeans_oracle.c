@@ -363,3 +363,57 @@ int oracle_diameter(const float *X, int64_t n, int32_t M, double *d2, int32_t *k
     *l_out = (int32_t)bl;
     return 0;
 }
+
+/*
+ * Farthest-point traversal from S given seed objects (another reading of
+ * Algorithm 2 step 3, e.g. the two ends of the diameter of step 1):
+ *   idx[m] = seeds[m] for m < S (as given, repeats allowed);
+ *   idx[m] = the object not among idx[0..m-1] whose smallest squared distance
+ *            to idx[0..m-1] is largest, lowest index on ties, for S <= m < K.
+ * Requires 1 <= S <= K <= n and seeds in [0, n). With S = 1 and seed 0 it is
+ * oracle_init_farthest.
+ */
+int oracle_init_farthest_from(const float *X, int64_t n, int32_t M, int32_t K,
+                              const int32_t *seeds, int32_t S, int32_t *idx)
+{
+    if (!X || !idx || !seeds || n < 1 || M < 1 || K < 1 || (int64_t)K > n || S < 1 || S > K)
+        return ORACLE_EINVAL;
+    for (int32_t s = 0; s < S; ++s)
+        if (seeds[s] < 0 || (int64_t)seeds[s] >= n)
+            return ORACLE_EINVAL;
+    double *closest = (double *)malloc((size_t)n * sizeof(double));
+    unsigned char *taken = (unsigned char *)calloc((size_t)n, 1);
+    if (!closest || !taken) {
+        free(closest);
+        free(taken);
+        return ORACLE_ENOMEM;
+    }
+    for (int64_t obj = 0; obj < n; ++obj)
+        closest[obj] = INFINITY;
+    idx[0] = seeds[0];
+    taken[seeds[0]] = 1;
+    for (int32_t m = 1; m < K; ++m) {
+        const float *newest = X + (int64_t)idx[m - 1] * M;
+        for (int64_t obj = 0; obj < n; ++obj) {
+            double dd = sqdist(X + obj * (int64_t)M, newest, M);
+            if (dd < closest[obj])
+                closest[obj] = dd;
+        }
+        if (m < S) {
+            idx[m] = seeds[m];
+        } else {
+            int64_t pick = -1;
+            for (int64_t obj = 0; obj < n; ++obj) {
+                if (taken[obj])
+                    continue;
+                if (pick < 0 || closest[obj] > closest[pick])
+                    pick = obj;
+            }
+            idx[m] = (int32_t)pick;
+        }
+        taken[idx[m]] = 1;
+    }
+    free(closest);
+    free(taken);
+    return 0;
+}

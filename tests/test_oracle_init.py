@@ -19,12 +19,12 @@ import oracle
 import workloads
 
 
-def _exact_farthest(X, K):
+def _exact_farthest(X, K, seeds=(0,)):
     """The rule written out in exact arithmetic: fp32 inputs are dyadic
     rationals, so Fractions give the exact squared distances."""
     Xf = [[Fraction(float(v)) for v in row] for row in X]
     n = len(Xf)
-    chosen = [0]
+    chosen = list(seeds)
     while len(chosen) < K:
         best, far = None, None
         for i in range(n):
@@ -120,3 +120,31 @@ def test_stored_workload_init_matches(name):
     numpy recipe) are the oracle's."""
     X, _, idx, _ = workloads.load(name)
     assert np.array_equal(oracle.init_farthest(X, workloads.get(name).K), idx)
+
+
+@pytest.mark.parametrize("n,M,K,seeds,seed", [(12, 2, 5, (3, 7), 0), (20, 3, 20, (19, 0, 5), 1),
+                                              (15, 1, 7, (4,), 2), (30, 4, 9, (2, 2), 3)])
+def test_from_seeds_matches_exact_rule(n, M, K, seeds, seed):
+    X = np.random.default_rng(seed).integers(-2, 3, (n, M)).astype(np.float32)
+    want = _exact_farthest(X, K, seeds)
+    assert oracle.init_farthest_from(X, K, seeds).tolist() == want
+
+
+def test_from_seed_zero_is_the_plain_traversal():
+    X, _ = workloads.random_case(3000, 6, 1, 5, "blobs")
+    assert np.array_equal(oracle.init_farthest_from(X, 40, [0]), oracle.init_farthest(X, 40))
+
+
+def test_from_the_diameter_ends():
+    X, _ = workloads.random_case(800, 3, 1, 6, "uniform")
+    _, k, l = oracle.diameter(X)
+    idx = oracle.init_farthest_from(X, 10, [k, l])
+    assert idx[:2].tolist() == [k, l]
+    assert idx.tolist() == _exact_farthest(X[:800], 10, (k, l))
+
+
+def test_from_seeds_rejects_bad_seeds():
+    X = np.zeros((5, 2), np.float32)
+    for seeds, K in (([5], 2), ([-1], 2), ([0, 1, 2], 2)):
+        with pytest.raises(ValueError):
+            oracle.init_farthest_from(X, K, seeds)

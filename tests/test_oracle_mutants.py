@@ -80,6 +80,11 @@ INIT_MUTANTS = {
                             "                nearest[i] = d;"),
     "init_starts_at_last_object": ("idx[0] = 0;\n    chosen[0] = 1;",
                                    "idx[0] = (int32_t)(n - 1);\n    chosen[n - 1] = 1;"),
+    "from_ties_to_highest_index": ("closest[obj] > closest[pick]", "closest[obj] >= closest[pick]"),
+    "from_second_seed_ignored": ("if (m < S) {\n            idx[m] = seeds[m];",
+                                 "if (m < 1) {\n            idx[m] = seeds[m];"),
+    "from_taken_not_excluded": ("if (taken[obj])\n                    continue;",
+                                "if (0 && taken[obj])\n                    continue;"),
     "init_drops_last_feature": ("double d = sqdist(X + i * (int64_t)M, c, M);",
                                 "double d = sqdist(X + i * (int64_t)M, c, M > 1 ? M - 1 : M);"),
 }
