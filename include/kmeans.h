@@ -125,6 +125,23 @@ size_t kmeans_init_workspace_bytes(int64_t n, int32_t M, int32_t K);
 int kmeans_init_farthest(const float *X, int64_t n, int32_t M, int32_t K, int32_t *init_idx,
                          float *centers, void *workspace, size_t workspace_bytes, void *stream);
 
+/*
+ * The same traversal from nseeds given seed objects (another reading of
+ * Algorithm 2 step 3, e.g. the two ends of the diameter that kmeans_diameter
+ * leaves in device memory):
+ *   init_idx[m] = seeds[m] for m < nseeds (as given; repeats allowed);
+ *   init_idx[m] = the object not among init_idx[0..m-1] farthest from them
+ *                 (as above), for nseeds <= m < K.
+ * seeds is an int32 [nseeds] DEVICE array read by the kernels (a seed outside
+ * [0, n) is taken as object 0); 1 <= nseeds <= K <= n, else KMEANS_EINVAL.
+ * Workspace as kmeans_init_workspace_bytes. kmeans_init_farthest is this call
+ * with the one seed 0. Asynchronous on `stream`.
+ */
+int kmeans_init_farthest_from(const float *X, int64_t n, int32_t M, int32_t K,
+                              const int32_t *seeds, int32_t nseeds, int32_t *init_idx,
+                              float *centers, void *workspace, size_t workspace_bytes,
+                              void *stream);
+
 /* Bytes of device workspace that kmeans_centroid needs (one fp64 row of
  * partial sums per workgroup, a few KB). 0 for refused shapes. Pure host. */
 size_t kmeans_centroid_workspace_bytes(int64_t n, int32_t M);

@@ -40,6 +40,7 @@ KMEANS_METRIC_L1 = 1 << 4
 
 EXPORTED = ("kmeans_workspace_bytes", "kmeans_strerror", "kmeans_assign", "kmeans_update",
             "kmeans_run", "kmeans_init_workspace_bytes", "kmeans_init_farthest",
+            "kmeans_init_farthest_from",
             "kmeans_centroid_workspace_bytes", "kmeans_centroid",
             "kmeans_diameter_workspace_bytes", "kmeans_diameter")
 
@@ -77,6 +78,8 @@ def _load() -> ctypes.CDLL:
     lib.kmeans_init_workspace_bytes.restype = sz
     lib.kmeans_init_farthest.argtypes = [p, i64, i32, i32, p, p, p, sz, p]
     lib.kmeans_init_farthest.restype = ctypes.c_int
+    lib.kmeans_init_farthest_from.argtypes = [p, i64, i32, i32, p, i32, p, p, p, sz, p]
+    lib.kmeans_init_farthest_from.restype = ctypes.c_int
     lib.kmeans_centroid_workspace_bytes.argtypes = [i64, i32]
     lib.kmeans_centroid_workspace_bytes.restype = sz
     lib.kmeans_centroid.argtypes = [p, i64, i32, p, p, sz, p]
@@ -147,8 +150,10 @@ def workspace(n: int, M: int, K: int, device, flags: int = 0) -> torch.Tensor:
     return torch.empty(nbytes, dtype=torch.uint8, device=device)
 
 
-def kmeans_init_farthest(X: torch.Tensor, K: int, ws: torch.Tensor | None = None, out=None):
-    """Algorithm 1 step 1 as farthest-point traversal from object 0.
+def kmeans_init_farthest(X: torch.Tensor, K: int, ws: torch.Tensor | None = None, out=None,
+                         seeds: torch.Tensor | None = None):
+    """Algorithm 1 step 1 as farthest-point traversal from object 0, or from
+    `seeds` (int32 device tensor, e.g. the diameter's pair).
 
     Returns (init_idx int32 [K], centers float32 [K, M]) on X's device;
     asynchronous on the current stream. `out` may supply both tensors."""
@@ -164,8 +169,17 @@ def kmeans_init_farthest(X: torch.Tensor, K: int, ws: torch.Tensor | None = None
         if nbytes == 0:
             raise KmeansError("kmeans_init_workspace_bytes", KMEANS_EINVAL)
         ws = torch.empty(nbytes, dtype=torch.uint8, device=X.device)
-    rc = _lib.kmeans_init_farthest(_dev_ptr(X), n, M, int(K), _dev_ptr(idx), _dev_ptr(centers),
-                                   _dev_ptr(ws), ws.numel(), _stream_ptr(X.device))
+    if seeds is None:
+        rc = _lib.kmeans_init_farthest(_dev_ptr(X), n, M, int(K), _dev_ptr(idx),
+                                       _dev_ptr(centers), _dev_ptr(ws), ws.numel(),
+                                       _stream_ptr(X.device))
+    else:
+        if not (seeds.is_cuda and seeds.dtype == torch.int32 and seeds.dim() == 1):
+            raise ValueError("seeds must be an int32 [S] tensor on a GPU")
+        seeds = seeds.contiguous()
+        rc = _lib.kmeans_init_farthest_from(_dev_ptr(X), n, M, int(K), _dev_ptr(seeds),
+                                            seeds.numel(), _dev_ptr(idx), _dev_ptr(centers),
+                                            _dev_ptr(ws), ws.numel(), _stream_ptr(X.device))
     if rc:
         raise KmeansError("kmeans_init_farthest", rc)
     return idx, centers

@@ -52,6 +52,7 @@
 // registers while the current step is computed, and written to the other of
 // two LDS buffers after it: one barrier per step.
 #include "lloyd_device.h"
+#include "diameter.h"
 
 #include <climits>
 

@@ -22,11 +22,16 @@
 // A last one-workgroup launch (p = K) only records idx[K-1]. With K = 1 that
 // launch is the only one and records object 0.
 //
+// The traversal may also start from S given seed objects (device array, e.g.
+// the two ends of the diameter): passes p <= S take seed p-1 as the newest
+// centre instead of the previous pass's farthest object.
+//
 // Streaming follows the distance kernels: 64-object tiles, each wave's next
 // tile in flight in registers while the current one is read from its LDS slot,
 // the ragged last tile handled after the loop by the one wave whose sequence
 // reaches it.
 #include "lloyd_device.h"
+#include "farthest.h"
 
 #include <array>
 #include <climits>
@@ -75,7 +80,8 @@ __global__ void __launch_bounds__(kFarMaxWaves * kWave)
 farthest_pass_kernel(const float *__restrict__ X, int64_t n, int K, int p,
                      double *__restrict__ nearest, double *__restrict__ cand_v,
                      int32_t *__restrict__ cand_i, int groups, int32_t *__restrict__ idx_out,
-                     float *__restrict__ centers_out)
+                     float *__restrict__ centers_out, const int32_t *__restrict__ seeds,
+                     int nseeds)
 {
     using G = TileGeom<M>;
     constexpr int V = G::kVecPerLane;
@@ -85,9 +91,15 @@ farthest_pass_kernel(const float *__restrict__ X, int64_t n, int K, int p,
     __shared__ double cd[M];                  // the newest centre, in fp64
     const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave, W = blockDim.x / kWave;
 
-    // the newest centre
+    // the newest centre: a seed (object 0 without seeds), or the farthest
+    // object of the previous pass
     int c = 0;
-    if (p > 1) {
+    if (p <= nseeds) {
+        if (seeds != nullptr) {
+            c = seeds[p - 1];
+            if (c < 0 || (int64_t)c >= n) c = 0;          // documented: outside [0, n) reads as 0
+        }
+    } else {
         const int half = ((p - 1) & 1) * groups;
         double v = -INFINITY;
         int i = INT_MAX;
@@ -171,7 +183,8 @@ hipError_t farthest_m(const FarthestArgs &a, const FarthestPlan &pl, hipStream_t
     for (int p = 1; p <= a.K; ++p) {
         const dim3 grid(p < a.K ? pl.groups : 1), block(pl.waves * kWave);
         hipLaunchKernelGGL(kern, grid, block, pl.lds_bytes, s, a.X, a.n, a.K, p, a.nearest,
-                           a.cand_v, a.cand_i, pl.groups, a.idx, a.centers);
+                           a.cand_v, a.cand_i, pl.groups, a.idx, a.centers, a.seeds,
+                           a.nseeds);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -207,7 +220,9 @@ FarthestPlan plan_farthest(int64_t n, int M)
 hipError_t launch_farthest(const FarthestArgs &a, const FarthestPlan &pl, hipStream_t s)
 {
     static constexpr auto table = far_table(std::make_integer_sequence<int, kMaxM>{});
-    if (a.M < 1 || a.M > kMaxM || a.K < 1 || (int64_t)a.K > a.n) return hipErrorInvalidValue;
+    if (a.M < 1 || a.M > kMaxM || a.K < 1 || (int64_t)a.K > a.n || a.nseeds < 1 ||
+        a.nseeds > a.K || (a.seeds == nullptr && a.nseeds != 1))
+        return hipErrorInvalidValue;
     return table[a.M - 1](a, pl, s);
 }
 

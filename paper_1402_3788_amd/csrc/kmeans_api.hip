@@ -4,6 +4,8 @@
 #include "../../include/kmeans.h"
 #include "lloyd.h"
 #include "lloyd_l1.h"
+#include "farthest.h"
+#include "diameter.h"
 
 #include <vector>
 
@@ -174,7 +176,17 @@ size_t kmeans_init_workspace_bytes(int64_t n, int32_t M, int32_t K)
 int kmeans_init_farthest(const float *X, int64_t n, int32_t M, int32_t K, int32_t *init_idx,
                          float *centers, void *workspace, size_t workspace_bytes, void *stream)
 {
+    return kmeans_init_farthest_from(X, n, M, K, nullptr, 1, init_idx, centers, workspace,
+                                     workspace_bytes, stream);
+}
+
+int kmeans_init_farthest_from(const float *X, int64_t n, int32_t M, int32_t K,
+                              const int32_t *seeds, int32_t nseeds, int32_t *init_idx,
+                              float *centers, void *workspace, size_t workspace_bytes,
+                              void *stream)
+{
     if (!X || !init_idx || !centers) return KMEANS_EINVAL;
+    if (nseeds < 1 || nseeds > K || (!seeds && nseeds != 1)) return KMEANS_EINVAL;
     int rc = check_shape(n, M, K);
     if (rc) return rc;
     if ((int64_t)K > n || !aligned16(X)) return KMEANS_EINVAL;
@@ -188,6 +200,8 @@ int kmeans_init_farthest(const float *X, int64_t n, int32_t M, int32_t K, int32_
     a.cand_i = reinterpret_cast<int32_t *>(ws + L.cand_i_off);
     a.idx = init_idx;
     a.centers = centers;
+    a.seeds = seeds;
+    a.nseeds = nseeds;
     return hip_status(launch_farthest(a, L.plan, static_cast<hipStream_t>(stream)));
 }
 

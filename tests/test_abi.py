@@ -161,6 +161,16 @@ def test_init_validation(kw, code):
     assert _init(**kw) == code
 
 
+@pytest.mark.parametrize("seeds,nseeds,K,code", [
+    (None, 2, 3, km.KMEANS_EINVAL), (FAKE, 0, 3, km.KMEANS_EINVAL), (FAKE, 4, 3, km.KMEANS_EINVAL),
+    (FAKE, 2, 101, km.KMEANS_EINVAL),
+])
+def test_init_from_validation(seeds, nseeds, K, code):
+    wsb = km.kmeans_init_workspace_bytes(100, 4, 3)
+    assert km._lib.kmeans_init_farthest_from(FAKE, 100, 4, K, seeds, nseeds, FAKE, FAKE, FAKE,
+                                             wsb, None) == code
+
+
 def test_centroid_and_diameter_workspace_bytes():
     assert km.kmeans_centroid_workspace_bytes(2_000_000, 25) > 0
     assert km.kmeans_centroid_workspace_bytes(0, 25) == 0

@@ -87,3 +87,31 @@ def test_init_workload_full_size(name):
     assert np.array_equal(C.cpu().numpy().view(np.uint32), X[stored].view(np.uint32))
     if w.K <= 16:
         assert np.array_equal(idx, oracle.init_farthest(X, w.K))
+
+
+@pytest.mark.parametrize("n,M,K,seeds,kind", [(1000, 3, 10, (999, 0), "uniform"),
+                                              (70_001, 25, 16, (5, 5, 70_000), "dups"),
+                                              (4097, 7, 33, (17,), "blobs"),
+                                              (64, 2, 64, (63, 1, 2, 3), "uniform")])
+def test_init_from_seeds_parity(n, M, K, seeds, kind):
+    X = _case(n, M, kind, seed=n + K)
+    _say(f"[init from seeds] n={n} M={M} K={K} seeds={seeds}")
+    s = torch.tensor(seeds, dtype=torch.int32, device=DEV)
+    idx, C = km.kmeans_init_farthest(torch.from_numpy(X).to(DEV), K, seeds=s)
+    torch.cuda.synchronize()
+    want = oracle.init_farthest_from(X, K, list(seeds))
+    assert np.array_equal(idx.cpu().numpy(), want)
+    assert np.array_equal(C.cpu().numpy().view(np.uint32), X[want].view(np.uint32))
+
+
+@pytest.mark.parametrize("n,M,K", [(20_000, 25, 16), (5_000, 3, 40)])
+def test_init_from_the_diameter_on_the_device(n, M, K):
+    """Algorithm 2 steps 1 and 3 composed on the device: the diameter's pair,
+    left in device memory by kmeans_diameter, seeds the traversal."""
+    X = _case(n, M, "blobs", seed=n)
+    Xd = torch.from_numpy(X).to(DEV)
+    _, pair, _ = km.kmeans_diameter(Xd)
+    idx, _ = km.kmeans_init_farthest(Xd, K, seeds=pair)
+    torch.cuda.synchronize()
+    _, k, l = oracle.diameter(X)
+    assert np.array_equal(idx.cpu().numpy(), oracle.init_farthest_from(X, K, [k, l]))
