@@ -33,6 +33,7 @@ import hashlib
 import json
 import os
 import re
+import statistics
 import sys
 import time
 
@@ -43,13 +44,28 @@ HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, vendor peak
 PROFILES = os.path.join(ROOT, "profiles")
 CSRC = os.path.join(ROOT, "paper_1402_3788_amd", "csrc")
 METRIC = "Lloyd iters/sec and points·iters/sec at n=2e6,M=25,K=16; % of HBM peak"
+PROTOCOL_RUNS = 10          # calls timed with events after the timed region
+PROTOCOL_ITERS = 100        # iterations per such call (iteration time)
+PROTOCOL_KERNEL_ITERS = 20  # iterations per call with every assign launch timed
+
+# arithmetic of the distance step on each path (the sums are fp64 on all)
+DTYPE = {"lane-mfma": "bf16x3-split/f32-acc, f64 re-decision", "tiles": "bf16x3-split/f32-acc, f64 re-decision",
+         "direct": "f32, f64 re-decision"}
+DISTANCE = {
+    "lane-mfma": "expanded form on the bf16 matrix cores: operands split into bf16 hi and lo, "
+                 "three products per block, fp32 accumulation; close calls re-decided in fp64",
+    "tiles": "expanded form on the bf16 matrix cores: operands split into bf16 hi and lo, "
+             "three products per block, fp32 accumulation; close tiles recomputed with fp32 "
+             "products, the closest calls re-decided in fp64",
+    "direct": "direct form in fp32 on the vector ALU; close calls re-decided in fp64",
+}
 
 # kernel that does the work of a step on each distance path, and the sources
 # it is built from (a committed counter summary is used only while they match)
 KERNELS = {
-    "lane-mfma": ("lloyd_lane_kernel<M, assign+accumulate, dist=mfma, split bf16 products>",
-                  ["lloyd_lane.hip", "lloyd_device.h", "lloyd.h"]),
-    "direct": ("lloyd_lane_kernel<M, assign+accumulate, dist=valu>",
+    "lane-mfma": ("lane_mfma_kernel<M, assign+accumulate> (split bf16 products)",
+                  ["lloyd_lane_mfma.hip", "lloyd_device.h", "lloyd.h"]),
+    "direct": ("lloyd_lane_kernel<M, assign+accumulate, P>",
                ["lloyd_lane.hip", "lloyd_device.h", "lloyd.h"]),
     "tiles": ("lloyd_tile_kernel<M, assign+accumulate, acc>",
               ["lloyd_tile.hip", "lloyd_device.h", "lloyd.h"]),
@@ -74,7 +90,7 @@ def _parse():
 
 def kernel_key(M: int, K: int, path: str) -> str:
     """Which kernel runs the iteration (mirrors the library's path choice)."""
-    lane_fits = K <= 16 and M <= 27
+    lane_fits = K <= 16 and M <= 32
     if path == "direct":
         return "direct"
     if path == "tiles":
@@ -135,6 +151,20 @@ def copy_bandwidth(torch, nbytes=1 << 30, reps=20):
     sec = s.elapsed_time(e) / 1e3 / reps
     del src, dst
     return 2 * nbytes / sec / 1e9
+
+
+def host_info() -> dict:
+    """CPU model and logical CPU count of the host this runs on."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"cpu_model": model, "nproc": os.cpu_count()}
 
 
 def init_bytes(n: int, M: int, K: int) -> int:
@@ -240,24 +270,43 @@ def main():
     km.kmeans_run(Xg, K, Cg, max(1, args.warmup), fixed_iters=True, path=path, out=out, ws=ws)
     torch.cuda.synchronize()
 
-    # timed region: exactly `steps` Lloyd iterations in one fixed-count run;
-    # the library records HIP events on the launch stream around the whole run
-    # and around the assign + accumulate launch of every 16th iteration (an
-    # event between launches costs the stream microseconds, so few are taken)
+    # timed region: exactly `steps` Lloyd iterations in one fixed-count call,
+    # host clock, bracketed by device synchronisation; no events inside it
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    _, _, _, iters, tm = km.kmeans_run(Xg, K, Cg, args.steps, fixed_iters=True, path=path,
-                                       timing=True, out=out, ws=ws)
+    _, _, _, iters = km.kmeans_run(Xg, K, Cg, args.steps, fixed_iters=True, path=path,
+                                   out=out, ws=ws)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     assert iters == args.steps
     sec = t1 - t0
     iters_per_s = args.steps / sec
+    fallbacks = km.ctl_fallbacks(ws)
+    reruns = km.ctl_reruns(ws)
     bytes_per_point = 4 * M + 4                    # read the object once, write its label
     launch_bytes = n * bytes_per_point
-    step_avg_s = tm.step_ms / 1e3 / tm.step_launches          # whole iteration
-    assign_avg_s = tm.assign_ms / 1e3 / tm.assign_samples     # the streaming launch alone
-    achieved = launch_bytes / assign_avg_s / 1e9
+
+    # kernel and iteration times from HIP events recorded by the library on
+    # the launch stream: PROTOCOL_RUNS further fixed-count calls of
+    # PROTOCOL_ITERS iterations, events around every call and around every
+    # assign + accumulate launch; medians over the calls
+    it_us, k_us = [], []
+    nsamp = 0
+    for _ in range(PROTOCOL_RUNS):
+        # events only around the call (and the first launch): iteration time
+        _, _, _, _, tm = km.kmeans_run(Xg, K, Cg, PROTOCOL_ITERS, fixed_iters=True, path=path,
+                                       timing=True, sample_every=PROTOCOL_ITERS + 1, out=out,
+                                       ws=ws)
+        it_us.append(tm.step_ms * 1e3 / tm.step_launches)
+    for _ in range(PROTOCOL_RUNS):
+        # events around every assign + accumulate launch: the kernel's duration
+        _, _, _, _, tm = km.kmeans_run(Xg, K, Cg, PROTOCOL_KERNEL_ITERS, fixed_iters=True,
+                                       path=path, timing=True, sample_every=1, out=out, ws=ws)
+        k_us.append(tm.assign_ms * 1e3 / tm.assign_samples)
+        nsamp += tm.assign_samples
+    iteration_us = statistics.median(it_us)
+    assign_us = statistics.median(k_us)
+    achieved = launch_bytes / (assign_us * 1e-6) / 1e9
     traffic = _traffic(key, w.name)
 
     result = {
@@ -271,21 +320,30 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": DTYPE.get(key, "f32"),
         "data": "synthetic",
         "config": {"workload": w.name, "n": n, "M": M, "K": K, "mode": "fixed iterations",
-                   "accumulation": "f64", "path": args.path},
+                   "distance": DISTANCE.get(key), "accumulation": "f64 sums in a fixed order",
+                   "path": args.path},
         "points_iters_per_s": round(iters_per_s * n, 1),
         "algorithmic_GBps_whole_step": round(launch_bytes * iters_per_s / 1e9, 1),
         "pct_hbm_peak_whole_step": round(100 * launch_bytes * iters_per_s / 1e9 / HBM_PEAK_GBPS, 2),
-        "kernel_avg_us": round(assign_avg_s * 1e6, 3),
-        "iteration_avg_us": round(step_avg_s * 1e6, 3),
-        "assign_launches_timed": tm.assign_samples,
+        # the protocol runs (events on the launch stream, medians over the calls)
+        "protocol": {"calls": PROTOCOL_RUNS, "iterations_per_call": PROTOCOL_ITERS,
+                     "kernel_calls": PROTOCOL_RUNS,
+                     "kernel_iterations_per_call": PROTOCOL_KERNEL_ITERS,
+                     "iteration_median_us": round(iteration_us, 3),
+                     "iteration_min_us": round(min(it_us), 3),
+                     "iteration_max_us": round(max(it_us), 3),
+                     "assign_launch_median_us": round(assign_us, 3),
+                     "assign_launches_timed": nsamp},
+        "kernel_avg_us": round(assign_us, 3),
+        "iteration_avg_us": round(iteration_us, 3),
         # close calls of the timed run, per iteration: 64-object tiles whose
         # split-precision scores were recomputed with fp32 products (tile
         # kernel), objects re-decided in fp64 (both kernels)
-        "reruns_per_iteration": round(km.ctl_reruns(ws) / args.steps, 2),
-        "fallbacks_per_iteration": round(km.ctl_fallbacks(ws) / args.steps, 2),
+        "reruns_per_iteration": round(reruns / args.steps, 2),
+        "fallbacks_per_iteration": round(fallbacks / args.steps, 2),
         "roofline": {
             "bound": "hbm",
             "achieved": round(achieved, 1),
@@ -295,6 +353,7 @@ def main():
             "traffic": traffic,
             "kernel": KERNELS[key][0].replace("<M,", f"<{M},"),
             "bytes_per_launch": launch_bytes,
+            "launch_us": round(assign_us, 3),
         },
     }
 
@@ -303,7 +362,7 @@ def main():
         # issues three bf16 products per 16 x 16 block of (object, centre) pairs
         # over 32 ceil(M/32) features (tiles with a close call add fp32 products)
         flops = 3 * 2 * (64 * -(-n // 64)) * (16 * -(-K // 16)) * (32 * -(-M // 32))
-        tf = flops / assign_avg_s / 1e12
+        tf = flops / (assign_us * 1e-6) / 1e12
         result["roofline_mfma"] = {"bound": "mfma", "achieved": round(tf, 1),
                                    "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                                    "frac": round(tf / BF16_PEAK_TFLOPS, 4),
@@ -364,20 +423,32 @@ def main():
 
     if not args.no_cpu_baseline:
         import oracle
-        t = time.perf_counter()
-        oracle.run(X, K, init, 1, fixed=True)
-        one = time.perf_counter() - t
-        T = int(max(1, min(20, 15.0 // max(one, 1e-3))))
-        t = time.perf_counter()
-        oracle.run(X, K, init, T, fixed=True)
-        cpu_s = time.perf_counter() - t
+        host = host_info()
+        # the oracle is single-threaded; pin this process to one core while it
+        # runs (in-process, no re-launch), then restore the affinity
+        allowed = os.sched_getaffinity(0)
+        core = min(allowed)
+        os.sched_setaffinity(0, {core})
+        try:
+            t = time.perf_counter()
+            oracle.run(X, K, init, 1, fixed=True)
+            one = time.perf_counter() - t
+            T = int(max(1, min(20, 15.0 // max(one, 1e-3))))
+            t = time.perf_counter()
+            oracle.run(X, K, init, T, fixed=True)
+            cpu_s = time.perf_counter() - t
+        finally:
+            os.sched_setaffinity(0, allowed)
         result["cpu_baseline"] = {
             "value": round(T / cpu_s, 4),
             "unit": "iters/s",
             "cores": 1,
             "kind": "oracle",
             "sample": f"{T} fixed Lloyd iterations over all {n} objects of the same workload "
-                      "(single-threaded C, fp64)",
+                      f"(single-threaded C, fp64), pinned to core {core}",
+            "cpu_model": host["cpu_model"],
+            "nproc": host["nproc"],
+            "cores_available": len(allowed),
         }
         # the paper's multi-threaded CPU regime (Algorithm 3) on every host
         # thread OpenMP offers: a second baseline, not the oracle

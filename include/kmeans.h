@@ -58,7 +58,7 @@ extern "C" {
 #define KMEANS_FIXED_ITERS  (1u << 0) /* kmeans_run: run exactly max_iter iterations, no early stop */
 #define KMEANS_PATH_DIRECT  (1u << 1) /* force the vector-ALU distance path                          */
 #define KMEANS_PATH_MFMA    (1u << 2) /* force a matrix-core (expanded-form) distance path: one      */
-                                      /* object per lane for K <= 16 and M <= 27, else 64-object      */
+                                      /* object per lane for K <= 16 and M <= 32, else 64-object      */
                                       /* tiles; KMEANS_EUNSUPPORTED when the tiles' per-workgroup     */
                                       /* state (centre operands, fp64 sums) does not fit in LDS       */
 #define KMEANS_PATH_TILES   (1u << 3) /* force the 64-object-tile matrix-core path (any K)           */
@@ -66,8 +66,12 @@ extern "C" {
                                       /* instead of Eq. (2) -- the paper allows another metric; the   */
                                       /* centres stay the centres of gravity of Eq. (1). One form (one */
                                       /* object per lane on the vector ALU): no path flag with it.     */
+#define KMEANS_FORCE_FP64   (1u << 5) /* decide every label from fp64 distances in the fixed          */
+                                      /* operation order (the path every close call takes anyway),    */
+                                      /* skipping the faster screening: slower, same results; for     */
+                                      /* checking that the screening changes no label.                 */
 /* Without a path flag: 64-object tiles on the matrix cores for K > 16, one
- * object per lane on the matrix cores for 5 <= K <= 16 (M <= 27), the vector
+ * object per lane on the matrix cores for 5 <= K <= 16 (M <= 32), the vector
  * ALU otherwise. Every path gives the same labels, centres and counts. */
 
 /* Optional per-call timing for kmeans_run (pass NULL for none). Each

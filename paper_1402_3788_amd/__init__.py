@@ -37,6 +37,7 @@ KMEANS_PATH_DIRECT = 1 << 1
 KMEANS_PATH_MFMA = 1 << 2
 KMEANS_PATH_TILES = 1 << 3
 KMEANS_METRIC_L1 = 1 << 4
+KMEANS_FORCE_FP64 = 1 << 5
 
 EXPORTED = ("kmeans_workspace_bytes", "kmeans_strerror", "kmeans_assign", "kmeans_update",
             "kmeans_run", "kmeans_init_workspace_bytes", "kmeans_init_farthest",
@@ -232,7 +233,7 @@ def kmeans_diameter(X: torch.Tensor, ws: torch.Tensor | None = None):
 
 
 def kmeans_assign(X: torch.Tensor, centers: torch.Tensor, with_min_d2: bool = False, path=None,
-                  metric: str = "l2"):
+                  metric: str = "l2", force_fp64: bool = False):
     """Algorithm 1 steps 2/4: labels[i] = nearest centre (lowest index on ties),
     by the squared Euclidean distance of Eq. (2) or, with metric="l1", by the
     city-block distance (min_d2 then holds that distance)."""
@@ -242,8 +243,9 @@ def kmeans_assign(X: torch.Tensor, centers: torch.Tensor, with_min_d2: bool = Fa
     K = C.shape[0]
     labels = torch.empty(n, dtype=torch.int32, device=X.device)
     d2 = torch.empty(n, dtype=torch.float32, device=X.device) if with_min_d2 else None
+    flags = _flags(path) | _metric(metric) | (KMEANS_FORCE_FP64 if force_fp64 else 0)
     rc = _lib.kmeans_assign(_dev_ptr(X), n, M, _dev_ptr(C), K, _dev_ptr(labels), _dev_ptr(d2),
-                            _flags(path) | _metric(metric), _stream_ptr(X.device))
+                            flags, _stream_ptr(X.device))
     if rc:
         raise KmeansError("kmeans_assign", rc)
     return (labels, d2) if with_min_d2 else labels
@@ -270,7 +272,7 @@ def kmeans_update(X: torch.Tensor, labels: torch.Tensor, K: int, prev_centers: t
 def kmeans_run(X: torch.Tensor, K: int, init_centers: torch.Tensor, max_iter: int,
                fixed_iters: bool = False, path=None, timing: bool = False,
                out=None, ws: torch.Tensor | None = None, sample_every: int = 0,
-               metric: str = "l2"):
+               metric: str = "l2", force_fp64: bool = False):
     """Algorithm 1 steps 2-7 from init_centers (synchronous); metric="l1"
     assigns by the city-block distance (the centres stay centres of gravity).
 
@@ -288,7 +290,8 @@ def kmeans_run(X: torch.Tensor, K: int, init_centers: torch.Tensor, max_iter: in
         counts = torch.empty(K, dtype=torch.int32, device=X.device)
     else:
         labels, centers, counts = out
-    flags = _flags(path) | _metric(metric) | (KMEANS_FIXED_ITERS if fixed_iters else 0)
+    flags = (_flags(path) | _metric(metric) | (KMEANS_FIXED_ITERS if fixed_iters else 0)
+             | (KMEANS_FORCE_FP64 if force_fp64 else 0))
     if ws is None:
         ws = workspace(n, M, K, X.device, flags)
     iters = ctypes.c_int32(0)

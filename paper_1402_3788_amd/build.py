@@ -21,7 +21,8 @@ SOURCES = ([("kmeans_api.hip", [], "kmeans_api.o"), ("lloyd_ctl.hip", [], "lloyd
             ("lloyd_centres.hip", [], "lloyd_centres.o"), ("farthest.hip", [], "farthest.o"),
             ("diameter.hip", [], "diameter.o"), ("lloyd_l1.hip", [], "lloyd_l1.o")]
            + [(f, [f"-DLLOYD_PART={p}"], f.replace(".hip", f"_part{p}.o"))
-              for f in ("lloyd_tile.hip", "lloyd_lane.hip") for p in range(PARTS)])
+              for f in ("lloyd_tile.hip", "lloyd_lane.hip", "lloyd_lane_mfma.hip")
+              for p in range(PARTS)])
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

@@ -7,14 +7,13 @@
 #include "farthest.h"
 #include "diameter.h"
 
-#include <vector>
 
 using namespace lloyd;
 
 namespace {
 
 constexpr uint32_t kKnownFlags = KMEANS_FIXED_ITERS | KMEANS_PATH_DIRECT | KMEANS_PATH_MFMA |
-                                  KMEANS_PATH_TILES | KMEANS_METRIC_L1;
+                                  KMEANS_PATH_TILES | KMEANS_METRIC_L1 | KMEANS_FORCE_FP64;
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
@@ -41,7 +40,7 @@ bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 // 64-object tiles (-1 when their workgroup state does not fit in LDS).
 // KMEANS_PATH_MFMA: the
 // matrix cores, one object per lane when the centre operands fit in registers
-// (K <= 16, M <= 27), else 64-object tiles when their workgroup state fits in
+// (K <= 16, M <= 32), else 64-object tiles when their workgroup state fits in
 // LDS, else -1 (refused). No flag: tiles for K > 16, one object per lane on the
 // matrix cores for 5 <= K <= 16, the vector ALU otherwise (and wherever the
 // matrix-core forms do not fit).
@@ -58,12 +57,40 @@ int select_path(int32_t M, int32_t K, uint32_t flags)
 AccumPlan plan_for(int p, int64_t n, int32_t M, int32_t K, Mode mode)
 {
     if (p == kPathTile) return plan_tile(n, M, K, mode);
-    return plan_lane(n, M, K, mode, p == kPathLaneMfma);
+    if (p == kPathLaneMfma) return plan_lane_mfma(n, M, K, mode);
+    return plan_lane(n, M, K, mode);
 }
 
 hipError_t launch_step(const StepArgs &a, Mode mode, const AccumPlan &plan, hipStream_t s)
 {
-    return plan.path == kPathTile ? launch_tile(a, mode, plan, s) : launch_lane(a, mode, plan, s);
+    if (plan.path == kPathTile) return launch_tile(a, mode, plan, s);
+    if (plan.path == kPathLaneMfma) return launch_lane_mfma(a, mode, plan, s);
+    return launch_lane(a, mode, plan, s);
+}
+
+// Per-thread, per-device state of kmeans_run that outlives a call: HIP events
+// for its optional timing (created on first use, kept) and a pinned host copy
+// of the control block (the read at the end of a call needs no staging).
+// Neither is ever released; a thread holds at most a few events per device and
+// 256 bytes of pinned memory.
+struct RunCache {
+    int device = -1;
+    hipEvent_t ev[2 + 2 * 64];   // kMaxSamples sampled launches
+    int nev = 0;
+    Ctl *pinned = nullptr;
+};
+
+RunCache &run_cache()
+{
+    static thread_local RunCache caches[16];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) dev = 0;
+    RunCache &c = caches[dev % 16];
+    if (c.device != dev) {
+        c = RunCache{};
+        c.device = dev;
+    }
+    return c;
 }
 
 // Workspace: [Ctl (256 B)] [fp64 workgroup partials G*K*M] [int32 workgroup
@@ -273,6 +300,7 @@ int kmeans_assign(const float *X, int64_t n, int32_t M, const float *centers, in
     StepArgs a{};
     a.X = X; a.n = n; a.M = M; a.C = centers; a.K = K;
     a.labels = labels; a.min_d2 = min_d2;
+    a.force64 = (flags & KMEANS_FORCE_FP64) ? 1 : 0;
     if (flags & KMEANS_METRIC_L1) {
         const L1Plan p1 = plan_l1(n, M, K);
         if (p1.waves < 1) return KMEANS_EUNSUPPORTED;
@@ -327,54 +355,66 @@ int kmeans_run(const float *X, int64_t n, int32_t M, int32_t K, const float *ini
     const bool l1 = (flags & KMEANS_METRIC_L1) != 0;
     const L1Plan p1 = l1 ? plan_l1(n, M, K) : L1Plan{};
     if (l1 && p1.waves < 1) return KMEANS_EUNSUPPORTED;
+    const int every = timing == nullptr ? 0 : (timing->sample_every > 0 ? timing->sample_every : 16);
+    // events: one before the first launch, one after the last, and a pair
+    // around each sampled assign launch
+    constexpr int kMaxSamples = 64;
+    int nsampled = every > 0 ? (max_iter + every - 1) / every : 0;
+    if (nsampled > kMaxSamples) nsampled = kMaxSamples;
+
+    RunCache &cache = run_cache();
+    if (timing) {
+        while (cache.nev < 2 + 2 * nsampled) {
+            if (hipEventCreate(&cache.ev[cache.nev]) != hipSuccess) return KMEANS_EHIP;
+            ++cache.nev;
+        }
+    }
+    if (cache.pinned == nullptr) {
+        void *p = nullptr;
+        if (hipHostMalloc(&p, sizeof(Ctl), hipHostMallocDefault) == hipSuccess)
+            cache.pinned = static_cast<Ctl *>(p);
+    }
+    Ctl pageable{};
+    Ctl *host = cache.pinned != nullptr ? cache.pinned : &pageable;
 
     StepArgs a{};
-    a.X = X; a.n = n; a.M = M; a.C = centers; a.K = K;
+    a.X = X; a.n = n; a.M = M; a.K = K;
     a.labels = labels;
     a.centers_out = centers;     // centres are updated in place, iteration by iteration
     a.counts_out = counts;
     bind_workspace(a, L, static_cast<char *>(workspace));
     a.fixed = fixed;
     a.compare = 1;
+    a.force64 = (flags & KMEANS_FORCE_FP64) ? 1 : 0;
     a.labels_in = labels;        // the L1 form accumulates from the labels it wrote
     Ctl *ctl = a.ctl;
 
     if ((rc = hip_status(launch_ctl_reset(ctl, s)))) return rc;
-    if (init_centers != centers) {
-        rc = hip_status(hipMemcpyAsync(centers, init_centers, sizeof(float) * (size_t)K * M,
-                                       hipMemcpyDeviceToDevice, s));
-        if (rc) return rc;
-    }
 
-    // events: [0] before the first launch, then pairs around the sampled
-    // assign launches, and the last one after the final launch
-    std::vector<hipEvent_t> ev;
+    int nev = 0;
     auto mark = [&]() -> int {
         if (!timing) return KMEANS_OK;
-        hipEvent_t e;
-        if (hipEventCreate(&e) != hipSuccess) return KMEANS_EHIP;
-        ev.push_back(e);
-        return hip_status(hipEventRecord(e, s));
-    };
-    const int every = timing == nullptr ? 0 : (timing->sample_every > 0 ? timing->sample_every : 16);
-    auto cleanup = [&]() {
-        for (hipEvent_t e : ev) (void)hipEventDestroy(e);
+        return hip_status(hipEventRecord(cache.ev[nev++], s));
     };
 
     // Two launches per iteration: assign + accumulate (fused), then the centres
-    // and the congruence test from the workgroup partials.
+    // and the congruence test from the workgroup partials. Iteration t assigns
+    // with the centres of iteration t - 1: the caller's initial centres for
+    // t = 1 (read in place; nothing is copied), `centers` afterwards, which
+    // every centres launch writes whole.
     // Enqueue iterations in chunks; between chunks (early-stop mode only) read
     // the control block to learn whether the centres have become congruent.
     // Launches past convergence return at their first instruction.
     int t = 1, chunk = 3, launched = 0;
-    Ctl host{};
     rc = mark();
     while (!rc && t <= max_iter) {
         // fixed-count runs enqueue everything at once; otherwise chunks grow 3, 6, 12, ...
         const int end = (fixed || t + chunk - 1 >= max_iter) ? max_iter : t + chunk - 1;
         for (int tt = t; tt <= end && !rc; ++tt) {
             a.t = tt;
-            const bool sampled = every > 0 && (tt - 1) % every == 0;
+            a.C = tt == 1 ? init_centers : centers;
+            const bool sampled =
+                every > 0 && (tt - 1) % every == 0 && (tt - 1) / every < kMaxSamples;
             if (sampled) rc = mark();
             if (!rc && l1) {
                 // L1: assign, then the sums of Eq. (1) from those labels
@@ -390,20 +430,17 @@ int kmeans_run(const float *X, int64_t n, int32_t M, int32_t K, const float *ini
         }
         t = end + 1;
         if (rc || t > max_iter) break;
-        rc = hip_status(hipMemcpyAsync(&host, ctl, sizeof(Ctl), hipMemcpyDeviceToHost, s));
+        rc = hip_status(hipMemcpyAsync(host, ctl, sizeof(Ctl), hipMemcpyDeviceToHost, s));
         if (!rc) rc = hip_status(hipStreamSynchronize(s));
-        if (rc || host.converged_at != 0) break;
+        if (rc || host->converged_at != 0) break;
         chunk = chunk * 2 < 64 ? chunk * 2 : 64;
     }
     if (!rc) rc = mark();
-    if (!rc) rc = hip_status(hipMemcpyAsync(&host, ctl, sizeof(Ctl), hipMemcpyDeviceToHost, s));
+    if (!rc) rc = hip_status(hipMemcpyAsync(host, ctl, sizeof(Ctl), hipMemcpyDeviceToHost, s));
     if (!rc) rc = hip_status(hipStreamSynchronize(s));
-    if (rc) {
-        cleanup();
-        return rc;
-    }
-    *iterations = host.converged_at != 0 ? host.converged_at : max_iter;
-    if (host.ring_stalls != 0) rc = KMEANS_EHIP;
+    if (rc) return rc;
+    *iterations = host->converged_at != 0 ? host->converged_at : max_iter;
+    if (host->ring_stalls != 0) rc = KMEANS_EHIP;
 
     if (timing) {
         timing->step_ms = 0.0;
@@ -412,21 +449,16 @@ int kmeans_run(const float *X, int64_t n, int32_t M, int32_t K, const float *ini
         timing->assign_samples = 0;
         timing->reserved = 0;
         float ms = 0.f;
-        if (ev.size() < 2 || hipEventElapsedTime(&ms, ev.front(), ev.back()) != hipSuccess) {
-            rc = KMEANS_EHIP;
-        } else {
-            timing->step_ms = ms;
-            for (size_t e = 1; e + 2 < ev.size(); e += 2) {
-                if (hipEventElapsedTime(&ms, ev[e], ev[e + 1]) != hipSuccess) {
-                    rc = KMEANS_EHIP;
-                    break;
-                }
-                timing->assign_ms += ms;
-                timing->assign_samples++;
-            }
+        if (nev < 2 || hipEventElapsedTime(&ms, cache.ev[0], cache.ev[nev - 1]) != hipSuccess)
+            return KMEANS_EHIP;
+        timing->step_ms = ms;
+        for (int e = 1; e + 2 < nev; e += 2) {
+            if (hipEventElapsedTime(&ms, cache.ev[e], cache.ev[e + 1]) != hipSuccess)
+                return KMEANS_EHIP;
+            timing->assign_ms += ms;
+            timing->assign_samples++;
         }
     }
-    cleanup();
     return rc;
 }
 

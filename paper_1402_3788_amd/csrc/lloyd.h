@@ -57,9 +57,9 @@ enum Mode : int {
 };
 
 // Distance paths: one object per lane with the direct form on the vector ALU
-// (lloyd_lane.hip), one object per lane with the scores formed on 16x16x4
-// matrix-core blocks (same kernel, K <= 16), or 64-object tiles with 16x16x4
-// matrix-core blocks and a cross-lane argmin (lloyd_tile.hip, any K).
+// (lloyd_lane.hip), one object per lane with the scores on the bf16 matrix
+// cores (lloyd_lane_mfma.hip, K <= 16), or 64-object tiles on the matrix cores
+// with a cross-lane argmin (lloyd_tile.hip, any K).
 enum Path : int { kPathValu = 0, kPathTile = 1, kPathLaneMfma = 2 };
 
 // Static LDS of a kernel (bytes), from the runtime's attributes; SIZE_MAX when
@@ -81,13 +81,14 @@ struct AccumPlan {
 };
 
 // Launch geometry for a problem shape (pure host code).
-AccumPlan plan_lane(int64_t n, int M, int K, Mode mode, bool mfma);
+AccumPlan plan_lane(int64_t n, int M, int K, Mode mode);
+AccumPlan plan_lane_mfma(int64_t n, int M, int K, Mode mode);
 AccumPlan plan_tile(int64_t n, int M, int K, Mode mode);
 // Whether the tile kernel's per-workgroup state (centre operands and fp64
 // slab) fits in one workgroup's LDS for this shape.
 bool tile_fits(int M, int K);
 // Whether the one-object-per-lane matrix-core form supports this shape (its
-// centre operands live in registers).
+// centre operands live in registers: K <= 16, M <= 32).
 bool lane_mfma_fits(int M, int K);
 
 struct StepArgs {
@@ -107,9 +108,11 @@ struct StepArgs {
     int t;                     // iteration number (1-based)
     int fixed;                 // no early stop
     int compare;               // record the change flag of iteration t
+    int force64;               // decide every label with fp64 distances
 };
 
 hipError_t launch_lane(const StepArgs &a, Mode mode, const AccumPlan &plan, hipStream_t s);
+hipError_t launch_lane_mfma(const StepArgs &a, Mode mode, const AccumPlan &plan, hipStream_t s);
 hipError_t launch_tile(const StepArgs &a, Mode mode, const AccumPlan &plan, hipStream_t s);
 
 hipError_t launch_ctl_reset(Ctl *ctl, hipStream_t s);

@@ -151,6 +151,87 @@ __device__ inline int argmin_fp64(const float *xs, const float *__restrict__ C, 
 }
 
 // ---------------------------------------------------------------------------
+// Cross-lane merges of the matrix-core layouts (both distance kernels). In a
+// 16x16 product D[i][j] sits in lane j + 16(i/4), register i%4, so the four
+// lanes l16 + 16g (g = 0..3) hold different centre rows of the same objects.
+
+// Second-best of two (best, second) pairs, b1 <= b2 and p1 <= p2:
+// min(max(b1, p1), min(b2, p2)).
+__device__ inline float second_of(float b1, float b2, float p1, float p2)
+{
+    return __builtin_amdgcn_fmed3f(b1, p1, fminf(b2, p2));
+}
+
+// Merge the (best, second, label) triples of lanes l and l ^ 16 (ROW = 16) or
+// l and l ^ 32 (ROW = 32): the row swap returns, in every lane, the triples of
+// both lanes of its pair; the merge keeps the lower label on equal scores.
+template <int ROW>
+__device__ inline void merge_rows(float &b1, float &b2, int &lb)
+{
+    auto swap = [](uint32_t v) {
+        if (ROW == 16) return __builtin_amdgcn_permlane16_swap(v, v, false, false);
+        return __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    };
+    const auto s1 = swap(__float_as_uint(b1));
+    const auto s2 = swap(__float_as_uint(b2));
+    const auto sl = swap((uint32_t)lb);
+    const float f1 = __uint_as_float(s1[0]), g1 = __uint_as_float(s1[1]);
+    const float f2 = __uint_as_float(s2[0]), g2 = __uint_as_float(s2[1]);
+    const int fl = (int)sl[0], gl = (int)sl[1];
+    const bool take = (g1 < f1) | ((g1 == f1) & (gl < fl));
+    b2 = second_of(f1, f2, g1, g2);
+    b1 = take ? g1 : f1;
+    lb = take ? gl : fl;
+}
+
+template <int ROW>
+__device__ inline float sum_rows(float v)
+{
+    uint32_t u = __float_as_uint(v);
+    const auto s = (ROW == 16) ? __builtin_amdgcn_permlane16_swap(u, u, false, false)
+                               : __builtin_amdgcn_permlane32_swap(u, u, false, false);
+    return __uint_as_float(s[0]) + __uint_as_float(s[1]);
+}
+
+// Packed (best, second) keys of object `lane` (column lane / 16 of the tile's
+// 16-object columns) from the per-column keys (k1[c], k2[c]) of the four lanes
+// l16 + 16 g' that hold its centre rows. Two exchange stages: with lane l ^ 32
+// (the lower half keeps columns 0, 1 and sends 2, 3; the upper half the
+// reverse), then with lane l ^ 16 (a lane keeps its own column and sends the
+// other); each received pair is merged into the kept one. Keys of different
+// centres never compare equal, so the order of a merge does not matter.
+__device__ inline void own_column_keys(const float (&k1)[4], const float (&k2)[4], int lane,
+                                       float &b1, float &b2)
+{
+    const bool up = lane >= 32;
+    const bool odd = (lane >> 4) & 1;
+    // the partner's value out of a swap's pair (see merge_rows)
+    auto other32 = [up](uint32_t v) {
+        const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+        return __uint_as_float(up ? r[0] : r[1]);
+    };
+    auto other16 = [odd](uint32_t v) {
+        const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+        return __uint_as_float(odd ? r[0] : r[1]);
+    };
+    float m1[2], m2[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const float o1 = up ? k1[2 + i] : k1[i], o2 = up ? k2[2 + i] : k2[i];   // kept
+        const float s1 = up ? k1[i] : k1[2 + i], s2 = up ? k2[i] : k2[2 + i];   // sent
+        const float p1 = other32(__float_as_uint(s1)), p2 = other32(__float_as_uint(s2));
+        m2[i] = second_of(o1, o2, p1, p2);
+        m1[i] = fminf(o1, p1);
+    }
+    const float o1 = odd ? m1[1] : m1[0], o2 = odd ? m2[1] : m2[0];
+    const float s1 = odd ? m1[0] : m1[1], s2 = odd ? m2[0] : m2[1];
+    const float p1 = other16(__float_as_uint(s1)), p2 = other16(__float_as_uint(s2));
+    b2 = second_of(o1, o2, p1, p2);
+    b1 = fminf(o1, p1);
+}
+
+
+// ---------------------------------------------------------------------------
 // Per-wave accumulation of the numerator and denominator of Eq. (1).
 //
 // A wave owns P fp64 slabs of K rows x (M+1) columns: columns 0..M-1 hold the

@@ -37,7 +37,7 @@ template <int MB>
 __global__ void __launch_bounds__(kL1MaxWaves * kWave)
 lloyd_l1_kernel(const float *__restrict__ X, int64_t n, int M, const float *__restrict__ C,
                 int K, int32_t *__restrict__ labels, float *__restrict__ min_d,
-                Ctl *__restrict__ ctl, int t, int fixed)
+                Ctl *__restrict__ ctl, int t, int fixed, int force64)
 {
     if (stop_before(ctl, t, fixed)) return;
     extern __shared__ __align__(16) float l1_lds[];
@@ -97,7 +97,7 @@ lloyd_l1_kernel(const float *__restrict__ X, int64_t n, int M, const float *__re
             }
         }
         float best = b1;
-        const bool close = b2 != INFINITY && !(b2 - b1 > tau * (b1 + b2));
+        const bool close = force64 || (b2 != INFINITY && !(b2 - b1 > tau * (b1 + b2)));
         if (close && i < n) {
             // too close to call in fp32: every centre again in fp64
             double bd = INFINITY;
@@ -139,7 +139,7 @@ hipError_t l1_launch_mb(const StepArgs &a, const L1Plan &pl, hipStream_t s)
     if (st > (size_t)kMaxLds || st + pl.lds_bytes > (size_t)kMaxLds)
         return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL(kern, dim3(pl.groups), dim3(pl.waves * kWave), pl.lds_bytes, s, a.X,
-                       a.n, a.M, a.C, a.K, a.labels, a.min_d2, a.ctl, a.t, a.fixed);
+                       a.n, a.M, a.C, a.K, a.labels, a.min_d2, a.ctl, a.t, a.fixed, a.force64);
     return hipGetLastError();
 }
 

@@ -1,0 +1,552 @@
+// Fused assign + accumulate for small K (K <= 16, M <= 32): one 64-object tile
+// per wavefront at a time, the scores on the bf16 matrix cores, and every
+// tile read from global memory twice -- once in the matrix operand layout and
+// once in the accumulation layout -- so that the cache does the transpose and
+// LDS holds nothing but the fp64 sums.
+//
+// Per tile q (objects 64q .. 64q+63) a wave does:
+//   1. operand loads (issued one tile ahead): lane (g, o) = (lane / 16,
+//      lane % 16) reads features 8g .. 8g+7 of object 16b + o of the tile for
+//      each 16-object block b = 0..3 -- two 16-byte loads per block, each
+//      starting at any float of a row (rows of M floats) and reading at most
+//      three floats into the next row, which the zero A operands past M ignore;
+//   2. accumulation loads (issued for the current tile, served by the cache
+//      the operand loads filled): lane (h, j) = (lane / 32, lane % 32) reads
+//      feature j of object s + 32h for s = 0..31;
+//   3. scores (Algorithm 1 steps 2/4, Eq. (2) in the expanded form
+//      score = |c|^2 - 2 x.c, |x|^2 being common to all centres): A = -2C
+//      (16 centres x 32 features, zero past K and M) and B = X^T, both split
+//      into bf16 hi and lo parts rounded to nearest, three
+//      v_mfma_f32_16x16x32_bf16 per block (lo(A) hi(B) + hi(A) lo(B) +
+//      hi(A) hi(B)) on top of |c|^2; lane (g, o) ends with the scores of
+//      centres 4g .. 4g+3 for object o of every block;
+//   4. the label: each score becomes a packed key (its low 4 bits replaced by
+//      the centre's index), each lane keeps the best and second-best key of
+//      every block, and two rounds of row swaps (v_permlane32_swap, then
+//      v_permlane16_swap) leave lane l with the two best keys of object l;
+//      a label is accepted when the two differ by more than twice the proven
+//      error bound, otherwise the object is re-decided over all centres with
+//      fp64 distances in the reference operation order (lowest index on ties),
+//      so every label is the exact-arithmetic argmin;
+//   5. accumulation (the numerator and denominator of Eq. (1)): lane l holds
+//      the slab row offset of object l (slab l / 32); in step s a swizzle
+//      broadcasts object s + 32h's offset to lanes (h, .), and lane (h, j)
+//      adds feature j to slab h with an LDS fp64 add. The two halves of a
+//      wave add to different slabs and the lanes of a half to different
+//      columns, so no two lanes of one add meet on an address: every sum is
+//      formed in a fixed order (objects of the wave's tiles in ascending
+//      order per slab) without relying on how the LDS orders the lanes of one
+//      instruction. Counts are integer LDS adds (order-free).
+// At the end the workgroup adds its slabs in a fixed order (waves, then
+// slabs) and writes one fp64 partial per (cluster, feature) and one count per
+// cluster; a second launch forms the centres (lloyd_centres.hip).
+//
+// Error bound of a score (why the label test is safe): with a = -2c_j and
+// b = x_j split as a = ah + al + ea (|ea| <= 2^-16 |a|, |al| <= 2^-8 (1+2^-8)|a|)
+// and likewise b, the dropped terms ah eb + al bl + ea b are below
+// 3.02 * 2^-16 |a b| per feature, and sum_j |a_j b_j| <= |c|^2 + |x|^2. The
+// bf16 products are exact in fp32. The matrix core adds the 96 products and
+// the |c|^2 seed in some order with at most 98 roundings; the bound assumes
+// only that each rounding is faithful (error below one unit in the last place,
+// 2^-23 relative), whatever the order or rounding direction, so the sums err by
+// at most 1.01 * 98 * 2^-23 of (|c|^2 + sum |a b|) <= (3|c|^2 + |x|^2). The
+// fp32 |c|^2 (M fused multiply-adds) errs by 25 * 2^-24 |c|^2 at M = 32.
+// A packed key moves its score by less than 2^(4-23) of the score's
+// magnitude, itself below (1 + E)(3|c|^2 + |x|^2). Together every key is
+// within E (3 max|c|^2 + |x|^2) of the exact score with
+//     E = 3.02 * 2^-16 + 104 * 2^-23 + 1.01 * 2^-19,
+// and a label is accepted when the two best keys differ by more than
+// 2.02 E (3.02 max|c|^2 + 1.0001 |x|^2) + 1e-30 (the fp32 |x|^2 and max|c|^2
+// are themselves within the margins; 1e-30 covers bf16 parts below the normal
+// range). |x|^2 here sums the squares of every value the lane group read,
+// including the up to seven floats past the object's M features: an upper
+// bound, which only widens the band (and makes an object whose neighbour holds
+// an infinity or a NaN go to the fp64 path).
+#include "lloyd.h"
+#include "lloyd_device.h"
+
+#include <float.h>
+#include <math.h>
+
+#include <array>
+#include <type_traits>
+#include <utility>
+
+#include "lloyd_parts.h"
+
+namespace lloyd {
+
+namespace {
+
+typedef float f4v __attribute__((ext_vector_type(4)));
+// Four floats at any 4-byte-aligned address: rows of X start on any float.
+typedef float f4u __attribute__((ext_vector_type(4), aligned(4)));
+
+constexpr int kWaves = 12;            // waves per workgroup (3 per SIMD)
+constexpr int kMinWavesPerSimd = 3;   // caps registers at 168 per lane
+constexpr int kMaxMLane = 32;         // features: four lane groups of eight
+[[maybe_unused]] constexpr int kMaxKLane = 16;        // centres: one 16-row A operand
+
+// LDS of a workgroup: [W][2][K][M] fp64 slabs, then [W][K] int32 counts.
+[[maybe_unused]] __host__ __device__ inline size_t lane_lds_bytes(int M, int K, int W)
+{
+    return (size_t)W * 2 * K * M * 8 + (size_t)W * K * 4;
+}
+
+// Object rows after the last row of a tile that the operand loads may touch
+// (up to three floats past a row): tiles whose rows have that many successors
+// in X take the unguarded loads.
+__host__ __device__ inline int64_t rows_after(int M) { return (3 + M - 1) / M; }
+
+// Broadcast of lane s of each 32-lane half (ds_swizzle in bit-mask mode: and
+// mask 0, or mask s).
+template <int S>
+[[maybe_unused]] __device__ inline int bcast32(int v)
+{
+    return __builtin_amdgcn_ds_swizzle(v, S << 5);
+}
+
+// f(integral_constant<int, S>) for S = 0 .. N-1, unrolled.
+template <class F, int... S>
+__device__ inline void static_for_impl(F &f, std::integer_sequence<int, S...>)
+{
+    (f(std::integral_constant<int, S>{}), ...);
+}
+template <int N, class F>
+__device__ inline void static_for(F &&f)
+{
+    static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+// Comparisons of packed keys. A key is a float whose low bits were replaced
+// by an index, so the compiler cannot prove it canonical and would quieten it
+// before every min / max; written out, each is one instruction. Keys of
+// finite scores are finite; a score that overflowed sends its object to the
+// fp64 path (its |x|^2 bound is infinite), whatever these return for it.
+[[maybe_unused]] __device__ inline float key_min(float a, float b)
+{
+    float r;
+    asm("v_min_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+[[maybe_unused]] __device__ inline float key_max(float a, float b)
+{
+    float r;
+    asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+[[maybe_unused]] __device__ inline float key_min3(float a, float b, float c)
+{
+    float r;
+    asm("v_min3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+    return r;
+}
+[[maybe_unused]] __device__ inline float key_med3(float a, float b, float c)
+{
+    float r;
+    asm("v_med3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+    return r;
+}
+
+// Best and second best of two (best, second) key pairs.
+[[maybe_unused]] __device__ inline void key_merge(float a1, float a2, float b1, float b2, float &m1, float &m2)
+{
+    m1 = key_min(a1, b1);
+    m2 = key_med3(a1, b1, key_min(a2, b2));
+}
+
+// The row swaps below exchange two registers at once: v_permlane32_swap(x, y)
+// gives lanes 0-31 the y of lane l+32 in place of their y, and lanes 32-63 the
+// x of lane l-32 in place of their x; v_permlane16_swap does the same between
+// even and odd 16-lane rows. With x = column c and y = column c + 2 (c + 1),
+// each lane ends with both lanes' values of the one column it keeps: the
+// lower half (even rows) column c, the upper half (odd rows) column c + 2
+// (c + 1), one in x and one in y.
+[[maybe_unused]] __device__ inline void swap32(float &x, float &y)
+{
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(y),
+                                                    false, false);
+    x = __uint_as_float(r[0]);
+    y = __uint_as_float(r[1]);
+}
+[[maybe_unused]] __device__ inline void swap16(float &x, float &y)
+{
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(y),
+                                                    false, false);
+    x = __uint_as_float(r[0]);
+    y = __uint_as_float(r[1]);
+}
+
+// (best, second) keys of object `lane` from the per-block keys (k1[b], k2[b])
+// of the four lanes l16 + 16g that hold its centre rows (lane 16b + l16 owns
+// object 16b + l16 of the tile): a swap with lane l ^ 32 and a merge keep
+// blocks {0, 1} in the lower half and {2, 3} in the upper half, then a swap
+// with lane l ^ 16 and a merge keep the lane's own block. Keys of different
+// centres never compare equal, so the merge order does not matter.
+[[maybe_unused]] __device__ inline void own_block_keys(float (&k1)[4], float (&k2)[4], float &b1, float &b2)
+{
+    float m1[2], m2[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        swap32(k1[i], k1[2 + i]);
+        swap32(k2[i], k2[2 + i]);
+        key_merge(k1[i], k2[i], k1[2 + i], k2[2 + i], m1[i], m2[i]);
+    }
+    swap16(m1[0], m1[1]);
+    swap16(m2[0], m2[1]);
+    key_merge(m1[0], m2[0], m1[1], m2[1], b1, b2);
+}
+
+// The same exchange for the per-block partial sums of |x|^2 (fp32 addition
+// is commutative, so both lanes of a pair form the same sums).
+[[maybe_unused]] __device__ inline float own_block_sum(float (&p)[4])
+{
+    swap32(p[0], p[2]);
+    swap32(p[1], p[3]);
+    float m0 = p[0] + p[2], m1 = p[1] + p[3];
+    swap16(m0, m1);
+    return m0 + m1;
+}
+
+template <int M, int MODE>
+__global__ void __launch_bounds__(kWaves * kWave, kMinWavesPerSimd)
+lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict__ C, int K,
+                 int32_t *__restrict__ labels, const int32_t *__restrict__ labels_in,
+                 float *__restrict__ min_d2, double *__restrict__ part_sums,
+                 int32_t *__restrict__ part_counts, Ctl *__restrict__ ctl, int t, int fixed,
+                 int force64)
+{
+    static_assert(M >= 1 && M <= kMaxMLane, "feature count");
+    constexpr bool kAcc = MODE != kAssign;
+    constexpr bool kDist = MODE != kAccumLabels;
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int W = blockDim.x / kWave;
+    const int wave = threadIdx.x / kWave;
+    const int lane = threadIdx.x % kWave;
+    const int g = lane >> 4, o16 = lane & 15;     // matrix layout
+    const int h = lane >> 5, j = lane & 31;       // accumulation layout
+
+    if (MODE == kAssignAccum && stop_before(ctl, t, fixed)) return;
+
+    double *slabs = reinterpret_cast<double *>(smem) + (size_t)wave * 2 * K * M;
+    int32_t *cnts = reinterpret_cast<int32_t *>(reinterpret_cast<double *>(smem) +
+                                                (size_t)W * 2 * K * M) + wave * K;
+    if (kAcc) {
+        for (int i = lane; i < 2 * K * M; i += kWave) slabs[i] = 0.0;
+        for (int i = lane; i < K; i += kWave) cnts[i] = 0;
+    }
+
+    // A operands for the whole launch: lane (g, o) holds -2 c_o, features
+    // 8g .. 8g+7 (zero past K and M), split into bf16 hi and lo, and the
+    // accumulator seeds |c_k|^2 of centres k = 4g .. 4g+3 (the largest finite
+    // float past K, so padding centres never win and their keys stay finite).
+    uint32_t ah[4], al[4];
+    f4v cseed = {0.f, 0.f, 0.f, 0.f};
+    float cmax = 0.f;
+    if (kDist) {
+        float a[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int f = 8 * g + e;
+            a[e] = (o16 < K && f < M) ? -2.0f * C[o16 * M + f] : 0.f;
+        }
+        split_bf16x8(a, ah, al);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int k = 4 * g + r;
+            float nk = FLT_MAX;
+            if (k < K) {
+                nk = 0.f;
+#pragma unroll
+                for (int f = 0; f < M; ++f) nk = __builtin_fmaf(C[k * M + f], C[k * M + f], nk);
+                cmax = fmaxf(cmax, nk);
+            }
+            cseed[r] = nk;
+        }
+        cmax = fmaxf(cmax, __shfl_xor(cmax, 16, kWave));
+        cmax = fmaxf(cmax, __shfl_xor(cmax, 32, kWave));
+    }
+    constexpr float kE = 3.02f * 1.5258789e-05f + 104.0f * 1.1920929e-07f + 1.01f * 1.9073486e-06f;
+    const uint32_t kKeyMask = ~15u;
+
+    const int64_t nt = (n + kWave - 1) / kWave;                    // tiles
+    int64_t nsafe = (n - rows_after(M)) / kWave;                   // unguarded tiles
+    if (nsafe < 0) nsafe = 0;
+    const int64_t stride = (int64_t)gridDim.x * W;
+    const int64_t q0 = (int64_t)wave * gridDim.x + blockIdx.x;
+
+    // operand loads of tile q (unguarded: q < nsafe). Chunk starts are
+    // clamped into the row, so a lane group with fewer than eight features
+    // left reads some of them twice (harmless: A is zero there, and |x|^2 is
+    // an upper bound).
+    const int c0 = 8 * g < M ? 8 * g : 0;
+    const int c1 = 8 * g + 4 < M ? 8 * g + 4 : c0;
+    auto load_ops = [&](int64_t q, f4v (&xb)[4][2]) {
+        const float *row = X + (q * kWave + o16) * (int64_t)M;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            xb[b][0] = *reinterpret_cast<const f4u *>(row + 16 * b * M + c0);
+            xb[b][1] = *reinterpret_cast<const f4u *>(row + 16 * b * M + c1);
+        }
+    };
+    // guarded form for the last tiles: zero past n and past M
+    auto load_ops_tail = [&](int64_t q, f4v (&xb)[4][2]) {
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            const int64_t r = q * kWave + 16 * b + o16;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int f = 8 * g + e;
+                xb[b][e / 4][e % 4] = (r < n && f < M) ? X[r * M + f] : 0.f;
+            }
+        }
+    };
+    const int jr = j < M ? j : M - 1;
+
+    int nfallback = 0;
+
+    // One tile: kTail selects the guarded loads and validity tests.
+    // The accumulation loads of tile q go out first, then the operand loads of
+    // tile qn into nxt (unguarded form only), so that waiting for the former
+    // never waits for the latter; every load is unconditional, so the waits
+    // count them exactly.
+    auto step = [&](int64_t q, f4v (&xb)[4][2], f4v (&nxt)[4][2], int64_t qn, auto tail) {
+        constexpr bool kTail = decltype(tail)::value;
+        const int64_t i = q * kWave + lane;           // this lane's object
+        const bool valid = !kTail || i < n;
+        float xa[32];
+        if (kAcc) {
+            const float *col = X + (q * kWave + 32 * h) * (int64_t)M + jr;
+#pragma unroll
+            for (int s = 0; s < 32; ++s) {
+                if (kTail) xa[s] = (q * kWave + 32 * h + s < n) ? col[(int64_t)s * M] : 0.f;
+                else xa[s] = col[(int64_t)s * M];
+            }
+        }
+        if (kDist && !kTail) load_ops(qn, nxt);
+        int lab = 0;
+        if (kDist) {
+            uint32_t bh[4][4], bl[4][4];
+            float xp[4];
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+                float v[8];
+                float acc = 0.f;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    v[e] = xb[b][e / 4][e % 4];
+                    acc = __builtin_fmaf(v[e], v[e], acc);
+                }
+                xp[b] = acc;
+                split_bf16x8(v, bh[b], bl[b]);
+            }
+            f4v d[4];
+#pragma unroll
+            for (int b = 0; b < 4; ++b) d[b] = cseed;
+#pragma unroll
+            for (int b = 0; b < 4; ++b)
+                d[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf8(al), as_bf8(bh[b]), d[b], 0, 0, 0);
+#pragma unroll
+            for (int b = 0; b < 4; ++b)
+                d[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf8(ah), as_bf8(bl[b]), d[b], 0, 0, 0);
+#pragma unroll
+            for (int b = 0; b < 4; ++b)
+                d[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf8(ah), as_bf8(bh[b]), d[b], 0, 0, 0);
+            // packed keys, best and second best of the lane's 4 centres per block
+            float k1[4], k2[4];
+            const uint32_t i0 = (uint32_t)(4 * g);
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+                float s[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    s[r] = __uint_as_float((__float_as_uint(d[b][r]) & kKeyMask) | (i0 + r));
+                const float lo01 = key_min(s[0], s[1]), hi01 = key_max(s[0], s[1]);
+                k2[b] = key_min(hi01, key_med3(lo01, s[2], s[3]));
+                k1[b] = key_min3(lo01, s[2], s[3]);
+            }
+            float b1, b2;
+            own_block_keys(k1, k2, b1, b2);
+            const float xsq = own_block_sum(xp);
+            lab = (int)(__float_as_uint(b1) & 15u);
+            lab = lab < K ? lab : K - 1;
+            const float thr = 2.02f * kE * (3.02f * cmax + 1.0001f * xsq) + 1e-30f;
+            const bool ok = !force64 && ((K == 1) || (b2 - b1 > thr));
+            float dmin = 0.f;
+            if (__ballot(valid && !ok) != 0) {
+                if (valid && !ok) {
+                    double bd;
+                    lab = argmin_fp64<M>(X + i * M, C, K, bd);
+                    dmin = (float)bd;
+                }
+                if (ctl != nullptr) nfallback += __popcll(__ballot(valid && !ok));
+            }
+            if (MODE == kAssign && min_d2 != nullptr && valid && ok) {
+                const float *xg = X + i * M;
+                const float *c = C + (int64_t)lab * M;
+                float dd = 0.f;
+#pragma unroll
+                for (int f = 0; f < M; ++f) {
+                    const float e = xg[f] - c[f];
+                    dd = __builtin_fmaf(e, e, dd);
+                }
+                dmin = dd;
+            }
+            if (valid) {
+                labels[i] = lab;
+                if (MODE == kAssign && min_d2 != nullptr) min_d2[i] = dmin;
+            }
+        } else {
+            lab = valid ? labels_in[i] : -1;
+            if (lab >= K) lab = -1;
+        }
+        if (kAcc) {
+            const bool adds = valid && lab >= 0;
+            // slab row of object `lane` (object s + 32h sits in slab h), -1: none
+            const int my_off = adds ? ((lane >> 5) * K + lab) * M : -1;
+            if (adds) atomicAdd(cnts + lab, 1);
+            // all 32 broadcasts first, then the adds (each add waits for its
+            // broadcast; issued in between they would wait one by one)
+            int o[32];
+            static_for<32>([&](auto sc) {
+                constexpr int s = decltype(sc)::value;
+                o[s] = bcast32<s>(my_off);
+            });
+            if (j < M) {
+#pragma unroll
+                for (int s = 0; s < 32; ++s)
+                    if ((!kTail && MODE != kAccumLabels) || o[s] >= 0)
+                        __hip_atomic_fetch_add(slabs + o[s] + j, (double)xa[s], __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_WAVEFRONT);
+            }
+        }
+    };
+
+    // Main loop over the unguarded tiles, the next tile's operand loads in
+    // flight in the other register set; then the guarded tail tiles.
+    // (The prefetch past a wave's last unguarded tile reloads tile nsafe - 1.)
+    f4v xb[2][4][2];
+    int64_t q = q0;
+    auto next = [&](int64_t qq) { return qq < nsafe ? qq : nsafe - 1; };
+    if (kDist && q < nsafe) load_ops(q, xb[0]);
+    for (; q < nsafe; q += 2 * stride) {
+        step(q, xb[0], xb[1], next(q + stride), std::false_type{});
+        if (q + stride >= nsafe) {
+            q += stride;
+            break;
+        }
+        step(q + stride, xb[1], xb[0], next(q + 2 * stride), std::false_type{});
+    }
+    for (; q < nt; q += stride) {
+        if (kDist) load_ops_tail(q, xb[0]);
+        step(q, xb[0], xb[1], q, std::true_type{});
+    }
+
+    if (ctl != nullptr && lane == 0 && nfallback > 0) atomicAdd(&ctl->fallbacks, nfallback);
+
+    if (kAcc) {
+        __syncthreads();
+        const double *all = reinterpret_cast<const double *>(smem);
+        const int32_t *allc = reinterpret_cast<const int32_t *>(all + (size_t)W * 2 * K * M);
+        double *ps = part_sums + (int64_t)blockIdx.x * K * M;
+        for (int e = threadIdx.x; e < K * M; e += blockDim.x) {
+            double s = 0.0;
+            for (int r = 0; r < 2 * W; ++r) s = s + all[(size_t)r * K * M + e];
+            ps[e] = s;
+        }
+        for (int k = threadIdx.x; k < K; k += blockDim.x) {
+            int32_t c = 0;
+            for (int w = 0; w < W; ++w) c += allc[w * K + k];
+            part_counts[(int64_t)blockIdx.x * K + k] = c;
+        }
+    }
+}
+
+template <int M>
+hipError_t launch_m(const StepArgs &a, Mode mode, const AccumPlan &p, hipStream_t s)
+{
+    const dim3 grid(p.groups), block(p.waves * kWave);
+#define LANE_MFMA_LAUNCH(MD)                                                                   \
+    do {                                                                                       \
+        auto kern = lane_mfma_kernel<M, MD>;                                                   \
+        if (p.lds_bytes > (size_t)kMaxLds) return hipErrorInvalidConfiguration;                \
+        hipLaunchKernelGGL(kern, grid, block, p.lds_bytes, s, a.X, a.n, a.C, a.K, a.labels,    \
+                           a.labels_in, a.min_d2, a.part_sums, a.part_counts, a.ctl, a.t,      \
+                           a.fixed, a.force64);                                                \
+    } while (0)
+    switch (mode) {
+    case kAssign: LANE_MFMA_LAUNCH(kAssign); break;
+    case kAssignAccum: LANE_MFMA_LAUNCH(kAssignAccum); break;
+    case kAccumLabels: LANE_MFMA_LAUNCH(kAccumLabels); break;
+    }
+#undef LANE_MFMA_LAUNCH
+    return hipGetLastError();
+}
+
+using LaunchFn = hipError_t (*)(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
+
+// This translation unit instantiates the kernel for the feature counts of one
+// part of [1, kMaxM] that are at most kMaxMLane.
+constexpr int kPartLo = LLOYD_PART * kMaxM / LLOYD_PARTS + 1;
+constexpr int kPartN = kMaxM / LLOYD_PARTS;
+
+template <int M>
+constexpr LaunchFn entry()
+{
+#ifdef LLOYD_ONLY_M
+    if constexpr (M != LLOYD_ONLY_M) return nullptr;
+    else
+#endif
+    if constexpr (M <= kMaxMLane) return &launch_m<M>;
+    else return nullptr;
+}
+
+template <int... Is>
+constexpr auto make_table(std::integer_sequence<int, Is...>)
+{
+    return std::array<LaunchFn, sizeof...(Is)>{entry<kPartLo + Is>()...};
+}
+
+}  // namespace
+
+hipError_t LLOYD_PART_FN(launch_lane_mfma_part)(const StepArgs &a, Mode mode, const AccumPlan &plan,
+                                                hipStream_t s)
+{
+    static constexpr auto table = make_table(std::make_integer_sequence<int, kPartN>{});
+    if (a.M < kPartLo || a.M >= kPartLo + kPartN) return hipErrorInvalidValue;
+    const LaunchFn fn = table[a.M - kPartLo];
+    return fn ? fn(a, mode, plan, s) : hipErrorInvalidValue;
+}
+
+#if LLOYD_PART == 0
+bool lane_mfma_fits(int M, int K) { return K <= kMaxKLane && M <= kMaxMLane; }
+
+AccumPlan plan_lane_mfma(int64_t n, int M, int K, Mode mode)
+{
+    AccumPlan p{};
+    p.path = kPathLaneMfma;
+    int W = kWaves;
+    const int64_t nq = (n + kWave - 1) / kWave;
+    while (W > 1 && W / 2 >= nq) W /= 2;
+    int64_t groups = (nq + W - 1) / W;
+    if (groups > kCUs) groups = kCUs;       // one persistent workgroup per compute unit
+    p.waves = W;
+    p.groups = (int)groups;
+    p.accum = 0;
+    p.lds_bytes = mode == kAssign ? 0 : lane_lds_bytes(M, K, W);
+    return p;
+}
+
+hipError_t launch_lane_mfma(const StepArgs &a, Mode mode, const AccumPlan &plan, hipStream_t s)
+{
+    if (a.M < 1 || a.M > kMaxMLane || a.K > kMaxKLane) return hipErrorInvalidValue;
+    switch ((a.M - 1) / (kMaxM / LLOYD_PARTS)) {
+#define LLOYD_CASE(P) case P: return launch_lane_mfma_part_##P(a, mode, plan, s);
+        LLOYD_PART_CASES
+#undef LLOYD_CASE
+    }
+    return hipErrorInvalidValue;
+}
+#endif
+
+}  // namespace lloyd

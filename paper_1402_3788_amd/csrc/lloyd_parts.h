@@ -25,4 +25,8 @@ hipError_t launch_lane_part_0(const StepArgs &, Mode, const AccumPlan &, hipStre
 hipError_t launch_lane_part_1(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
 hipError_t launch_lane_part_2(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
 hipError_t launch_lane_part_3(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
+hipError_t launch_lane_mfma_part_0(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
+hipError_t launch_lane_mfma_part_1(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
+hipError_t launch_lane_mfma_part_2(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
+hipError_t launch_lane_mfma_part_3(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
 }  // namespace lloyd

@@ -155,88 +155,13 @@ __device__ inline void ring_pass(uint32_t *turn, uint32_t next)
     __hip_atomic_store(turn, next, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
-// Second-best of two (best, second) pairs, b1 <= b2 and p1 <= p2:
-// min(max(b1, p1), min(b2, p2)).
-__device__ inline float second_of(float b1, float b2, float p1, float p2)
-{
-    return __builtin_amdgcn_fmed3f(b1, p1, fminf(b2, p2));
-}
-
-// Merge the (best, second, label) triples of lanes l and l ^ 16 (ROW = 16) or
-// l and l ^ 32 (ROW = 32): the row swap returns, in every lane, the triples of
-// both lanes of its pair; the merge keeps the lower label on equal scores.
-template <int ROW>
-__device__ inline void merge_rows(float &b1, float &b2, int &lb)
-{
-    auto swap = [](uint32_t v) {
-        if (ROW == 16) return __builtin_amdgcn_permlane16_swap(v, v, false, false);
-        return __builtin_amdgcn_permlane32_swap(v, v, false, false);
-    };
-    const auto s1 = swap(__float_as_uint(b1));
-    const auto s2 = swap(__float_as_uint(b2));
-    const auto sl = swap((uint32_t)lb);
-    const float f1 = __uint_as_float(s1[0]), g1 = __uint_as_float(s1[1]);
-    const float f2 = __uint_as_float(s2[0]), g2 = __uint_as_float(s2[1]);
-    const int fl = (int)sl[0], gl = (int)sl[1];
-    const bool take = (g1 < f1) | ((g1 == f1) & (gl < fl));
-    b2 = second_of(f1, f2, g1, g2);
-    b1 = take ? g1 : f1;
-    lb = take ? gl : fl;
-}
-
-template <int ROW>
-__device__ inline float sum_rows(float v)
-{
-    uint32_t u = __float_as_uint(v);
-    const auto s = (ROW == 16) ? __builtin_amdgcn_permlane16_swap(u, u, false, false)
-                               : __builtin_amdgcn_permlane32_swap(u, u, false, false);
-    return __uint_as_float(s[0]) + __uint_as_float(s[1]);
-}
-
-// Packed (best, second) keys of object `lane` (column lane / 16 of the tile's
-// 16-object columns) from the per-column keys (k1[c], k2[c]) of the four lanes
-// l16 + 16 g' that hold its centre rows. Two exchange stages: with lane l ^ 32
-// (the lower half keeps columns 0, 1 and sends 2, 3; the upper half the
-// reverse), then with lane l ^ 16 (a lane keeps its own column and sends the
-// other); each received pair is merged into the kept one. Keys of different
-// centres never compare equal, so the order of a merge does not matter.
-__device__ inline void own_column_keys(const float (&k1)[4], const float (&k2)[4], int lane,
-                                       float &b1, float &b2)
-{
-    const bool up = lane >= 32;
-    const bool odd = (lane >> 4) & 1;
-    // the partner's value out of a swap's pair (see merge_rows)
-    auto other32 = [up](uint32_t v) {
-        const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
-        return __uint_as_float(up ? r[0] : r[1]);
-    };
-    auto other16 = [odd](uint32_t v) {
-        const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
-        return __uint_as_float(odd ? r[0] : r[1]);
-    };
-    float m1[2], m2[2];
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        const float o1 = up ? k1[2 + i] : k1[i], o2 = up ? k2[2 + i] : k2[i];   // kept
-        const float s1 = up ? k1[i] : k1[2 + i], s2 = up ? k2[i] : k2[2 + i];   // sent
-        const float p1 = other32(__float_as_uint(s1)), p2 = other32(__float_as_uint(s2));
-        m2[i] = second_of(o1, o2, p1, p2);
-        m1[i] = fminf(o1, p1);
-    }
-    const float o1 = odd ? m1[1] : m1[0], o2 = odd ? m2[1] : m2[0];
-    const float s1 = odd ? m1[0] : m1[1], s2 = odd ? m2[0] : m2[1];
-    const float p1 = other16(__float_as_uint(s1)), p2 = other16(__float_as_uint(s2));
-    b2 = second_of(o1, o2, p1, p2);
-    b1 = fminf(o1, p1);
-}
-
-
 template <int M, int MODE, int ACC>
 __global__ void __launch_bounds__(kMaxWaves * kWave)
 lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restrict__ C, int K,
                   int32_t *__restrict__ labels, const int32_t *__restrict__ labels_in,
                   float *__restrict__ min_d2, double *__restrict__ part_sums,
-                  int32_t *__restrict__ part_counts, Ctl *__restrict__ ctl, int t, int fixed)
+                  int32_t *__restrict__ part_counts, Ctl *__restrict__ ctl, int t, int fixed,
+                  int force64)
 {
     using TG = TileGeom<M>;
     constexpr int KS = (M + 3) / 4;          // 4-feature steps of the fp32 products
@@ -587,11 +512,11 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
             const float e1 = 3.02f * 1.5258789e-05f + 1.03f * (float)(96 * KC + 2) * 5.9604645e-8f +
                              1.01f * key_rel;
             const float thr1 = 2.02f * e1 * (3.02f * cmax + 1.0001f * mx) + 1e-30f;
-            bool ok = (K == 1) || (mb2 - mb1 > thr1);
+            bool ok = !force64 && ((K == 1) || (mb2 - mb1 > thr1));
 
             // ---- pass 2 (tiles with a call too close for pass 1): the fp32
             // products, A = -2C read from C, B = X^T from the tile.
-            if (__ballot(valid && !ok) != 0) {
+            if (!force64 && __ballot(valid && !ok) != 0) {
                 float bop[kCols][KS];
 #pragma unroll
                 for (int c = 0; c < kCols; ++c) {
@@ -739,7 +664,7 @@ hipError_t launch_m(const StepArgs &a, Mode mode, const AccumPlan &p, hipStream_
             return hipErrorInvalidConfiguration;                                               \
         hipLaunchKernelGGL(kern, grid, block, p.lds_bytes, s, a.X, a.n, a.C, a.K, a.labels,    \
                            a.labels_in, a.min_d2, a.part_sums, a.part_counts, a.ctl, a.t,      \
-                           a.fixed);                                                           \
+                           a.fixed, a.force64);                                                \
     } while (0)
     switch (mode) {
     case kAssign: LLOYD_MFMA_LAUNCH(kAssign, 0); break;

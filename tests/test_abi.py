@@ -43,7 +43,7 @@ def test_header_constants_match_binding():
         m = re.search(rf"#define {name}\s+(-?\d+)", text)
         assert int(m.group(1)) == getattr(km, name)
     for name in ["KMEANS_FIXED_ITERS", "KMEANS_PATH_DIRECT", "KMEANS_PATH_MFMA",
-                 "KMEANS_PATH_TILES", "KMEANS_METRIC_L1"]:
+                 "KMEANS_PATH_TILES", "KMEANS_METRIC_L1", "KMEANS_FORCE_FP64"]:
         m = re.search(rf"#define {name}\s+\(1u << (\d+)\)", text)
         assert (1 << int(m.group(1))) == getattr(km, name)
 
@@ -64,6 +64,11 @@ def test_workspace_bytes():
     assert km.kmeans_workspace_bytes(10, 4, 4, 1 << 9) == 0     # unknown flag
     assert km.kmeans_workspace_bytes(10**6, 25, 16, km.KMEANS_METRIC_L1) > 0
     assert km.kmeans_workspace_bytes(10, 4, 4, km.KMEANS_METRIC_L1 | km.KMEANS_PATH_MFMA) == 0
+    # the all-fp64 decision combines with every path and metric
+    for f in (0, km.KMEANS_PATH_DIRECT, km.KMEANS_PATH_MFMA, km.KMEANS_PATH_TILES,
+              km.KMEANS_METRIC_L1):
+        assert km.kmeans_workspace_bytes(10**5, 25, 16, f | km.KMEANS_FORCE_FP64) == \
+            km.kmeans_workspace_bytes(10**5, 25, 16, f)
     # partials grow with K*M; the control block is always there
     assert km.kmeans_workspace_bytes(10**6, 25, 256) > km.kmeans_workspace_bytes(10**6, 25, 16)
     assert km.kmeans_workspace_bytes(1, 1, 1) >= 256
@@ -128,7 +133,7 @@ def test_update_validation(kw, code):
     (dict(flags=km.KMEANS_PATH_DIRECT | km.KMEANS_PATH_MFMA), km.KMEANS_EINVAL),
     (dict(flags=km.KMEANS_PATH_MFMA | km.KMEANS_PATH_TILES), km.KMEANS_EINVAL),
     (dict(flags=km.KMEANS_PATH_TILES, M=16, K=1024, wsb=1 << 30), km.KMEANS_EUNSUPPORTED),
-    (dict(flags=1 << 5), km.KMEANS_EINVAL), (dict(ws=None), km.KMEANS_EWORKSPACE),
+    (dict(flags=1 << 9), km.KMEANS_EINVAL), (dict(ws=None), km.KMEANS_EWORKSPACE),
     (dict(flags=km.KMEANS_METRIC_L1 | km.KMEANS_PATH_TILES), km.KMEANS_EINVAL),
     (dict(wsb=16), km.KMEANS_EWORKSPACE),
 ])

@@ -281,39 +281,3 @@ def test_workload3_fixed_mode_as_benchmarked():
     assert np.array_equal(lab.cpu().numpy(), olab)
     assert np.array_equal(cnt.cpu().numpy(), ocnt)
     check_centers(C.cpu().numpy(), oC)
-
-
-def _stepwise_at_scale(name, T, sample=20_000):
-    """Full-size check without the full oracle trajectory: the GPU's labels of
-    pass T are compared with the oracle's assignment (to the GPU's own centres
-    of pass T-1) on a seeded sample of objects, and the GPU's centres of pass T
-    with the oracle's Eq. (1) over all objects with the GPU's labels. The GPU's
-    farthest-point initial centres are compared with the stored ones."""
-    w = workloads.get(name)
-    X, _, init_idx, init = workloads.load(name)
-    Xg, Cg = _gpu(X), _gpu(init)
-    # the initial centres at this size: the GPU traversal gives the stored ones
-    gidx, gC = km.kmeans_init_farthest(Xg, w.K)
-    assert np.array_equal(gidx.cpu().numpy(), init_idx)
-    assert np.array_equal(gC.cpu().numpy().view(np.uint32), init.view(np.uint32))
-    _say(f"[scale] {w.name}: GPU {T - 1} and {T} fixed iterations")
-    _, Cprev, _, _ = km.kmeans_run(Xg, w.K, Cg, T - 1, fixed_iters=True)
-    lab, C, cnt, it = km.kmeans_run(Xg, w.K, Cg, T, fixed_iters=True)
-    assert it == T
-    Cprev, lab, C, cnt = Cprev.cpu().numpy(), lab.cpu().numpy(), C.cpu().numpy(), cnt.cpu().numpy()
-    idx = np.random.default_rng(99).choice(X.shape[0], sample, replace=False)
-    olab, d1, d2 = oracle.assign(X[idx], Cprev, with_dist=True)
-    check_labels(lab[idx], olab, oracle.gap_rel(d1, d2))
-    oC, ocnt = oracle.update(X, lab, w.K, Cprev)
-    assert np.array_equal(cnt, ocnt)
-    nbits = check_centers(C, oC)
-    _say(f"[scale] {w.name}: sampled labels match; centres differ in {nbits} coordinates")
-    del Xg
-
-
-def test_workload4_at_scale():
-    _stepwise_at_scale("4", 30)
-
-
-def test_workload5_at_scale():
-    _stepwise_at_scale("5", 30, sample=10_000)
