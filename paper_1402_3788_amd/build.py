@@ -41,16 +41,28 @@ def hipcc() -> str:
     return os.path.join(rocm, "bin", "hipcc")
 
 
-def build(verbose: bool = True, jobs: int = 8) -> str:
-    """Compile every source to an object file (in parallel), then link."""
+def _newest_header() -> float:
+    heads = [os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".h")]
+    heads.append(os.path.join(ROOT, "include", "kmeans.h"))
+    return max(os.path.getmtime(h) for h in heads)
+
+
+def build(verbose: bool = True, jobs: int = 8, incremental: bool = False) -> str:
+    """Compile every source to an object file (in parallel), then link.
+    incremental: skip objects newer than their source and every header."""
     objdir = os.path.join(HERE, "_build")
     os.makedirs(objdir, exist_ok=True)
     procs = []
     objs = []
     t0 = time.time()
+    head_t = _newest_header()
     for src, extra, oname in SOURCES:
         obj = os.path.join(objdir, oname)
         objs.append(obj)
+        if incremental and os.path.exists(obj):
+            ot = os.path.getmtime(obj)
+            if ot > os.path.getmtime(os.path.join(CSRC, src)) and ot > head_t:
+                continue
         cmd = [hipcc(), *HIPCC_FLAGS, *extra, "-c", os.path.join(CSRC, src), "-o", obj]
         procs.append((src, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)))
         while sum(p.poll() is None for _, p in procs) >= jobs:
@@ -78,4 +90,4 @@ def build(verbose: bool = True, jobs: int = 8) -> str:
 
 
 if __name__ == "__main__":
-    build()
+    build(incremental="--incremental" in sys.argv)

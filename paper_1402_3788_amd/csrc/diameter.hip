@@ -33,11 +33,14 @@
 //           e = x_j - c_j, d = d + e*e (features ascending, each operation
 //           rounded) and the lexicographic best (largest d, then lowest k,
 //           then lowest l) is kept.
-// B bounds |d~ - d| for every pair: with u = 2^-24 and gamma_m = m u / (1 - m u),
+// B bounds |d~ - d| for every pair: with u = 2^-24, gamma_m = m u / (1 - m u)
+// for this code's own round-to-nearest fp32 arithmetic and
+// phi_m = 2 m u / (1 - 2 m u) for the matrix core's additions (assumed only
+// faithful: each within 2^-23 relative, in any order or direction),
 //   |d~ - d| <= E (|y_k|^2 + |y_l|^2),
 //   E = 4.01 u (centring) + 4.03 * 2^-16 (dropped split terms, three per
 //       feature at most 3.02 * 2^-16 |a b|, and 2^-16 for each norm operand)
-//       + 1.01 gamma_M (the fp32 norms) + 2.02 gamma_{3P+2} (fp32 sums),
+//       + 1.01 gamma_M (the fp32 norms) + 2.02 phi_{3P+2} (the sums),
 // so B = 1.25 * 2.02 * E * max_i n_i covers every pair (1.25: margin). The
 // true pair has d~ >= D2 - B >= d~* - 2B, so it is always re-evaluated, and
 // the result is exact whatever the split products round to.
@@ -190,7 +193,8 @@ __device__ inline float diam_threshold(const uint32_t *counters, int M)
     constexpr int P = 32 * KS;
     const double u = 5.9604644775390625e-8;           // 2^-24
     auto gamma = [&](int m) { return m * u / (1.0 - m * u); };
-    const double E = 4.01 * u + 4.03 * 1.52587890625e-05 + 1.01 * gamma(M) + 2.02 * gamma(3 * P + 2);
+    auto phi = [&](int m) { return 2.0 * m * u / (1.0 - 2.0 * m * u); };
+    const double E = 4.01 * u + 4.03 * 1.52587890625e-05 + 1.01 * gamma(M) + 2.02 * phi(3 * P + 2);
     const double maxn = (double)__uint_as_float(counters[0]);
     const double B = 1.25 * 2.02 * E * maxn;
     const double thr = (double)key_float(counters[1]) - 2.0 * B;

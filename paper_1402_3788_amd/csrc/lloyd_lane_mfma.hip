@@ -10,9 +10,10 @@
 //      each 16-object block b = 0..3 -- two 16-byte loads per block, each
 //      starting at any float of a row (rows of M floats) and reading at most
 //      three floats into the next row, which the zero A operands past M ignore;
-//   2. accumulation loads (issued for the current tile, served by the cache
-//      the operand loads filled): lane (h, j) = (lane / 32, lane % 32) reads
-//      feature j of object s + 32h for s = 0..31;
+//   2. accumulation loads, issued right after the operand loads of the same
+//      tile so that both meet the same cache lines in flight (X crosses HBM
+//      and L2 once): lane (h, j) = (lane / 32, lane % 32) reads feature j of
+//      object s + 32h for s = 0..31;
 //   3. scores (Algorithm 1 steps 2/4, Eq. (2) in the expanded form
 //      score = |c|^2 - 2 x.c, |x|^2 being common to all centres): A = -2C
 //      (16 centres x 32 features, zero past K and M) and B = X^T, both split
@@ -28,10 +29,11 @@
 //      error bound, otherwise the object is re-decided over all centres with
 //      fp64 distances in the reference operation order (lowest index on ties),
 //      so every label is the exact-arithmetic argmin;
-//   5. accumulation (the numerator and denominator of Eq. (1)): lane l holds
-//      the slab row offset of object l (slab l / 32); in step s a swizzle
-//      broadcasts object s + 32h's offset to lanes (h, .), and lane (h, j)
-//      adds feature j to slab h with an LDS fp64 add. The two halves of a
+//   5. accumulation (the numerator and denominator of Eq. (1)): lane l
+//      writes the slab row offset of object l (slab l / 32) to the wave's
+//      offset table; lanes (h, .) read the offsets of objects 32h .. 32h+31
+//      back with broadcast 16-byte reads, and in step s lane (h, j) adds
+//      feature j of object s + 32h to slab h with an LDS fp64 add. The two halves of a
 //      wave add to different slabs and the lanes of a half to different
 //      columns, so no two lanes of one add meet on an address: every sum is
 //      formed in a fixed order (objects of the wave's tiles in ascending
@@ -82,41 +84,27 @@ typedef float f4v __attribute__((ext_vector_type(4)));
 // Four floats at any 4-byte-aligned address: rows of X start on any float.
 typedef float f4u __attribute__((ext_vector_type(4), aligned(4)));
 
-constexpr int kWaves = 12;            // waves per workgroup (3 per SIMD)
-constexpr int kMinWavesPerSimd = 3;   // caps registers at 168 per lane
+// Waves per workgroup: two per SIMD. The two register sets of the tile loads
+// in flight (operands and accumulation values, 64 registers each) take what a
+// third wave would need; measured at K = 16, M = 25, n = 2e6, two waves with
+// both loads in flight beat three with the accumulation loads issued a tile
+// later (whose lines have by then left the cache).
+constexpr int kWaves = 8;
+constexpr int kMinWavesPerSimd = 2;   // caps registers at 256 per lane
 constexpr int kMaxMLane = 32;         // features: four lane groups of eight
 [[maybe_unused]] constexpr int kMaxKLane = 16;        // centres: one 16-row A operand
 
-// LDS of a workgroup: [W][2][K][M] fp64 slabs, then [W][K] int32 counts.
+// LDS of a workgroup: [W][2][K][M] fp64 slabs, [W][K] int32 counts, then
+// [W][64] int32 slab offsets of the objects of the current tile.
 [[maybe_unused]] __host__ __device__ inline size_t lane_lds_bytes(int M, int K, int W)
 {
-    return (size_t)W * 2 * K * M * 8 + (size_t)W * K * 4;
+    return (size_t)W * 2 * K * M * 8 + (size_t)W * K * 4 + (size_t)W * kWave * 4;
 }
 
 // Object rows after the last row of a tile that the operand loads may touch
 // (up to three floats past a row): tiles whose rows have that many successors
 // in X take the unguarded loads.
-__host__ __device__ inline int64_t rows_after(int M) { return (3 + M - 1) / M; }
-
-// Broadcast of lane s of each 32-lane half (ds_swizzle in bit-mask mode: and
-// mask 0, or mask s).
-template <int S>
-[[maybe_unused]] __device__ inline int bcast32(int v)
-{
-    return __builtin_amdgcn_ds_swizzle(v, S << 5);
-}
-
-// f(integral_constant<int, S>) for S = 0 .. N-1, unrolled.
-template <class F, int... S>
-__device__ inline void static_for_impl(F &f, std::integer_sequence<int, S...>)
-{
-    (f(std::integral_constant<int, S>{}), ...);
-}
-template <int N, class F>
-__device__ inline void static_for(F &&f)
-{
-    static_for_impl(f, std::make_integer_sequence<int, N>{});
-}
+[[maybe_unused]] __host__ __device__ inline int64_t rows_after(int M) { return (3 + M - 1) / M; }
 
 // Comparisons of packed keys. A key is a float whose low bits were replaced
 // by an index, so the compiler cannot prove it canonical and would quieten it
@@ -221,7 +209,9 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
     constexpr bool kDist = MODE != kAccumLabels;
     extern __shared__ __align__(16) unsigned char smem[];
     const int W = blockDim.x / kWave;
-    const int wave = threadIdx.x / kWave;
+    // wave-uniform (scalar) wave index, so that tile addresses are scalar
+    // bases with 32-bit lane offsets
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int lane = threadIdx.x % kWave;
     const int g = lane >> 4, o16 = lane & 15;     // matrix layout
     const int h = lane >> 5, j = lane & 31;       // accumulation layout
@@ -231,6 +221,8 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
     double *slabs = reinterpret_cast<double *>(smem) + (size_t)wave * 2 * K * M;
     int32_t *cnts = reinterpret_cast<int32_t *>(reinterpret_cast<double *>(smem) +
                                                 (size_t)W * 2 * K * M) + wave * K;
+    int32_t *offs = reinterpret_cast<int32_t *>(reinterpret_cast<double *>(smem) +
+                                                (size_t)W * 2 * K * M) + W * K + wave * kWave;
     if (kAcc) {
         for (int i = lane; i < 2 * K * M; i += kWave) slabs[i] = 0.0;
         for (int i = lane; i < K; i += kWave) cnts[i] = 0;
@@ -282,11 +274,12 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
     const int c0 = 8 * g < M ? 8 * g : 0;
     const int c1 = 8 * g + 4 < M ? 8 * g + 4 : c0;
     auto load_ops = [&](int64_t q, f4v (&xb)[4][2]) {
-        const float *row = X + (q * kWave + o16) * (int64_t)M;
+        const float *tb = X + q * (kWave * M);                 // scalar
+        const int r0 = o16 * M;
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
-            xb[b][0] = *reinterpret_cast<const f4u *>(row + 16 * b * M + c0);
-            xb[b][1] = *reinterpret_cast<const f4u *>(row + 16 * b * M + c1);
+            xb[b][0] = *reinterpret_cast<const f4u *>(tb + (r0 + 16 * b * M + c0));
+            xb[b][1] = *reinterpret_cast<const f4u *>(tb + (r0 + 16 * b * M + c1));
         }
     };
     // guarded form for the last tiles: zero past n and past M
@@ -305,25 +298,31 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
 
     int nfallback = 0;
 
-    // One tile: kTail selects the guarded loads and validity tests.
-    // The accumulation loads of tile q go out first, then the operand loads of
-    // tile qn into nxt (unguarded form only), so that waiting for the former
-    // never waits for the latter; every load is unconditional, so the waits
-    // count them exactly.
-    auto step = [&](int64_t q, f4v (&xb)[4][2], f4v (&nxt)[4][2], int64_t qn, auto tail) {
+    // accumulation values of tile q (lane (h, j): feature j of objects
+    // 32h .. 32h+31; the guarded form reads zeros past n)
+    auto load_acc = [&](int64_t q, float (&xa)[32], auto tail) {
+        constexpr bool kTail = decltype(tail)::value;
+        const float *tb = X + q * (kWave * M);                 // scalar
+        const int c = 32 * h * M + jr;
+#pragma unroll
+        for (int s = 0; s < 32; ++s) {
+            if (kTail) xa[s] = (q * kWave + 32 * h + s < n) ? tb[c + s * M] : 0.f;
+            else xa[s] = tb[c + s * M];
+        }
+    };
+    // One tile (kTail: the guarded loads and validity tests): xb / xa hold its
+    // operand and accumulation values (loaded one tile earlier); the loads of
+    // tile qn go into nxt / xan first (unguarded form only). Every load is
+    // unconditional, so the waits count them exactly.
+    auto step = [&](int64_t q, f4v (&xb)[4][2], float (&xa)[32], f4v (&nxt)[4][2],
+                    float (&xan)[32], int64_t qn, auto tail) {
         constexpr bool kTail = decltype(tail)::value;
         const int64_t i = q * kWave + lane;           // this lane's object
         const bool valid = !kTail || i < n;
-        float xa[32];
-        if (kAcc) {
-            const float *col = X + (q * kWave + 32 * h) * (int64_t)M + jr;
-#pragma unroll
-            for (int s = 0; s < 32; ++s) {
-                if (kTail) xa[s] = (q * kWave + 32 * h + s < n) ? col[(int64_t)s * M] : 0.f;
-                else xa[s] = col[(int64_t)s * M];
-            }
+        if (!kTail) {
+            if (kDist) load_ops(qn, nxt);
+            if (kAcc) load_acc(qn, xan, std::false_type{});
         }
-        if (kDist && !kTail) load_ops(qn, nxt);
         int lab = 0;
         if (kDist) {
             uint32_t bh[4][4], bl[4][4];
@@ -407,11 +406,18 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
             if (adds) atomicAdd(cnts + lab, 1);
             // all 32 broadcasts first, then the adds (each add waits for its
             // broadcast; issued in between they would wait one by one)
+            // all 32 offsets first (8 broadcast reads), then the adds
             int o[32];
-            static_for<32>([&](auto sc) {
-                constexpr int s = decltype(sc)::value;
-                o[s] = bcast32<s>(my_off);
-            });
+            offs[lane] = my_off;
+            __builtin_amdgcn_wave_barrier();
+            {
+                const int4 *src = reinterpret_cast<const int4 *>(offs + 32 * h);
+#pragma unroll
+                for (int r = 0; r < 8; ++r) {
+                    const int4 v = src[r];
+                    o[4 * r] = v.x; o[4 * r + 1] = v.y; o[4 * r + 2] = v.z; o[4 * r + 3] = v.w;
+                }
+            }
             if (j < M) {
 #pragma unroll
                 for (int s = 0; s < 32; ++s)
@@ -426,20 +432,25 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
     // flight in the other register set; then the guarded tail tiles.
     // (The prefetch past a wave's last unguarded tile reloads tile nsafe - 1.)
     f4v xb[2][4][2];
+    float xa[2][32];
     int64_t q = q0;
     auto next = [&](int64_t qq) { return qq < nsafe ? qq : nsafe - 1; };
-    if (kDist && q < nsafe) load_ops(q, xb[0]);
+    if (q < nsafe) {
+        if (kDist) load_ops(q, xb[0]);
+        if (kAcc) load_acc(q, xa[0], std::false_type{});
+    }
     for (; q < nsafe; q += 2 * stride) {
-        step(q, xb[0], xb[1], next(q + stride), std::false_type{});
+        step(q, xb[0], xa[0], xb[1], xa[1], next(q + stride), std::false_type{});
         if (q + stride >= nsafe) {
             q += stride;
             break;
         }
-        step(q + stride, xb[1], xb[0], next(q + 2 * stride), std::false_type{});
+        step(q + stride, xb[1], xa[1], xb[0], xa[0], next(q + 2 * stride), std::false_type{});
     }
     for (; q < nt; q += stride) {
         if (kDist) load_ops_tail(q, xb[0]);
-        step(q, xb[0], xb[1], q, std::true_type{});
+        if (kAcc) load_acc(q, xa[0], std::true_type{});
+        step(q, xb[0], xa[0], xb[1], xa[1], q, std::true_type{});
     }
 
     if (ctl != nullptr && lane == 0 && nfallback > 0) atomicAdd(&ctl->fallbacks, nfallback);

@@ -12,14 +12,17 @@
 //   pass 1 (every tile): split precision on the bf16 matrix cores, three
 //     v_mfma_f32_16x16x32_bf16 per block on operands split into bf16 hi and
 //     lo parts rounded to nearest; each score is within E (3|c|^2 + |x|^2) of
-//     the exact one (E = 3.02 * 2^-16 + 1.03 gamma_{96 ceil(M/32) + 2}); the
+//     the exact one (E = 3.02 * 2^-16 + 1.01 (96 ceil(M/32) + 2 + M/6) 2^-23,
+//     assuming only that the matrix core rounds each addition faithfully); the
 //     scores are scanned as packed (score, index) keys, and a label is
 //     accepted when the two best keys differ by more than twice that bound
 //     plus the keys' truncation (with |c|^2 bounded by the largest centre
 //     norm and margins);
 //   pass 2 (tiles with a call too close for pass 1): fp32 products, a
 //     v_mfma_f32_16x16x4f32 chain over the features, whose error is bounded by
-//     gamma_{M+2} (3|c|^2 + |x|^2); a label is accepted at 2.5 times that;
+//     1.01 (4 ceil(M/4) + 3 + M/6) 2^-23 (3|c|^2 + |x|^2) under the same
+//     assumption (each product and each addition rounded faithfully); a label
+//     is accepted at 2.02 times that;
 //   the objects still too close are re-decided with fp64 distances in the
 //   fixed operation order, over all centres, lowest index on ties.
 //
@@ -271,8 +274,12 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
         __syncthreads();
     }
     const float cmax = (MODE != kAccumLabels) ? *s_cmax : 0.f;
-    // fp32 error bound of a score, relative to (3|c|^2 + |x|^2), with margins
-    constexpr float kGuard = 2.5f * 1.01f * (float)(M + 2) * 5.9604645e-8f;
+    // fp32 error bound of a pass-2 score, relative to (3|c|^2 + |x|^2): 4 KS
+    // products and 4 KS + 2 additions on the matrix core, each rounded
+    // faithfully (within 2^-23 relative, in any order and direction), and the
+    // fp32 |c|^2 (M fused multiply-adds, 2^-24 each, against 3|c|^2); twice
+    // that (two scores) with margins
+    constexpr float kGuard = 2.02f * 1.01f * ((float)(4 * KS + 3) + (float)M / 6.0f) * 1.1920929e-07f;
 
     const int g = lane >> 4, l16 = lane & 15;
     int nfallback = 0;
@@ -500,16 +507,19 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
             // with a = ah + al + ea, b = bh + bl + eb (|ea| <= 2^-16 |a|, |al|
             // <= 2^-8 (1 + 2^-8) |a|, likewise b) the dropped terms
             // (a - ea) eb + al bl + ea b are below 3.02 * 2^-16 |a b| per
-            // feature; the products are exact in fp32 and their fp32 sums with
-            // |c|^2 add gamma_{96 KC + 2} of the terms' magnitudes; |c|^2 in
-            // fp32 adds gamma_M |c|^2. With 2|c_j x_j| <= c_j^2 + x_j^2 each
-            // score is within E (|x|^2 + 3|c|^2), E = 3.02 * 2^-16 + 1.03 gamma.
+            // feature; the products are exact in fp32 and their sums with |c|^2
+            // take at most 96 KC + 2 roundings on the matrix core, each assumed
+            // only faithful (within 2^-23 relative, any order or direction), so
+            // they add (96 KC + 2) 2^-23 of the terms' magnitudes; |c|^2 in fp32
+            // adds M 2^-24 |c|^2. With 2|c_j x_j| <= c_j^2 + x_j^2 each score is
+            // within E (|x|^2 + 3|c|^2), E = 3.02 * 2^-16 + 1.01 (96 KC + 2 + M/6) 2^-23.
             // A packed key moves its score by less than 2^(bits - 23) of the
             // score's magnitude, itself below (1 + E)(|x|^2 + 3|c|^2). So the
             // label stands when the two best keys differ by more than twice
             // E + 1.01 * 2^(bits - 23) (with margins).
             const float key_rel = __uint_as_float((uint32_t)(127 - 23 + kbits) << 23);   // 2^(bits-23)
-            const float e1 = 3.02f * 1.5258789e-05f + 1.03f * (float)(96 * KC + 2) * 5.9604645e-8f +
+            const float e1 = 3.02f * 1.5258789e-05f +
+                             1.01f * ((float)(96 * KC + 2) + (float)M / 6.0f) * 1.1920929e-07f +
                              1.01f * key_rel;
             const float thr1 = 2.02f * e1 * (3.02f * cmax + 1.0001f * mx) + 1e-30f;
             bool ok = !force64 && ((K == 1) || (mb2 - mb1 > thr1));

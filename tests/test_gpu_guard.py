@@ -1,0 +1,124 @@
+"""Calls accepted just outside the guard band of the split-precision scores.
+
+Both matrix-core distance kernels take a label from bf16 split-precision scores
+only when the two best scores differ by more than a proven bound on their
+error (Eq. (2) in the expanded form; the bound assumes no more than faithful
+rounding of the matrix core's additions), and re-decide every other object
+with fp64 distances. The re-decision path is exercised elsewhere with objects
+on bisectors; here every object is built so that its exact best-vs-second gap
+lies between 1.0 and 1.3 times the kernel's threshold, so that the kernel
+accepts it from the split-precision scores, and its label must still equal the
+oracle's. Were the true error of the scores larger than the bound, such calls
+are where labels would go wrong.
+
+The objects are built on the host from exact arithmetic: a point of the
+bisector hyperplane of two centres a and b, moved towards a by the distance
+that makes |x - b|^2 - |x - a|^2 equal to the target gap; after rounding x to
+fp32 the gap and the threshold are recomputed in fp64 and only objects with
+the ratio in [1.0, 1.3] are kept.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_1402_3788_amd as km
+
+pytestmark = pytest.mark.gpu
+
+DEV = torch.device("cuda:0") if torch.cuda.is_available() else None
+U23 = 2.0 ** -23
+
+
+def lane_threshold(cmax, xsq):
+    """One object per lane, K <= 16 (keys carry 4 index bits)."""
+    E = 3.02 * 2.0 ** -16 + 104 * U23 + 1.01 * 2.0 ** -19
+    return 2.02 * E * (3.02 * cmax + 1.0001 * xsq) + 1e-30
+
+
+def tile_threshold(cmax, xsq, K, M):
+    """64-object tiles, first pass (keys carry enough bits for the padded K)."""
+    KC = (M + 31) // 32
+    KT = ((K + 15) // 16 + 1) // 2 * 2
+    bits = 5 if KT <= 2 else 6 if KT <= 4 else 7 if KT <= 8 else 8
+    e1 = 3.02 * 2.0 ** -16 + 1.01 * (96 * KC + 2 + M / 6.0) * U23 + 1.01 * 2.0 ** (bits - 23)
+    return 2.02 * e1 * (3.02 * cmax + 1.0001 * xsq) + 1e-30
+
+
+def near_threshold_objects(C, n, thr_fn, seed, live):
+    """n objects whose exact gap between their two nearest centres is 1.0 to
+    1.3 times thr_fn(cmax, |x|^2); only the features flagged in `live` are
+    non-zero."""
+    rng = np.random.default_rng(seed)
+    K, M = C.shape
+    Cd = C.astype(np.float64)
+    cmax = float(np.max(np.sum(C.astype(np.float32) ** 2, axis=1, dtype=np.float32)))
+    out = []
+    while len(out) < n:
+        a, b = rng.choice(K, 2, replace=False)
+        d = Cd[a] - Cd[b]
+        dist = np.linalg.norm(d)
+        u = d / dist
+        mid = 0.5 * (Cd[a] + Cd[b])
+        noise = rng.standard_normal(M) * live * 0.05 * dist
+        noise -= np.dot(noise, u) * u                        # stay on the bisector
+        p = mid + noise
+        xsq = float(np.dot(p, p))
+        f = rng.uniform(1.05, 1.25)
+        lam = f * thr_fn(cmax, xsq) / (2.0 * dist)          # |x-b|^2 - |x-a|^2 = 2 lam dist
+        x = (p + lam * u).astype(np.float32)
+        xd = x.astype(np.float64)
+        dists = np.sum((xd - Cd) ** 2, axis=1)
+        order = np.argsort(dists)
+        if order[0] != a or order[1] != b:
+            continue
+        gap = dists[order[1]] - dists[order[0]]
+        ratio = gap / thr_fn(cmax, float(np.dot(xd, xd)))
+        if 1.0 <= ratio <= 1.3:
+            out.append(x)
+    return np.stack(out)
+
+
+def _run_one_pass(X, C, path):
+    n, M = X.shape
+    K = C.shape[0]
+    flags = {"mfma": km.KMEANS_PATH_MFMA, "tiles": km.KMEANS_PATH_TILES}[path]
+    ws = km.workspace(n, M, K, DEV, flags | km.KMEANS_FIXED_ITERS)
+    lab, _, _, _ = km.kmeans_run(torch.from_numpy(X).to(DEV), K, torch.from_numpy(C).to(DEV), 1,
+                                 fixed_iters=True, path=path, ws=ws)
+    return lab.cpu().numpy(), km.ctl_fallbacks(ws), km.ctl_reruns(ws)
+
+
+@pytest.mark.parametrize("K", [16, 9])
+def test_lane_kernel_accepts_near_threshold(K):
+    # features 0..6 and 24 are zero, so the lane kernel's |x|^2 (which adds
+    # the squares of a few floats past each row, the next object's first
+    # features) is exactly |x|^2 and its threshold the one computed here
+    M = 25
+    live = np.ones(M)
+    live[:7] = 0
+    live[24] = 0
+    rng = np.random.default_rng(K)
+    C = (rng.uniform(-50, 50, (K, M)) * live).astype(np.float32)
+    X = near_threshold_objects(C, 6000, lane_threshold, K + 1, live)
+    lab, fallbacks, _ = _run_one_pass(X, C, "mfma")
+    olab = oracle.assign(X, C)
+    print(f"[guard lane] K={K}: {len(X)} objects at 1.0-1.3 x the threshold, "
+          f"{fallbacks} re-decided in fp64", flush=True)
+    assert np.array_equal(lab, olab)
+    assert fallbacks < len(X) // 4          # the calls were accepted, not re-decided
+
+
+@pytest.mark.parametrize("K,M", [(64, 25), (256, 25)])
+def test_tile_kernel_accepts_near_threshold(K, M):
+    live = np.ones(M)
+    rng = np.random.default_rng(K + M)
+    C = rng.uniform(-50, 50, (K, M)).astype(np.float32)
+    thr = lambda cmax, xsq: tile_threshold(cmax, xsq, K, M)   # noqa: E731
+    X = near_threshold_objects(C, 6000, thr, K + M + 1, live)
+    lab, fallbacks, reruns = _run_one_pass(X, C, "tiles")
+    olab = oracle.assign(X, C)
+    print(f"[guard tile] K={K}: {len(X)} objects at 1.0-1.3 x the first-pass threshold, "
+          f"{reruns} tiles recomputed, {fallbacks} re-decided in fp64", flush=True)
+    assert np.array_equal(lab, olab)
+    assert reruns < (len(X) // 64) // 4
