@@ -266,6 +266,26 @@ def main():
            torch.empty(K, dtype=torch.int32, device=dev))
     ws = km.workspace(n, M, K, dev, flags)
 
+    # Kernel and iteration times from HIP events recorded by the library on
+    # the launch stream: PROTOCOL_RUNS fixed-count calls of PROTOCOL_ITERS
+    # iterations with events around every call, and PROTOCOL_RUNS calls with
+    # events around every assign + accumulate launch; medians over the calls.
+    # They run before the timed region, which they also bring out of the
+    # idle state (low clocks) the input generation left the GPU in.
+    it_us, k_us = [], []
+    nsamp = 0
+    for _ in range(PROTOCOL_RUNS):
+        # events only around the call (and the first launch): iteration time
+        _, _, _, _, tm = km.kmeans_run(Xg, K, Cg, PROTOCOL_ITERS, fixed_iters=True, path=path,
+                                       timing=True, sample_every=PROTOCOL_ITERS + 1, out=out,
+                                       ws=ws)
+        it_us.append(tm.step_ms * 1e3 / tm.step_launches)
+    for _ in range(PROTOCOL_RUNS):
+        # events around every assign + accumulate launch: the kernel's duration
+        _, _, _, _, tm = km.kmeans_run(Xg, K, Cg, PROTOCOL_KERNEL_ITERS, fixed_iters=True,
+                                       path=path, timing=True, sample_every=1, out=out, ws=ws)
+        k_us.append(tm.assign_ms * 1e3 / tm.assign_samples)
+        nsamp += tm.assign_samples
     # warmup
     km.kmeans_run(Xg, K, Cg, max(1, args.warmup), fixed_iters=True, path=path, out=out, ws=ws)
     torch.cuda.synchronize()
@@ -286,24 +306,6 @@ def main():
     bytes_per_point = 4 * M + 4                    # read the object once, write its label
     launch_bytes = n * bytes_per_point
 
-    # kernel and iteration times from HIP events recorded by the library on
-    # the launch stream: PROTOCOL_RUNS further fixed-count calls of
-    # PROTOCOL_ITERS iterations, events around every call and around every
-    # assign + accumulate launch; medians over the calls
-    it_us, k_us = [], []
-    nsamp = 0
-    for _ in range(PROTOCOL_RUNS):
-        # events only around the call (and the first launch): iteration time
-        _, _, _, _, tm = km.kmeans_run(Xg, K, Cg, PROTOCOL_ITERS, fixed_iters=True, path=path,
-                                       timing=True, sample_every=PROTOCOL_ITERS + 1, out=out,
-                                       ws=ws)
-        it_us.append(tm.step_ms * 1e3 / tm.step_launches)
-    for _ in range(PROTOCOL_RUNS):
-        # events around every assign + accumulate launch: the kernel's duration
-        _, _, _, _, tm = km.kmeans_run(Xg, K, Cg, PROTOCOL_KERNEL_ITERS, fixed_iters=True,
-                                       path=path, timing=True, sample_every=1, out=out, ws=ws)
-        k_us.append(tm.assign_ms * 1e3 / tm.assign_samples)
-        nsamp += tm.assign_samples
     iteration_us = statistics.median(it_us)
     assign_us = statistics.median(k_us)
     achieved = launch_bytes / (assign_us * 1e-6) / 1e9
