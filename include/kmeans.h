@@ -223,6 +223,30 @@ int kmeans_run(const float *X, int64_t n, int32_t M, int32_t K, const float *ini
                int32_t *counts, int32_t *iterations, void *workspace,
                size_t workspace_bytes, void *stream, kmeans_timing_t *timing);
 
+/*
+ * kmeans_run without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation). Same arguments, results and behaviour as
+ * kmeans_run with timing == NULL, except:
+ *   - the workspace is a static array the library holds on each GPU it runs
+ *     on (KMEANS_NOALLOC_MAX_WORKSPACE bytes, reserved when the library is
+ *     loaded on the device and kept until the process ends); a shape whose
+ *     kmeans_workspace_bytes(n, M, K, flags) exceeds it returns
+ *     KMEANS_EWORKSPACE with nothing enqueued;
+ *   - the call allocates nothing: no device or pinned host memory, no events
+ *     (the control block is read back into host stack memory);
+ *   - every call on one GPU uses that GPU's one array: calls that overlap on
+ *     a GPU (other host threads, or other streams) race and give undefined
+ *     results. Each call starts by clearing what must start at zero, so
+ *     consecutive calls need nothing in between.
+ * The current HIP device selects the array; `stream` must belong to it.
+ * Synchronous, like kmeans_run.
+ */
+#define KMEANS_NOALLOC_MAX_WORKSPACE ((size_t)16 << 20)
+int kmeans_run_noalloc(const float *X, int64_t n, int32_t M, int32_t K, const float *init_centers,
+                       int32_t max_iter, uint32_t flags, int32_t *labels, float *centers,
+                       int32_t *counts, int32_t *iterations, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

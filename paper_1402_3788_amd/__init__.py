@@ -13,6 +13,7 @@ Entry points (same names as the C ABI):
     kmeans_init_farthest(X, K, ws=None) -> (init_idx, centers)
     kmeans_centroid(X, ws=None) -> centroid
     kmeans_diameter(X, ws=None) -> (d2, pair, centroid)
+    kmeans_run_noalloc(X, K, init_centers, max_iter, out, ...) -> iterations
     kmeans_workspace_bytes(n, M, K, flags=0), kmeans_init_workspace_bytes(n, M, K),
     kmeans_strerror(code)
 """
@@ -43,7 +44,7 @@ EXPORTED = ("kmeans_workspace_bytes", "kmeans_strerror", "kmeans_assign", "kmean
             "kmeans_run", "kmeans_init_workspace_bytes", "kmeans_init_farthest",
             "kmeans_init_farthest_from",
             "kmeans_centroid_workspace_bytes", "kmeans_centroid",
-            "kmeans_diameter_workspace_bytes", "kmeans_diameter")
+            "kmeans_diameter_workspace_bytes", "kmeans_diameter", "kmeans_run_noalloc")
 
 
 class KmeansTiming(ctypes.Structure):
@@ -89,6 +90,8 @@ def _load() -> ctypes.CDLL:
     lib.kmeans_diameter_workspace_bytes.restype = sz
     lib.kmeans_diameter.argtypes = [p, i64, i32, p, p, p, p, sz, p]
     lib.kmeans_diameter.restype = ctypes.c_int
+    lib.kmeans_run_noalloc.argtypes = [p, i64, i32, i32, p, i32, u32, p, p, p, p, p]
+    lib.kmeans_run_noalloc.restype = ctypes.c_int
     return lib
 
 
@@ -306,6 +309,30 @@ def kmeans_run(X: torch.Tensor, K: int, init_centers: torch.Tensor, max_iter: in
         raise KmeansError("kmeans_run", rc)
     res = (labels, centers, counts, int(iters.value))
     return res + (tm,) if timing else res
+
+
+NOALLOC_MAX_WORKSPACE = 16 << 20      # KMEANS_NOALLOC_MAX_WORKSPACE
+
+
+def kmeans_run_noalloc(X: torch.Tensor, K: int, init_centers: torch.Tensor, max_iter: int,
+                       out, fixed_iters: bool = False, path=None, metric: str = "l2",
+                       force_fp64: bool = False) -> int:
+    """kmeans_run on the library's static per-GPU workspace (no allocation in
+    the call): `out` = (labels, centers, counts) tensors to fill. Returns the
+    iteration count."""
+    _check_x(X)
+    n, M = X.shape
+    init = init_centers.contiguous()
+    labels, centers, counts = out
+    flags = (_flags(path) | _metric(metric) | (KMEANS_FIXED_ITERS if fixed_iters else 0)
+             | (KMEANS_FORCE_FP64 if force_fp64 else 0))
+    iters = ctypes.c_int32(0)
+    rc = _lib.kmeans_run_noalloc(_dev_ptr(X), n, M, int(K), _dev_ptr(init), int(max_iter), flags,
+                                 _dev_ptr(labels), _dev_ptr(centers), _dev_ptr(counts),
+                                 ctypes.byref(iters), _stream_ptr(X.device))
+    if rc:
+        raise KmeansError("kmeans_run_noalloc", rc)
+    return int(iters.value)
 
 
 def ctl_fallbacks(ws: torch.Tensor) -> int:

@@ -7,6 +7,8 @@
 #include "farthest.h"
 #include "diameter.h"
 
+#include <mutex>
+
 
 using namespace lloyd;
 
@@ -169,6 +171,170 @@ bool diameter_fits(int64_t n, int32_t M)
 {
     const DiameterPlan p = plan_diameter(n, M);
     return p.chunks <= 65535 && p.row_blocks <= INT32_MAX;
+}
+
+
+// Workspace of kmeans_run_noalloc: one array per GPU, allocated with the code
+// object when the library is loaded on a device and kept until the process
+// ends. In host code `scratch` names a host-side stand-in, not the device
+// array: its device address, which differs from GPU to GPU, comes from
+// hipGetSymbolAddress with the device current, once per device, and only that
+// address is ever handed to kernels or copies.
+constexpr size_t kScratchBytes = KMEANS_NOALLOC_MAX_WORKSPACE;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+int scratch_on_current_device(char **out)
+{
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static char *addr[kMaxDevices] = {};
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return KMEANS_EHIP;
+    std::lock_guard<std::mutex> lock(mu);
+    if (addr[dev] == nullptr) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr)
+            return KMEANS_EHIP;
+        addr[dev] = static_cast<char *>(p);
+    }
+    *out = addr[dev];
+    return KMEANS_OK;
+}
+
+// Arguments of kmeans_run that need no workspace (the shared validation).
+int check_run(const float *X, int64_t n, int32_t M, int32_t K, const float *init_centers,
+              int32_t max_iter, uint32_t flags, const int32_t *labels, const float *centers,
+              const int32_t *counts, const int32_t *iterations)
+{
+    if (!X || !init_centers || !labels || !centers || !counts || !iterations) return KMEANS_EINVAL;
+    int rc = check_shape(n, M, K);
+    if (rc) return rc;
+    if (max_iter < 1) return KMEANS_EINVAL;
+    if ((rc = check_flags(flags))) return rc;
+    if (!aligned16(X)) return KMEANS_EINVAL;
+    if (select_path(M, K, flags) < 0) return KMEANS_EUNSUPPORTED;
+    return KMEANS_OK;
+}
+
+// The Lloyd loop on a validated call; ws holds L.total bytes. With
+// may_allocate false nothing is allocated: no events (timing must be null) and
+// the control block is read back into pageable host memory.
+int run_impl(const float *X, int64_t n, int32_t M, int32_t K, const float *init_centers,
+             int32_t max_iter, uint32_t flags, int32_t *labels, float *centers, int32_t *counts,
+             int32_t *iterations, const Layout &L, char *ws, hipStream_t s,
+             kmeans_timing_t *timing, bool may_allocate)
+{
+    int rc = KMEANS_OK;
+    const int fixed = (flags & KMEANS_FIXED_ITERS) ? 1 : 0;
+    const bool l1 = (flags & KMEANS_METRIC_L1) != 0;
+    const L1Plan p1 = l1 ? plan_l1(n, M, K) : L1Plan{};
+    if (l1 && p1.waves < 1) return KMEANS_EUNSUPPORTED;
+    const int every = timing == nullptr ? 0 : (timing->sample_every > 0 ? timing->sample_every : 16);
+    // events: one before the first launch, one after the last, and a pair
+    // around each sampled assign launch
+    constexpr int kMaxSamples = 64;
+    int nsampled = every > 0 ? (max_iter + every - 1) / every : 0;
+    if (nsampled > kMaxSamples) nsampled = kMaxSamples;
+
+    RunCache &cache = run_cache();
+    if (timing && !may_allocate) return KMEANS_EINVAL;
+    if (timing) {
+        while (cache.nev < 2 + 2 * nsampled) {
+            if (hipEventCreate(&cache.ev[cache.nev]) != hipSuccess) return KMEANS_EHIP;
+            ++cache.nev;
+        }
+    }
+    if (may_allocate && cache.pinned == nullptr) {
+        void *p = nullptr;
+        if (hipHostMalloc(&p, sizeof(Ctl), hipHostMallocDefault) == hipSuccess)
+            cache.pinned = static_cast<Ctl *>(p);
+    }
+    Ctl pageable{};
+    Ctl *host = (may_allocate && cache.pinned != nullptr) ? cache.pinned : &pageable;
+
+    StepArgs a{};
+    a.X = X; a.n = n; a.M = M; a.K = K;
+    a.labels = labels;
+    a.centers_out = centers;     // centres are updated in place, iteration by iteration
+    a.counts_out = counts;
+    bind_workspace(a, L, ws);
+    a.fixed = fixed;
+    a.compare = 1;
+    a.force64 = (flags & KMEANS_FORCE_FP64) ? 1 : 0;
+    a.labels_in = labels;        // the L1 form accumulates from the labels it wrote
+    Ctl *ctl = a.ctl;
+
+    if ((rc = hip_status(launch_ctl_reset(ctl, s)))) return rc;
+
+    int nev = 0;
+    auto mark = [&]() -> int {
+        if (!timing) return KMEANS_OK;
+        return hip_status(hipEventRecord(cache.ev[nev++], s));
+    };
+
+    // Two launches per iteration: assign + accumulate (fused), then the centres
+    // and the congruence test from the workgroup partials. Iteration t assigns
+    // with the centres of iteration t - 1: the caller's initial centres for
+    // t = 1 (read in place; nothing is copied), `centers` afterwards, which
+    // every centres launch writes whole.
+    // Enqueue iterations in chunks; between chunks (early-stop mode only) read
+    // the control block to learn whether the centres have become congruent.
+    // Launches past convergence return at their first instruction.
+    int t = 1, chunk = 3, launched = 0;
+    rc = mark();
+    while (!rc && t <= max_iter) {
+        // fixed-count runs enqueue everything at once; otherwise chunks grow 3, 6, 12, ...
+        const int end = (fixed || t + chunk - 1 >= max_iter) ? max_iter : t + chunk - 1;
+        for (int tt = t; tt <= end && !rc; ++tt) {
+            a.t = tt;
+            a.C = tt == 1 ? init_centers : centers;
+            const bool sampled =
+                every > 0 && (tt - 1) % every == 0 && (tt - 1) / every < kMaxSamples;
+            if (sampled) rc = mark();
+            if (!rc && l1) {
+                // L1: assign, then the sums of Eq. (1) from those labels
+                rc = hip_status(launch_l1(a, p1, s));
+                if (!rc && sampled) rc = mark();
+                if (!rc) rc = hip_status(launch_step(a, kAccumLabels, L.plan, s));
+            } else if (!rc) {
+                rc = hip_status(launch_step(a, kAssignAccum, L.plan, s));
+                if (!rc && sampled) rc = mark();
+            }
+            if (!rc) rc = hip_status(launch_centres(a, L.plan.groups, s));
+            ++launched;
+        }
+        t = end + 1;
+        if (rc || t > max_iter) break;
+        rc = hip_status(hipMemcpyAsync(host, ctl, sizeof(Ctl), hipMemcpyDeviceToHost, s));
+        if (!rc) rc = hip_status(hipStreamSynchronize(s));
+        if (rc || host->converged_at != 0) break;
+        chunk = chunk * 2 < 64 ? chunk * 2 : 64;
+    }
+    if (!rc) rc = mark();
+    if (!rc) rc = hip_status(hipMemcpyAsync(host, ctl, sizeof(Ctl), hipMemcpyDeviceToHost, s));
+    if (!rc) rc = hip_status(hipStreamSynchronize(s));
+    if (rc) return rc;
+    *iterations = host->converged_at != 0 ? host->converged_at : max_iter;
+    if (host->ring_stalls != 0) rc = KMEANS_EHIP;
+
+    if (timing) {
+        timing->step_ms = 0.0;
+        timing->assign_ms = 0.0;
+        timing->step_launches = launched;
+        timing->assign_samples = 0;
+        timing->reserved = 0;
+        float ms = 0.f;
+        if (nev < 2 || hipEventElapsedTime(&ms, cache.ev[0], cache.ev[nev - 1]) != hipSuccess)
+            return KMEANS_EHIP;
+        timing->step_ms = ms;
+        for (int e = 1; e + 2 < nev; e += 2) {
+            if (hipEventElapsedTime(&ms, cache.ev[e], cache.ev[e + 1]) != hipSuccess)
+                return KMEANS_EHIP;
+            timing->assign_ms += ms;
+            timing->assign_samples++;
+        }
+    }
+    return rc;
 }
 
 }  // namespace
@@ -340,126 +506,29 @@ int kmeans_run(const float *X, int64_t n, int32_t M, int32_t K, const float *ini
                int32_t *iterations, void *workspace, size_t workspace_bytes, void *stream,
                kmeans_timing_t *timing)
 {
-    if (!X || !init_centers || !labels || !centers || !counts || !iterations) return KMEANS_EINVAL;
-    int rc = check_shape(n, M, K);
+    int rc = check_run(X, n, M, K, init_centers, max_iter, flags, labels, centers, counts,
+                       iterations);
     if (rc) return rc;
-    if (max_iter < 1) return KMEANS_EINVAL;
-    if ((rc = check_flags(flags))) return rc;
-    if (!aligned16(X)) return KMEANS_EINVAL;
-    if (select_path(M, K, flags) < 0) return KMEANS_EUNSUPPORTED;
     const Layout L = layout(n, M, K, flags);
     if (!workspace || workspace_bytes < L.total) return KMEANS_EWORKSPACE;
+    return run_impl(X, n, M, K, init_centers, max_iter, flags, labels, centers, counts,
+                    iterations, L, static_cast<char *>(workspace),
+                    static_cast<hipStream_t>(stream), timing, true);
+}
 
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    const int fixed = (flags & KMEANS_FIXED_ITERS) ? 1 : 0;
-    const bool l1 = (flags & KMEANS_METRIC_L1) != 0;
-    const L1Plan p1 = l1 ? plan_l1(n, M, K) : L1Plan{};
-    if (l1 && p1.waves < 1) return KMEANS_EUNSUPPORTED;
-    const int every = timing == nullptr ? 0 : (timing->sample_every > 0 ? timing->sample_every : 16);
-    // events: one before the first launch, one after the last, and a pair
-    // around each sampled assign launch
-    constexpr int kMaxSamples = 64;
-    int nsampled = every > 0 ? (max_iter + every - 1) / every : 0;
-    if (nsampled > kMaxSamples) nsampled = kMaxSamples;
-
-    RunCache &cache = run_cache();
-    if (timing) {
-        while (cache.nev < 2 + 2 * nsampled) {
-            if (hipEventCreate(&cache.ev[cache.nev]) != hipSuccess) return KMEANS_EHIP;
-            ++cache.nev;
-        }
-    }
-    if (cache.pinned == nullptr) {
-        void *p = nullptr;
-        if (hipHostMalloc(&p, sizeof(Ctl), hipHostMallocDefault) == hipSuccess)
-            cache.pinned = static_cast<Ctl *>(p);
-    }
-    Ctl pageable{};
-    Ctl *host = cache.pinned != nullptr ? cache.pinned : &pageable;
-
-    StepArgs a{};
-    a.X = X; a.n = n; a.M = M; a.K = K;
-    a.labels = labels;
-    a.centers_out = centers;     // centres are updated in place, iteration by iteration
-    a.counts_out = counts;
-    bind_workspace(a, L, static_cast<char *>(workspace));
-    a.fixed = fixed;
-    a.compare = 1;
-    a.force64 = (flags & KMEANS_FORCE_FP64) ? 1 : 0;
-    a.labels_in = labels;        // the L1 form accumulates from the labels it wrote
-    Ctl *ctl = a.ctl;
-
-    if ((rc = hip_status(launch_ctl_reset(ctl, s)))) return rc;
-
-    int nev = 0;
-    auto mark = [&]() -> int {
-        if (!timing) return KMEANS_OK;
-        return hip_status(hipEventRecord(cache.ev[nev++], s));
-    };
-
-    // Two launches per iteration: assign + accumulate (fused), then the centres
-    // and the congruence test from the workgroup partials. Iteration t assigns
-    // with the centres of iteration t - 1: the caller's initial centres for
-    // t = 1 (read in place; nothing is copied), `centers` afterwards, which
-    // every centres launch writes whole.
-    // Enqueue iterations in chunks; between chunks (early-stop mode only) read
-    // the control block to learn whether the centres have become congruent.
-    // Launches past convergence return at their first instruction.
-    int t = 1, chunk = 3, launched = 0;
-    rc = mark();
-    while (!rc && t <= max_iter) {
-        // fixed-count runs enqueue everything at once; otherwise chunks grow 3, 6, 12, ...
-        const int end = (fixed || t + chunk - 1 >= max_iter) ? max_iter : t + chunk - 1;
-        for (int tt = t; tt <= end && !rc; ++tt) {
-            a.t = tt;
-            a.C = tt == 1 ? init_centers : centers;
-            const bool sampled =
-                every > 0 && (tt - 1) % every == 0 && (tt - 1) / every < kMaxSamples;
-            if (sampled) rc = mark();
-            if (!rc && l1) {
-                // L1: assign, then the sums of Eq. (1) from those labels
-                rc = hip_status(launch_l1(a, p1, s));
-                if (!rc && sampled) rc = mark();
-                if (!rc) rc = hip_status(launch_step(a, kAccumLabels, L.plan, s));
-            } else if (!rc) {
-                rc = hip_status(launch_step(a, kAssignAccum, L.plan, s));
-                if (!rc && sampled) rc = mark();
-            }
-            if (!rc) rc = hip_status(launch_centres(a, L.plan.groups, s));
-            ++launched;
-        }
-        t = end + 1;
-        if (rc || t > max_iter) break;
-        rc = hip_status(hipMemcpyAsync(host, ctl, sizeof(Ctl), hipMemcpyDeviceToHost, s));
-        if (!rc) rc = hip_status(hipStreamSynchronize(s));
-        if (rc || host->converged_at != 0) break;
-        chunk = chunk * 2 < 64 ? chunk * 2 : 64;
-    }
-    if (!rc) rc = mark();
-    if (!rc) rc = hip_status(hipMemcpyAsync(host, ctl, sizeof(Ctl), hipMemcpyDeviceToHost, s));
-    if (!rc) rc = hip_status(hipStreamSynchronize(s));
+int kmeans_run_noalloc(const float *X, int64_t n, int32_t M, int32_t K, const float *init_centers,
+                       int32_t max_iter, uint32_t flags, int32_t *labels, float *centers,
+                       int32_t *counts, int32_t *iterations, void *stream)
+{
+    int rc = check_run(X, n, M, K, init_centers, max_iter, flags, labels, centers, counts,
+                       iterations);
     if (rc) return rc;
-    *iterations = host->converged_at != 0 ? host->converged_at : max_iter;
-    if (host->ring_stalls != 0) rc = KMEANS_EHIP;
-
-    if (timing) {
-        timing->step_ms = 0.0;
-        timing->assign_ms = 0.0;
-        timing->step_launches = launched;
-        timing->assign_samples = 0;
-        timing->reserved = 0;
-        float ms = 0.f;
-        if (nev < 2 || hipEventElapsedTime(&ms, cache.ev[0], cache.ev[nev - 1]) != hipSuccess)
-            return KMEANS_EHIP;
-        timing->step_ms = ms;
-        for (int e = 1; e + 2 < nev; e += 2) {
-            if (hipEventElapsedTime(&ms, cache.ev[e], cache.ev[e + 1]) != hipSuccess)
-                return KMEANS_EHIP;
-            timing->assign_ms += ms;
-            timing->assign_samples++;
-        }
-    }
-    return rc;
+    const Layout L = layout(n, M, K, flags);
+    if (L.total > kScratchBytes) return KMEANS_EWORKSPACE;
+    char *ws = nullptr;
+    if ((rc = scratch_on_current_device(&ws))) return rc;
+    return run_impl(X, n, M, K, init_centers, max_iter, flags, labels, centers, counts,
+                    iterations, L, ws, static_cast<hipStream_t>(stream), nullptr, false);
 }
 
 }  // extern "C"
