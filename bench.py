@@ -44,7 +44,7 @@ HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, vendor peak
 PROFILES = os.path.join(ROOT, "profiles")
 CSRC = os.path.join(ROOT, "paper_1402_3788_amd", "csrc")
 METRIC = "Lloyd iters/sec and points·iters/sec at n=2e6,M=25,K=16; % of HBM peak"
-PROTOCOL_RUNS = 10          # calls timed with events after the timed region
+PROTOCOL_RUNS = 10          # calls timed with events before the timed region
 PROTOCOL_ITERS = 100        # iterations per such call (iteration time)
 PROTOCOL_KERNEL_ITERS = 20  # iterations per call with every assign launch timed
 
@@ -266,10 +266,12 @@ def main():
            torch.empty(K, dtype=torch.int32, device=dev))
     ws = km.workspace(n, M, K, dev, flags)
 
-    # Kernel and iteration times from HIP events recorded by the library on
-    # the launch stream: PROTOCOL_RUNS fixed-count calls of PROTOCOL_ITERS
-    # iterations with events around every call, and PROTOCOL_RUNS calls with
-    # events around every assign + accumulate launch; medians over the calls.
+    # Kernel and iteration times from HIP events of the library's own: on
+    # the launch stream, PROTOCOL_RUNS fixed-count calls of PROTOCOL_ITERS
+    # iterations with events around every call, and PROTOCOL_RUNS calls whose
+    # every assign + accumulate launch is made with a pair of events that its
+    # dispatch stamps at start and end (the kernel's own duration, as a kernel
+    # trace reports it); medians over the calls.
     # They run before the timed region, which they also bring out of the
     # idle state (low clocks) the input generation left the GPU in.
     it_us, k_us = [], []
@@ -281,7 +283,7 @@ def main():
                                        ws=ws)
         it_us.append(tm.step_ms * 1e3 / tm.step_launches)
     for _ in range(PROTOCOL_RUNS):
-        # events around every assign + accumulate launch: the kernel's duration
+        # every assign + accumulate launch stamped by its dispatch: the kernel's duration
         _, _, _, _, tm = km.kmeans_run(Xg, K, Cg, PROTOCOL_KERNEL_ITERS, fixed_iters=True,
                                        path=path, timing=True, sample_every=1, out=out, ws=ws)
         k_us.append(tm.assign_ms * 1e3 / tm.assign_samples)

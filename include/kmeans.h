@@ -78,11 +78,13 @@ extern "C" {
  * iteration is two launches on `stream`: assign + accumulate (Algorithm 1
  * steps 2/4 and the sums of Eq. (1)), then the centres and the congruence test
  * (Eq. (1), steps 6-7). HIP events are recorded on `stream` before the first
- * and after the last launch of the call (step_ms), and around the assign +
- * accumulate launch of every sample_every-th iteration (assign_ms). An event
- * between two launches costs the stream several microseconds, so the sampled
- * launches are kept few. In early-stop mode step_ms also contains the host's
- * convergence polls; timing is meant for KMEANS_FIXED_ITERS runs.
+ * and after the last launch of the call (step_ms). The assigning launch of
+ * every sample_every-th iteration (for the L1 metric the assign launch, else
+ * the fused assign + accumulate launch) is made with hipExtLaunchKernel and a
+ * pair of events that its dispatch stamps at its start and end (assign_ms: the
+ * kernel's own duration, nothing between launches). In early-stop mode step_ms
+ * also contains the host's convergence polls; timing is meant for
+ * KMEANS_FIXED_ITERS runs.
  *   in:  sample_every  (0 = every 16th iteration, 1 = every iteration)
  *   out: the other fields */
 typedef struct kmeans_timing {
@@ -136,10 +138,12 @@ int kmeans_init_farthest(const float *X, int64_t n, int32_t M, int32_t K, int32_
  *   init_idx[m] = seeds[m] for m < nseeds (as given; repeats allowed);
  *   init_idx[m] = the object not among init_idx[0..m-1] farthest from them
  *                 (as above), for nseeds <= m < K.
- * seeds is an int32 [nseeds] DEVICE array read by the kernels (a seed outside
- * [0, n) is taken as object 0); 1 <= nseeds <= K <= n, else KMEANS_EINVAL.
- * Workspace as kmeans_init_workspace_bytes. kmeans_init_farthest is this call
- * with the one seed 0. Asynchronous on `stream`.
+ * seeds is an int32 [nseeds] DEVICE array; the call reads it back (one small
+ * copy on `stream`, so it waits for the work that wrote the seeds) and returns
+ * KMEANS_EINVAL, with nothing enqueued, if a seed lies outside [0, n).
+ * 1 <= nseeds <= K <= n, else KMEANS_EINVAL. Workspace as
+ * kmeans_init_workspace_bytes. kmeans_init_farthest is this call with the one
+ * seed 0 (which needs no read-back). Otherwise asynchronous on `stream`.
  */
 int kmeans_init_farthest_from(const float *X, int64_t n, int32_t M, int32_t K,
                               const int32_t *seeds, int32_t nseeds, int32_t *init_idx,

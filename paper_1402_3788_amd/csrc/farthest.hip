@@ -97,7 +97,7 @@ farthest_pass_kernel(const float *__restrict__ X, int64_t n, int K, int p,
     if (p <= nseeds) {
         if (seeds != nullptr) {
             c = seeds[p - 1];
-            if (c < 0 || (int64_t)c >= n) c = 0;          // documented: outside [0, n) reads as 0
+            if (c < 0 || (int64_t)c >= n) c = 0;          // refused on the host; reads stay in bounds
         }
     } else {
         const int half = ((p - 1) & 1) * groups;

@@ -231,7 +231,7 @@ int run_impl(const float *X, int64_t n, int32_t M, int32_t K, const float *init_
     if (l1 && p1.waves < 1) return KMEANS_EUNSUPPORTED;
     const int every = timing == nullptr ? 0 : (timing->sample_every > 0 ? timing->sample_every : 16);
     // events: one before the first launch, one after the last, and a pair
-    // around each sampled assign launch
+    // stamped with the start and end of each sampled assigning launch
     constexpr int kMaxSamples = 64;
     int nsampled = every > 0 ? (max_iter + every - 1) / every : 0;
     if (nsampled > kMaxSamples) nsampled = kMaxSamples;
@@ -290,15 +290,19 @@ int run_impl(const float *X, int64_t n, int32_t M, int32_t K, const float *init_
             a.C = tt == 1 ? init_centers : centers;
             const bool sampled =
                 every > 0 && (tt - 1) % every == 0 && (tt - 1) / every < kMaxSamples;
-            if (sampled) rc = mark();
-            if (!rc && l1) {
+            if (sampled) {
+                // the pair is stamped by the assigning dispatch itself
+                a.ev_start = cache.ev[nev++];
+                a.ev_stop = cache.ev[nev++];
+            }
+            if (l1) {
                 // L1: assign, then the sums of Eq. (1) from those labels
                 rc = hip_status(launch_l1(a, p1, s));
-                if (!rc && sampled) rc = mark();
+                a.ev_start = a.ev_stop = nullptr;
                 if (!rc) rc = hip_status(launch_step(a, kAccumLabels, L.plan, s));
-            } else if (!rc) {
+            } else {
                 rc = hip_status(launch_step(a, kAssignAccum, L.plan, s));
-                if (!rc && sampled) rc = mark();
+                a.ev_start = a.ev_stop = nullptr;
             }
             if (!rc) rc = hip_status(launch_centres(a, L.plan.groups, s));
             ++launched;
@@ -385,6 +389,19 @@ int kmeans_init_farthest_from(const float *X, int64_t n, int32_t M, int32_t K,
     if ((int64_t)K > n || !aligned16(X)) return KMEANS_EINVAL;
     const InitLayout L = init_layout(n, M);
     if (!workspace || workspace_bytes < L.total) return KMEANS_EWORKSPACE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (seeds != nullptr) {
+        // the seeds live in device memory (often written by kmeans_diameter on
+        // the same stream): read them back once, after the work that writes
+        // them, and refuse any outside [0, n) before anything is enqueued
+        int32_t host[kMaxK];
+        if (hipMemcpyAsync(host, seeds, sizeof(int32_t) * (size_t)nseeds, hipMemcpyDeviceToHost,
+                           s) != hipSuccess ||
+            hipStreamSynchronize(s) != hipSuccess)
+            return KMEANS_EHIP;
+        for (int i = 0; i < nseeds; ++i)
+            if (host[i] < 0 || (int64_t)host[i] >= n) return KMEANS_EINVAL;
+    }
     char *ws = static_cast<char *>(workspace);
     FarthestArgs a{};
     a.X = X; a.n = n; a.M = M; a.K = K;
@@ -395,7 +412,7 @@ int kmeans_init_farthest_from(const float *X, int64_t n, int32_t M, int32_t K,
     a.centers = centers;
     a.seeds = seeds;
     a.nseeds = nseeds;
-    return hip_status(launch_farthest(a, L.plan, static_cast<hipStream_t>(stream)));
+    return hip_status(launch_farthest(a, L.plan, s));
 }
 
 size_t kmeans_centroid_workspace_bytes(int64_t n, int32_t M)

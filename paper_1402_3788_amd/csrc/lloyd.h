@@ -1,6 +1,7 @@
 // Internal declarations shared by the kernel files and the C-ABI layer.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -47,6 +48,15 @@ __device__ inline bool stop_before(Ctl *ctl, int t, int fixed)
     if (stop && blockIdx.x == 0 && threadIdx.x == 0 && ctl->converged_at == 0)
         ctl->converged_at = t - 1;
     return stop;
+}
+
+// Early exit of a launch that accumulates from the labels another launch of
+// the same iteration assigned (the L1 metric's second launch): once the run
+// has converged, the assigning launch before it on the stream has evaluated
+// the stop rule and recorded the iteration, so the value is settled here.
+__device__ inline bool stop_after_assign(const Ctl *ctl, int fixed)
+{
+    return ctl != nullptr && !fixed && ctl->converged_at != 0;
 }
 
 // What a launch of the distance kernels does with the assignment.
@@ -109,6 +119,8 @@ struct StepArgs {
     int fixed;                 // no early stop
     int compare;               // record the change flag of iteration t
     int force64;               // decide every label with fp64 distances
+    hipEvent_t ev_start;       // optional: stamped when the assigning launch's
+    hipEvent_t ev_stop;        //   dispatch starts and ends (null: not timed)
 };
 
 hipError_t launch_lane(const StepArgs &a, Mode mode, const AccumPlan &plan, hipStream_t s);

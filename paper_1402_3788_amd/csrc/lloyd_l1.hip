@@ -43,7 +43,7 @@ lloyd_l1_kernel(const float *__restrict__ X, int64_t n, int M, const float *__re
     extern __shared__ __align__(16) float l1_lds[];
     const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave, W = blockDim.x / kWave;
     f4v *cen = reinterpret_cast<f4v *>(l1_lds);               // [K][MB / 4]
-    float *slot = l1_lds + (size_t)K * MB + (size_t)w * kWave * M;
+    float *slot = l1_lds + (size_t)K * MB + (size_t)w * kWave * M;   // 16-byte aligned: K*MB, 64*M multiples of 4
 
     for (int e = threadIdx.x; e < K * MB; e += blockDim.x) {
         const int k = e / MB, j = e % MB;
@@ -58,11 +58,20 @@ lloyd_l1_kernel(const float *__restrict__ X, int64_t n, int M, const float *__re
     int nfallback = 0;
 
     for (int64_t q = (int64_t)w * gridDim.x + blockIdx.x; q < ntiles; q += stride) {
-        // stage the tile (64 objects, M features each, zeros past n)
+        // stage the tile (64 objects, M features each): a full tile is 16 M
+        // aligned float4s (X is 16-byte aligned and 64 M floats a multiple of
+        // 4), read with 16-byte loads; the last, partial tile element by
+        // element with zeros past n
         const int64_t base = q * kWave * (int64_t)M;
-        const int64_t total = n * (int64_t)M;
-        for (int e = lane; e < kWave * M; e += kWave)
-            slot[e] = base + e < total ? X[base + e] : 0.f;
+        if ((q + 1) * kWave <= n) {
+            const f4v *src = reinterpret_cast<const f4v *>(X + base);
+            f4v *dst = reinterpret_cast<f4v *>(slot);
+            for (int v = lane; v < 16 * M; v += kWave) dst[v] = src[v];
+        } else {
+            const int64_t total = n * (int64_t)M;
+            for (int e = lane; e < kWave * M; e += kWave)
+                slot[e] = base + e < total ? X[base + e] : 0.f;
+        }
         __builtin_amdgcn_wave_barrier();
         const int64_t i = q * kWave + lane;
 
@@ -138,8 +147,9 @@ hipError_t l1_launch_mb(const StepArgs &a, const L1Plan &pl, hipStream_t s)
     static const size_t st = static_lds_bytes(reinterpret_cast<const void *>(kern));
     if (st > (size_t)kMaxLds || st + pl.lds_bytes > (size_t)kMaxLds)
         return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL(kern, dim3(pl.groups), dim3(pl.waves * kWave), pl.lds_bytes, s, a.X,
-                       a.n, a.M, a.C, a.K, a.labels, a.min_d2, a.ctl, a.t, a.fixed, a.force64);
+    hipExtLaunchKernelGGL(kern, dim3(pl.groups), dim3(pl.waves * kWave), pl.lds_bytes, s,
+                          a.ev_start, a.ev_stop, 0, a.X, a.n, a.M, a.C, a.K, a.labels, a.min_d2,
+                          a.ctl, a.t, a.fixed, a.force64);
     return hipGetLastError();
 }
 

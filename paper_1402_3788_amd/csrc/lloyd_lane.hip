@@ -76,6 +76,7 @@ lloyd_lane_kernel(const float *__restrict__ X, int64_t n, const float *__restric
     const int lane = threadIdx.x % kWave;
 
     if (MODE == kAssignAccum && stop_before(ctl, t, fixed)) return;
+    if (MODE == kAccumLabels && stop_after_assign(ctl, fixed)) return;
 
     float *tile = reinterpret_cast<float *>(smem) + wave * G::kSlot;
     int32_t *offs = reinterpret_cast<int32_t *>(smem + (size_t)W * G::kSlot * 4) + wave * kWave;
@@ -205,9 +206,9 @@ hipError_t launch_m(const StepArgs &a, Mode mode, const AccumPlan &p, hipStream_
         static const size_t st = static_lds_bytes(reinterpret_cast<const void *>(kern));       \
         if (st > (size_t)kMaxLds || st + p.lds_bytes > (size_t)kMaxLds)                        \
             return hipErrorInvalidConfiguration;                                               \
-        hipLaunchKernelGGL(kern, grid, block, p.lds_bytes, s, a.X, a.n, a.C, a.K, a.labels,    \
-                           a.labels_in, a.min_d2, a.part_sums, a.part_counts, a.ctl, a.t,      \
-                           a.fixed, a.force64);                                                \
+        hipExtLaunchKernelGGL(kern, grid, block, p.lds_bytes, s, a.ev_start, a.ev_stop, 0,     \
+                              a.X, a.n, a.C, a.K, a.labels, a.labels_in, a.min_d2,            \
+                              a.part_sums, a.part_counts, a.ctl, a.t, a.fixed, a.force64);    \
     } while (0)
     const bool one = p.accum == 1;
     switch (mode) {

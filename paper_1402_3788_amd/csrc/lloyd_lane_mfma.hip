@@ -217,6 +217,7 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
     const int h = lane >> 5, j = lane & 31;       // accumulation layout
 
     if (MODE == kAssignAccum && stop_before(ctl, t, fixed)) return;
+    if (MODE == kAccumLabels && stop_after_assign(ctl, fixed)) return;
 
     double *slabs = reinterpret_cast<double *>(smem) + (size_t)wave * 2 * K * M;
     int32_t *cnts = reinterpret_cast<int32_t *>(reinterpret_cast<double *>(smem) +
@@ -481,9 +482,9 @@ hipError_t launch_m(const StepArgs &a, Mode mode, const AccumPlan &p, hipStream_
     do {                                                                                       \
         auto kern = lane_mfma_kernel<M, MD>;                                                   \
         if (p.lds_bytes > (size_t)kMaxLds) return hipErrorInvalidConfiguration;                \
-        hipLaunchKernelGGL(kern, grid, block, p.lds_bytes, s, a.X, a.n, a.C, a.K, a.labels,    \
-                           a.labels_in, a.min_d2, a.part_sums, a.part_counts, a.ctl, a.t,      \
-                           a.fixed, a.force64);                                                \
+        hipExtLaunchKernelGGL(kern, grid, block, p.lds_bytes, s, a.ev_start, a.ev_stop, 0,     \
+                              a.X, a.n, a.C, a.K, a.labels, a.labels_in, a.min_d2,            \
+                              a.part_sums, a.part_counts, a.ctl, a.t, a.fixed, a.force64);    \
     } while (0)
     switch (mode) {
     case kAssign: LANE_MFMA_LAUNCH(kAssign); break;

@@ -185,6 +185,7 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
     const int kbits = key_bits(KT);        // index bits of the packed keys
 
     if (MODE == kAssignAccum && stop_before(ctl, t, fixed)) return;
+    if (MODE == kAccumLabels && stop_after_assign(ctl, fixed)) return;
 
     const MfmaLds L = mfma_lds(M, K, W, kAcc);
     float *tiles = reinterpret_cast<float *>(smem + L.tiles);
@@ -672,9 +673,9 @@ hipError_t launch_m(const StepArgs &a, Mode mode, const AccumPlan &p, hipStream_
         static const size_t st = static_lds_bytes(reinterpret_cast<const void *>(kern));       \
         if (st > (size_t)kMaxLds || st + p.lds_bytes > (size_t)kMaxLds)                        \
             return hipErrorInvalidConfiguration;                                               \
-        hipLaunchKernelGGL(kern, grid, block, p.lds_bytes, s, a.X, a.n, a.C, a.K, a.labels,    \
-                           a.labels_in, a.min_d2, a.part_sums, a.part_counts, a.ctl, a.t,      \
-                           a.fixed, a.force64);                                                \
+        hipExtLaunchKernelGGL(kern, grid, block, p.lds_bytes, s, a.ev_start, a.ev_stop, 0,     \
+                              a.X, a.n, a.C, a.K, a.labels, a.labels_in, a.min_d2,            \
+                              a.part_sums, a.part_counts, a.ctl, a.t, a.fixed, a.force64);    \
     } while (0)
     switch (mode) {
     case kAssign: LLOYD_MFMA_LAUNCH(kAssign, 0); break;

@@ -92,7 +92,11 @@ def test_init_workload_full_size(name):
 @pytest.mark.parametrize("n,M,K,seeds,kind", [(1000, 3, 10, (999, 0), "uniform"),
                                               (70_001, 25, 16, (5, 5, 70_000), "dups"),
                                               (4097, 7, 33, (17,), "blobs"),
-                                              (64, 2, 64, (63, 1, 2, 3), "uniform")])
+                                              (64, 2, 64, (63, 1, 2, 3), "uniform"),
+                                              # as many seeds as centres: the last,
+                                              # one-workgroup launch takes a seed
+                                              (500, 4, 6, (7, 3, 499, 0, 3, 250), "uniform"),
+                                              (40, 3, 40, tuple(range(39, -1, -1)), "blobs")])
 def test_init_from_seeds_parity(n, M, K, seeds, kind):
     X = _case(n, M, kind, seed=n + K)
     _say(f"[init from seeds] n={n} M={M} K={K} seeds={seeds}")
@@ -102,6 +106,22 @@ def test_init_from_seeds_parity(n, M, K, seeds, kind):
     want = oracle.init_farthest_from(X, K, list(seeds))
     assert np.array_equal(idx.cpu().numpy(), want)
     assert np.array_equal(C.cpu().numpy().view(np.uint32), X[want].view(np.uint32))
+
+
+@pytest.mark.parametrize("seeds", [(5, 1000), (-1,), (3, 7, 2**31 - 1)])
+def test_init_from_seeds_outside_the_set_are_refused(seeds):
+    # the oracle refuses them too; nothing is written
+    X = _case(1000, 3, "uniform", seed=4)
+    Xd = torch.from_numpy(X).to(DEV)
+    idx = torch.full((8,), -5, dtype=torch.int32, device=DEV)
+    C = torch.full((8, 3), 7.0, dtype=torch.float32, device=DEV)
+    with pytest.raises(km.KmeansError) as e:
+        km.kmeans_init_farthest(Xd, 8, seeds=torch.tensor(seeds, dtype=torch.int32, device=DEV),
+                                out=(idx, C))
+    assert e.value.code == km.KMEANS_EINVAL
+    assert (idx == -5).all() and (C == 7.0).all()
+    with pytest.raises(ValueError):
+        oracle.init_farthest_from(X, 8, list(seeds))
 
 
 @pytest.mark.parametrize("n,M,K", [(20_000, 25, 16), (5_000, 3, 40)])

@@ -12,6 +12,8 @@ over all K-subsets), and invariants of the traversal.
 import itertools
 from fractions import Fraction
 
+import os
+
 import numpy as np
 import pytest
 
@@ -120,6 +122,20 @@ def test_stored_workload_init_matches(name):
     numpy recipe) are the oracle's."""
     X, _, idx, _ = workloads.load(name)
     assert np.array_equal(oracle.init_farthest(X, workloads.get(name).K), idx)
+
+
+@pytest.mark.parametrize("name", ["blobs25d-n2m-k256", "zipfnoise25d-n20m-k64"])
+def test_stored_init_is_the_oracles(name):
+    """The initial objects stored for the two fixed-30 workloads are the ones
+    oracle.init_farthest chose on the same inputs: the trajectory goldens,
+    written from the oracle alone (tests/golden/make_trajectories.py), record
+    the oracle's indices and the SHA-256 of the inputs they were chosen on."""
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                        f"trajectory_{name}.npz")
+    g = np.load(path, allow_pickle=False)
+    entry = workloads._init_table()[name]
+    assert entry["sha256_x"] == str(g["sha256_x"])
+    assert np.array_equal(np.asarray(entry["init"]), g["init_idx"])
 
 
 @pytest.mark.parametrize("n,M,K,seeds,seed", [(12, 2, 5, (3, 7), 0), (20, 3, 20, (19, 0, 5), 1),
