@@ -58,7 +58,7 @@ extern "C" {
 #define KMEANS_FIXED_ITERS  (1u << 0) /* kmeans_run: run exactly max_iter iterations, no early stop */
 #define KMEANS_PATH_DIRECT  (1u << 1) /* force the vector-ALU distance path                          */
 #define KMEANS_PATH_MFMA    (1u << 2) /* force a matrix-core (expanded-form) distance path: one      */
-                                      /* object per lane for K <= 16 and M <= 32, else 64-object      */
+                                      /* object per lane for K <= 64 and M <= 32, else 64-object      */
                                       /* tiles; KMEANS_EUNSUPPORTED when the tiles' per-workgroup     */
                                       /* state (centre operands, fp64 sums) does not fit in LDS       */
 #define KMEANS_PATH_TILES   (1u << 3) /* force the 64-object-tile matrix-core path (any K)           */
@@ -70,9 +70,11 @@ extern "C" {
                                       /* operation order (the path every close call takes anyway),    */
                                       /* skipping the faster screening: slower, same results; for     */
                                       /* checking that the screening changes no label.                 */
-/* Without a path flag: 64-object tiles on the matrix cores for K > 16, one
- * object per lane on the matrix cores for 5 <= K <= 16 (M <= 32), the vector
- * ALU otherwise. Every path gives the same labels, centres and counts. */
+/* Without a path flag: one object per lane on the matrix cores for
+ * 5 <= K <= 64 (M <= 32), 64-object tiles on the matrix cores for other
+ * K > 16, the vector ALU otherwise. Every path gives the same labels and
+ * counts, and centres equal to within the rounding of fp64 sums (each path
+ * sums in its own fixed order). */
 
 /* Optional per-call timing for kmeans_run (pass NULL for none). Each
  * iteration is two launches on `stream`: assign + accumulate (Algorithm 1

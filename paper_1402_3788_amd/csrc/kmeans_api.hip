@@ -52,8 +52,8 @@ int select_path(int32_t M, int32_t K, uint32_t flags)
     const bool lane = lane_mfma_fits(M, K), tile = tile_fits(M, K);
     if (flags & KMEANS_PATH_TILES) return tile ? kPathTile : -1;
     if (flags & KMEANS_PATH_MFMA) return lane ? kPathLaneMfma : tile ? kPathTile : -1;
-    if (K > 16) return tile ? kPathTile : kPathValu;
-    return (lane && K >= 5) ? kPathLaneMfma : kPathValu;
+    if (lane && K >= 5) return kPathLaneMfma;
+    return (K > 16 && tile) ? kPathTile : kPathValu;
 }
 
 AccumPlan plan_for(int p, int64_t n, int32_t M, int32_t K, Mode mode)

@@ -127,20 +127,27 @@ __device__ inline void store_tile(float *tile, int lane,
 // features; read per centre so the rare re-decision holds no fp64 copy of the
 // object in registers.
 template <int M>
+__device__ inline double dist_fp64(const float *xs, const float *c)
+{
+    double d = 0.0;
+#pragma unroll
+    for (int j = 0; j < M; ++j) {
+        const double e = (double)xs[j] - (double)c[j];
+        const double sq = e * e;
+        d = d + sq;
+    }
+    return d;
+}
+
+// Nearest centre by dist_fp64 over all K centres, lowest index on ties.
+template <int M>
 __device__ inline int argmin_fp64(const float *xs, const float *__restrict__ C, int K,
                                   double &best_out)
 {
     double best = INFINITY;
     int lab = 0;
     for (int k = 0; k < K; ++k) {
-        const float *c = C + k * M;
-        double d = 0.0;
-#pragma unroll
-        for (int j = 0; j < M; ++j) {
-            const double e = (double)xs[j] - (double)c[j];
-            const double sq = e * e;
-            d = d + sq;
-        }
+        const double d = dist_fp64<M>(xs, C + k * M);
         if (d < best) {
             best = d;
             lab = k;

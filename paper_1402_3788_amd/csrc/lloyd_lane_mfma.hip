@@ -1,8 +1,9 @@
-// Fused assign + accumulate for small K (K <= 16, M <= 32): one 64-object tile
-// per wavefront at a time, the scores on the bf16 matrix cores, and every
-// tile read from global memory twice -- once in the matrix operand layout and
-// once in the accumulation layout -- so that the cache does the transpose and
-// LDS holds nothing but the fp64 sums.
+// Fused assign + accumulate for K <= 64, M <= 32: one 64-object tile per
+// wavefront at a time, the scores on the bf16 matrix cores in one, two or four
+// 16-centre blocks (KB), and every tile read from global memory twice -- once
+// in the matrix operand layout and once in the accumulation layout -- so that
+// the cache does the transpose and LDS holds nothing but the fp64 sums (and,
+// for KB > 1, the centre operands).
 //
 // Per tile q (objects 64q .. 64q+63) a wave does:
 //   1. operand loads (issued one tile ahead): lane (g, o) = (lane / 16,
@@ -13,32 +14,37 @@
 //   2. accumulation loads, issued right after the operand loads of the same
 //      tile so that both meet the same cache lines in flight (X crosses HBM
 //      and L2 once): lane (h, j) = (lane / 32, lane % 32) reads feature j of
-//      object s + 32h for s = 0..31;
+//      32 objects of the tile (s + 32h with two slabs, 2s + h with one);
 //   3. scores (Algorithm 1 steps 2/4, Eq. (2) in the expanded form
-//      score = |c|^2 - 2 x.c, |x|^2 being common to all centres): A = -2C
-//      (16 centres x 32 features, zero past K and M) and B = X^T, both split
-//      into bf16 hi and lo parts rounded to nearest, three
-//      v_mfma_f32_16x16x32_bf16 per block (lo(A) hi(B) + hi(A) lo(B) +
-//      hi(A) hi(B)) on top of |c|^2; lane (g, o) ends with the scores of
-//      centres 4g .. 4g+3 for object o of every block;
-//   4. the label: each score becomes a packed key (its low 4 bits replaced by
-//      the centre's index), each lane keeps the best and second-best key of
-//      every block, and two rounds of row swaps (v_permlane32_swap, then
-//      v_permlane16_swap) leave lane l with the two best keys of object l;
-//      a label is accepted when the two differ by more than twice the proven
-//      error bound, otherwise the object is re-decided over all centres with
-//      fp64 distances in the reference operation order (lowest index on ties),
-//      so every label is the exact-arithmetic argmin;
+//      score = |c|^2 - 2 x.c, |x|^2 being common to all centres): per centre
+//      block A = -2C (16 centres x 32 features, zero past K and M) and B = X^T,
+//      both split into bf16 hi and lo parts rounded to nearest, three
+//      v_mfma_f32_16x16x32_bf16 per object block (lo(A) hi(B) + hi(A) lo(B) +
+//      hi(A) hi(B)) on top of |c|^2; lane (g, o) gets the scores of centres
+//      16cb + 4g .. 16cb + 4g + 3 for object o of every object block;
+//   4. the label: each score becomes a packed key (its low 4, 5 or 6 bits
+//      replaced by the centre's index), each lane keeps the best and
+//      second-best key of each object block over the centre blocks, and two
+//      rounds of row swaps (v_permlane32_swap, then v_permlane16_swap) leave
+//      lane l with the two best keys of object l; a label is accepted when the
+//      two differ by more than twice the proven error bound thr/2. Otherwise
+//      (a close call) the keys are formed again, every centre whose key is
+//      within thr of the best becomes a candidate (no other centre can be the
+//      nearest), and the object is decided among its candidates with fp64
+//      distances in the reference operation order (lowest index on ties), so
+//      every label is the exact-arithmetic argmin;
 //   5. accumulation (the numerator and denominator of Eq. (1)): lane l
-//      writes the slab row offset of object l (slab l / 32) to the wave's
-//      offset table; lanes (h, .) read the offsets of objects 32h .. 32h+31
-//      back with broadcast 16-byte reads, and in step s lane (h, j) adds
-//      feature j of object s + 32h to slab h with an LDS fp64 add. The two halves of a
-//      wave add to different slabs and the lanes of a half to different
-//      columns, so no two lanes of one add meet on an address: every sum is
-//      formed in a fixed order (objects of the wave's tiles in ascending
-//      order per slab) without relying on how the LDS orders the lanes of one
-//      instruction. Counts are integer LDS adds (order-free).
+//      writes the slab row offset of object l to the wave's offset table;
+//      lanes (h, .) read the offsets of their 32 objects back with broadcast
+//      16-byte reads, and in step s lane (h, j) adds feature j of its object
+//      of the step with an LDS fp64 add. With two slabs per wave (KB <= 2) the
+//      halves of a tile add to different slabs and the lanes of a half to
+//      different columns, so no two lanes of one add meet on an address; with
+//      one slab (KB = 4, whose eight waves' slabs would not fit twice) the
+//      objects 2s and 2s + 1 of a step meet on an address when they share a
+//      cluster, and the LDS applies the lanes of an add in ascending order. So
+//      every sum is formed in a fixed order: objects of the wave's tiles in
+//      ascending order per slab. Counts are integer LDS adds (order-free).
 // At the end the workgroup adds its slabs in a fixed order (waves, then
 // slabs) and writes one fp64 partial per (cluster, feature) and one count per
 // cluster; a second launch forms the centres (lloyd_centres.hip).
@@ -53,17 +59,22 @@
 // 2^-23 relative), whatever the order or rounding direction, so the sums err by
 // at most 1.01 * 98 * 2^-23 of (|c|^2 + sum |a b|) <= (3|c|^2 + |x|^2). The
 // fp32 |c|^2 (M fused multiply-adds) errs by 25 * 2^-24 |c|^2 at M = 32.
-// A packed key moves its score by less than 2^(4-23) of the score's
-// magnitude, itself below (1 + E)(3|c|^2 + |x|^2). Together every key is
-// within E (3 max|c|^2 + |x|^2) of the exact score with
-//     E = 3.02 * 2^-16 + 104 * 2^-23 + 1.01 * 2^-19,
+// A packed key with b index bits moves its score by less than 2^(b-23) of
+// the score's magnitude, itself below (1 + E)(3|c|^2 + |x|^2). Together every
+// key is within E (3 max|c|^2 + |x|^2) of the exact score with
+//     E = 3.02 * 2^-16 + 104 * 2^-23 + 1.01 * 2^(b-23),
 // and a label is accepted when the two best keys differ by more than
 // 2.02 E (3.02 max|c|^2 + 1.0001 |x|^2) + 1e-30 (the fp32 |x|^2 and max|c|^2
 // are themselves within the margins; 1e-30 covers bf16 parts below the normal
 // range). |x|^2 here sums the squares of every value the lane group read,
 // including the up to seven floats past the object's M features: an upper
 // bound, which only widens the band (and makes an object whose neighbour holds
-// an infinity or a NaN go to the fp64 path).
+// an infinity or a NaN go to the fp64 path). The same bound makes a close
+// call's candidate set complete: a centre whose key exceeds the best key b1 by
+// more than thr has an exact score above b1 + thr - e >= b1 + e (e the error
+// bound of one key, thr >= 2.02 e), while the best key's centre scores at most
+// b1 + e; the 1 % margin keeps that gap far above fp64 rounding, so the fp64
+// distances order the candidates as they order all centres.
 #include "lloyd.h"
 #include "lloyd_device.h"
 
@@ -92,13 +103,35 @@ typedef float f4u __attribute__((ext_vector_type(4), aligned(4)));
 constexpr int kWaves = 8;
 constexpr int kMinWavesPerSimd = 2;   // caps registers at 256 per lane
 constexpr int kMaxMLane = 32;         // features: four lane groups of eight
-[[maybe_unused]] constexpr int kMaxKLane = 16;        // centres: one 16-row A operand
+[[maybe_unused]] constexpr int kMaxKLane = 64;   // centres: up to four 16-row A operands
 
-// LDS of a workgroup: [W][2][K][M] fp64 slabs, [W][K] int32 counts, then
-// [W][64] int32 slab offsets of the objects of the current tile.
-[[maybe_unused]] __host__ __device__ inline size_t lane_lds_bytes(int M, int K, int W)
+// 16-centre blocks of a launch (1, 2 or 4) and the index bits of its keys.
+__host__ __device__ constexpr int lane_blocks(int K) { return K <= 16 ? 1 : K <= 32 ? 2 : 4; }
+[[maybe_unused]] __host__ __device__ constexpr int key_bits_of(int KB) { return KB == 1 ? 4 : KB == 2 ? 5 : 6; }
+// fp64 slabs per wave: two (the halves of a tile; no two lanes of one add
+// meet) while eight waves' worth fit; one for four blocks (the two objects of
+// a step then share it, the LDS applying the lanes of one add in order).
+__host__ __device__ constexpr int lane_slabs(int KB) { return KB == 4 ? 1 : 2; }
+
+// With more than one 16-centre block the A operands and seeds of the blocks
+// (48 bytes per lane and block) live in LDS, read again for every tile,
+// instead of in registers.
+__host__ __device__ constexpr bool lane_a_in_lds(int KB) { return KB > 1; }
+
+// LDS of a workgroup: with accumulation [W][S][K][M] fp64 slabs, [W][K] int32
+// counts and [W][64] int32 slab offsets of the objects of the current tile;
+// with distances and more than one block, the A table [3][KB][64] x 16 bytes.
+[[maybe_unused]] __host__ __device__ inline size_t lane_acc_bytes(int M, int K, int W)
 {
-    return (size_t)W * 2 * K * M * 8 + (size_t)W * K * 4 + (size_t)W * kWave * 4;
+    const int S = lane_slabs(lane_blocks(K));
+    return (size_t)W * S * K * M * 8 + (size_t)W * K * 4 + (size_t)W * kWave * 4;
+}
+[[maybe_unused]] __host__ __device__ inline size_t lane_lds_bytes(int M, int K, int W, Mode mode)
+{
+    const int KB = lane_blocks(K);
+    const size_t acc = mode == kAssign ? 0 : lane_acc_bytes(M, K, W);
+    const size_t tab = (mode != kAccumLabels && lane_a_in_lds(KB)) ? (size_t)3 * KB * kWave * 16 : 0;
+    return acc + tab;
 }
 
 // Object rows after the last row of a tile that the operand loads may touch
@@ -196,7 +229,17 @@ constexpr int kMaxMLane = 32;         // features: four lane groups of eight
     return m0 + m1;
 }
 
-template <int M, int MODE>
+// Bitwise or of x over the four lanes l16 + 16g (g = 0..3), in each of them:
+// a row swap returns, in every lane, the values of both lanes of its pair.
+[[maybe_unused]] __device__ inline uint32_t or_rows(uint32_t x)
+{
+    const auto a = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+    x = a[0] | a[1];
+    const auto b = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+    return b[0] | b[1];
+}
+
+template <int M, int MODE, int KB>
 __global__ void __launch_bounds__(kWaves * kWave, kMinWavesPerSimd)
 lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict__ C, int K,
                  int32_t *__restrict__ labels, const int32_t *__restrict__ labels_in,
@@ -205,8 +248,15 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
                  int force64)
 {
     static_assert(M >= 1 && M <= kMaxMLane, "feature count");
+    static_assert(KB == 1 || KB == 2 || KB == 4, "centre blocks");
     constexpr bool kAcc = MODE != kAssign;
     constexpr bool kDist = MODE != kAccumLabels;
+    constexpr int S = lane_slabs(KB);          // fp64 slabs per wave
+    constexpr int kBits = key_bits_of(KB);     // index bits of a packed key
+    // With more than one block the operand loads of the next tile go into the
+    // registers of the current one once it is split (one register set), which
+    // leaves room for the A operands of the other blocks.
+    constexpr bool kOneOpSet = KB > 1;
     extern __shared__ __align__(16) unsigned char smem[];
     const int W = blockDim.x / kWave;
     // wave-uniform (scalar) wave index, so that tile addresses are scalar
@@ -219,48 +269,87 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
     if (MODE == kAssignAccum && stop_before(ctl, t, fixed)) return;
     if (MODE == kAccumLabels && stop_after_assign(ctl, fixed)) return;
 
-    double *slabs = reinterpret_cast<double *>(smem) + (size_t)wave * 2 * K * M;
+    double *slabs = reinterpret_cast<double *>(smem) + (size_t)wave * S * K * M;
     int32_t *cnts = reinterpret_cast<int32_t *>(reinterpret_cast<double *>(smem) +
-                                                (size_t)W * 2 * K * M) + wave * K;
+                                                (size_t)W * S * K * M) + wave * K;
     int32_t *offs = reinterpret_cast<int32_t *>(reinterpret_cast<double *>(smem) +
-                                                (size_t)W * 2 * K * M) + W * K + wave * kWave;
+                                                (size_t)W * S * K * M) + W * K + wave * kWave;
     if (kAcc) {
-        for (int i = lane; i < 2 * K * M; i += kWave) slabs[i] = 0.0;
+        for (int i = lane; i < S * K * M; i += kWave) slabs[i] = 0.0;
         for (int i = lane; i < K; i += kWave) cnts[i] = 0;
     }
 
-    // A operands for the whole launch: lane (g, o) holds -2 c_o, features
-    // 8g .. 8g+7 (zero past K and M), split into bf16 hi and lo, and the
-    // accumulator seeds |c_k|^2 of centres k = 4g .. 4g+3 (the largest finite
-    // float past K, so padding centres never win and their keys stay finite).
-    uint32_t ah[4], al[4];
-    f4v cseed = {0.f, 0.f, 0.f, 0.f};
+    // A operands for the whole launch: for block cb, lane (g, o) holds
+    // -2 c_{16cb+o}, features 8g .. 8g+7 (zero past K and M), split into bf16
+    // hi and lo, and the accumulator seeds |c_k|^2 of centres k = 16cb + 4g ..
+    // 16cb + 4g + 3 (the largest finite float past K, so padding centres never
+    // win and their keys stay finite).
+    constexpr bool kALds = kDist && lane_a_in_lds(KB);
+    uint32_t ah[KB][4], al[KB][4];
+    f4v cseed[KB];
     float cmax = 0.f;
+    // the A table in LDS: [hi | lo | seeds][KB][64 lanes], 16 bytes each
+    uint4 *atab = reinterpret_cast<uint4 *>(smem + (kAcc ? lane_acc_bytes(M, K, W) : 0));
     if (kDist) {
-        float a[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int f = 8 * g + e;
-            a[e] = (o16 < K && f < M) ? -2.0f * C[o16 * M + f] : 0.f;
-        }
-        split_bf16x8(a, ah, al);
+        for (int cb = 0; cb < KB; ++cb) {
+            float a[8];
+            const int ko = 16 * cb + o16;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int k = 4 * g + r;
-            float nk = FLT_MAX;
-            if (k < K) {
-                nk = 0.f;
-#pragma unroll
-                for (int f = 0; f < M; ++f) nk = __builtin_fmaf(C[k * M + f], C[k * M + f], nk);
-                cmax = fmaxf(cmax, nk);
+            for (int e = 0; e < 8; ++e) {
+                const int f = 8 * g + e;
+                a[e] = (ko < K && f < M) ? -2.0f * C[ko * M + f] : 0.f;
             }
-            cseed[r] = nk;
+            split_bf16x8(a, ah[cb], al[cb]);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int k = 16 * cb + 4 * g + r;
+                float nk = FLT_MAX;
+                if (k < K) {
+                    nk = 0.f;
+#pragma unroll
+                    for (int f = 0; f < M; ++f) nk = __builtin_fmaf(C[k * M + f], C[k * M + f], nk);
+                    cmax = fmaxf(cmax, nk);
+                }
+                cseed[cb][r] = nk;
+            }
+            if (kALds && wave == 0) {
+                atab[(0 * KB + cb) * kWave + lane] = make_uint4(ah[cb][0], ah[cb][1], ah[cb][2], ah[cb][3]);
+                atab[(1 * KB + cb) * kWave + lane] = make_uint4(al[cb][0], al[cb][1], al[cb][2], al[cb][3]);
+                atab[(2 * KB + cb) * kWave + lane] =
+                    make_uint4(__float_as_uint(cseed[cb][0]), __float_as_uint(cseed[cb][1]),
+                               __float_as_uint(cseed[cb][2]), __float_as_uint(cseed[cb][3]));
+            }
         }
         cmax = fmaxf(cmax, __shfl_xor(cmax, 16, kWave));
         cmax = fmaxf(cmax, __shfl_xor(cmax, 32, kWave));
+        if (kALds) __syncthreads();
     }
-    constexpr float kE = 3.02f * 1.5258789e-05f + 104.0f * 1.1920929e-07f + 1.01f * 1.9073486e-06f;
-    const uint32_t kKeyMask = ~15u;
+    // block cb's operands and seeds: registers, or the LDS table
+    auto a_ops = [&](int cb, uint32_t (&h4)[4], uint32_t (&l4)[4], f4v &seed) {
+        if (kALds) {
+            const uint4 u = atab[(0 * KB + cb) * kWave + lane];
+            const uint4 v = atab[(1 * KB + cb) * kWave + lane];
+            const uint4 w = atab[(2 * KB + cb) * kWave + lane];
+            h4[0] = u.x; h4[1] = u.y; h4[2] = u.z; h4[3] = u.w;
+            l4[0] = v.x; l4[1] = v.y; l4[2] = v.z; l4[3] = v.w;
+            seed[0] = __uint_as_float(w.x); seed[1] = __uint_as_float(w.y);
+            seed[2] = __uint_as_float(w.z); seed[3] = __uint_as_float(w.w);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                h4[e] = ah[cb][e];
+                l4[e] = al[cb][e];
+            }
+            seed = cseed[cb];
+        }
+    };
+    // error bound of a key relative to (3|c|^2 + |x|^2); the last term is the
+    // packing of a kBits-bit index into the low bits
+    constexpr float kKeyRel = kBits == 4 ? 1.9073486e-06f : kBits == 5 ? 3.8146973e-06f : 7.6293945e-06f;
+    constexpr float kE = 3.02f * 1.5258789e-05f + 104.0f * 1.1920929e-07f + 1.01f * kKeyRel;
+    constexpr uint32_t kIdxMask = (1u << kBits) - 1u;
+    constexpr uint32_t kKeyMask = ~kIdxMask;
 
     const int64_t nt = (n + kWave - 1) / kWave;                    // tiles
     int64_t nsafe = (n - rows_after(M)) / kWave;                   // unguarded tiles
@@ -299,29 +388,35 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
 
     int nfallback = 0;
 
-    // accumulation values of tile q (lane (h, j): feature j of objects
-    // 32h .. 32h+31; the guarded form reads zeros past n)
+    // Accumulation layout: in step s lane (h, j) adds feature j of object
+    // s + 32h of the tile into slab h (two slabs), or of object 2s + h (one
+    // slab: objects in ascending order, the two of a step meeting on an
+    // address only in the LDS's lane order).
+    // accumulation values of tile q (the guarded form reads zeros past n)
     auto load_acc = [&](int64_t q, float (&xa)[32], auto tail) {
         constexpr bool kTail = decltype(tail)::value;
         const float *tb = X + q * (kWave * M);                 // scalar
-        const int c = 32 * h * M + jr;
+        const int c = (S == 2 ? 32 * h : h) * M + jr;
+        constexpr int kObjStride = S == 2 ? 1 : 2;
 #pragma unroll
         for (int s = 0; s < 32; ++s) {
-            if (kTail) xa[s] = (q * kWave + 32 * h + s < n) ? tb[c + s * M] : 0.f;
-            else xa[s] = tb[c + s * M];
+            if (kTail) xa[s] = (q * kWave + (S == 2 ? 32 * h : h) + kObjStride * s < n)
+                                   ? tb[c + kObjStride * s * M] : 0.f;
+            else xa[s] = tb[c + kObjStride * s * M];
         }
     };
     // One tile (kTail: the guarded loads and validity tests): xb / xa hold its
     // operand and accumulation values (loaded one tile earlier); the loads of
-    // tile qn go into nxt / xan first (unguarded form only). Every load is
-    // unconditional, so the waits count them exactly.
+    // tile qn go into nxt / xan (unguarded form only; with one operand set,
+    // nxt is xb itself, loaded once it is split). Every load is unconditional,
+    // so the waits count them exactly.
     auto step = [&](int64_t q, f4v (&xb)[4][2], float (&xa)[32], f4v (&nxt)[4][2],
                     float (&xan)[32], int64_t qn, auto tail) {
         constexpr bool kTail = decltype(tail)::value;
         const int64_t i = q * kWave + lane;           // this lane's object
         const bool valid = !kTail || i < n;
         if (!kTail) {
-            if (kDist) load_ops(qn, nxt);
+            if (kDist && !kOneOpSet) load_ops(qn, nxt);
             if (kAcc) load_acc(qn, xan, std::false_type{});
         }
         int lab = 0;
@@ -340,46 +435,174 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
                 xp[b] = acc;
                 split_bf16x8(v, bh[b], bl[b]);
             }
-            f4v d[4];
-#pragma unroll
-            for (int b = 0; b < 4; ++b) d[b] = cseed;
-#pragma unroll
-            for (int b = 0; b < 4; ++b)
-                d[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf8(al), as_bf8(bh[b]), d[b], 0, 0, 0);
-#pragma unroll
-            for (int b = 0; b < 4; ++b)
-                d[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf8(ah), as_bf8(bl[b]), d[b], 0, 0, 0);
-#pragma unroll
-            for (int b = 0; b < 4; ++b)
-                d[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf8(ah), as_bf8(bh[b]), d[b], 0, 0, 0);
-            // packed keys, best and second best of the lane's 4 centres per block
+            if (kOneOpSet && !kTail && kDist) load_ops(qn, nxt);
+            // per block: three products per 16-object column, then packed
+            // keys (low kBits bits replaced by the centre index) folded into
+            // the lane's best and second-best key of each column
             float k1[4], k2[4];
             const uint32_t i0 = (uint32_t)(4 * g);
 #pragma unroll
-            for (int b = 0; b < 4; ++b) {
-                float s[4];
+            for (int cb = 0; cb < KB; ++cb) {
+                uint32_t h4[4], l4[4];
+                f4v seed;
+                a_ops(cb, h4, l4, seed);
+                f4v d[4];
 #pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    s[r] = __uint_as_float((__float_as_uint(d[b][r]) & kKeyMask) | (i0 + r));
-                const float lo01 = key_min(s[0], s[1]), hi01 = key_max(s[0], s[1]);
-                k2[b] = key_min(hi01, key_med3(lo01, s[2], s[3]));
-                k1[b] = key_min3(lo01, s[2], s[3]);
+                for (int b = 0; b < 4; ++b) d[b] = seed;
+#pragma unroll
+                for (int b = 0; b < 4; ++b)
+                    d[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf8(l4), as_bf8(bh[b]), d[b], 0, 0, 0);
+#pragma unroll
+                for (int b = 0; b < 4; ++b)
+                    d[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf8(h4), as_bf8(bl[b]), d[b], 0, 0, 0);
+#pragma unroll
+                for (int b = 0; b < 4; ++b)
+                    d[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf8(h4), as_bf8(bh[b]), d[b], 0, 0, 0);
+#pragma unroll
+                for (int b = 0; b < 4; ++b) {
+                    float s[4];
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        s[r] = __uint_as_float((__float_as_uint(d[b][r]) & kKeyMask) |
+                                               (i0 + (uint32_t)(16 * cb + r)));
+                    if (cb == 0) {
+                        const float lo01 = key_min(s[0], s[1]), hi01 = key_max(s[0], s[1]);
+                        k2[b] = key_min(hi01, key_med3(lo01, s[2], s[3]));
+                        k1[b] = key_min3(lo01, s[2], s[3]);
+                    } else {
+                        // two keys at a time: the second best of the running
+                        // pair and the two is min(second, med3(best, a, b))
+#pragma unroll
+                        for (int r = 0; r < 4; r += 2) {
+                            const float n2 = key_min(k2[b], key_med3(k1[b], s[r], s[r + 1]));
+                            k1[b] = key_min3(k1[b], s[r], s[r + 1]);
+                            k2[b] = n2;
+                        }
+                    }
+                }
             }
             float b1, b2;
             own_block_keys(k1, k2, b1, b2);
             const float xsq = own_block_sum(xp);
-            lab = (int)(__float_as_uint(b1) & 15u);
+            lab = (int)(__float_as_uint(b1) & kIdxMask);
             lab = lab < K ? lab : K - 1;
             const float thr = 2.02f * kE * (3.02f * cmax + 1.0001f * xsq) + 1e-30f;
             const bool ok = !force64 && ((K == 1) || (b2 - b1 > thr));
             float dmin = 0.f;
-            if (__ballot(valid && !ok) != 0) {
-                if (valid && !ok) {
-                    double bd;
-                    lab = argmin_fp64<M>(X + i * M, C, K, bd);
-                    dmin = (float)bd;
+            const bool close = valid && !ok;
+            if (__ballot(close) != 0) {
+                if (force64) {
+                    if (valid) {
+                        double bd;
+                        lab = argmin_fp64<M>(X + i * M, C, K, bd);
+                        dmin = (float)bd;
+                    }
+                } else {
+                    // Close calls: only centres whose key is within thr of the
+                    // best key can be the nearest (a key errs by at most half
+                    // of thr, so any other centre's exact score exceeds the
+                    // best centre's). The keys are formed again exactly as
+                    // above, each lane marks its candidates for the object of
+                    // each column, the four lanes of an object combine their
+                    // marks, and the object's lane decides among its
+                    // candidates with fp64 distances in ascending index order
+                    // (lowest index on ties).
+                    const float lim_own = close ? b1 + thr : -INFINITY;
+                    uint32_t clo = 0u, chi = 0u;
+                    // one column at a time; with one operand register set
+                    // (which holds the next tile by now) the column's
+                    // operands are read again, in a loop kept rolled so that
+                    // only one column's values are live
+                    auto column = [&](int b, const float (&v)[8]) {
+                        uint32_t rh[4], rl[4];
+                        split_bf16x8(v, rh, rl);
+                        const float lim = __shfl(lim_own, 16 * b + o16, kWave);
+                        uint32_t mlo = 0u, mhi = 0u;
+#pragma unroll
+                        for (int cb = 0; cb < KB; ++cb) {
+                            uint32_t h4[4], l4[4];
+                            f4v d;
+                            a_ops(cb, h4, l4, d);
+                            d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf8(l4), as_bf8(rh), d, 0, 0, 0);
+                            d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf8(h4), as_bf8(rl), d, 0, 0, 0);
+                            d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf8(h4), as_bf8(rh), d, 0, 0, 0);
+#pragma unroll
+                            for (int r = 0; r < 4; ++r) {
+                                const uint32_t idx = i0 + (uint32_t)(16 * cb + r);
+                                const float key =
+                                    __uint_as_float((__float_as_uint(d[r]) & kKeyMask) | idx);
+                                const uint32_t bit = key <= lim ? 1u << (idx & 31u) : 0u;
+                                if (cb < 2) mlo |= bit;
+                                else mhi |= bit;
+                            }
+                        }
+                        // lane l16 + 16b keeps the marks of its own object
+                        mlo = or_rows(mlo);
+                        if (KB == 4) mhi = or_rows(mhi);
+                        clo = g == b ? mlo : clo;
+                        chi = g == b ? mhi : chi;
+                    };
+                    if (kOneOpSet) {
+#pragma unroll 1
+                        for (int b = 0; b < 4; ++b) {
+                            float v[8];
+                            if (kTail) {
+                                const int64_t r = q * kWave + 16 * b + o16;
+#pragma unroll
+                                for (int e = 0; e < 8; ++e) {
+                                    const int f = 8 * g + e;
+                                    v[e] = (r < n && f < M) ? X[r * M + f] : 0.f;
+                                }
+                            } else {
+                                const float *rb = X + q * (kWave * M) + (o16 * M + 16 * b * M);
+                                const f4v u0 = *reinterpret_cast<const f4u *>(rb + c0);
+                                const f4v u1 = *reinterpret_cast<const f4u *>(rb + c1);
+#pragma unroll
+                                for (int e = 0; e < 4; ++e) {
+                                    v[e] = u0[e];
+                                    v[4 + e] = u1[e];
+                                }
+                            }
+                            column(b, v);
+                        }
+                    } else {
+#pragma unroll
+                        for (int b = 0; b < 4; ++b) {
+                            float v[8];
+#pragma unroll
+                            for (int e = 0; e < 8; ++e) v[e] = xb[b][e / 4][e % 4];
+                            column(b, v);
+                        }
+                    }
+                    if (K < 32) clo &= (1u << K) - 1u;      // padding centres never count
+                    if (K > 32 && K < 64) chi &= (1u << (K - 32)) - 1u;
+                    if (close) {
+                        const float *xs = X + i * M;
+                        double best = INFINITY;
+                        int bl = 0;
+                        while (clo != 0u) {
+                            const int k = __builtin_ctz(clo);
+                            clo &= clo - 1u;
+                            const double dd = dist_fp64<M>(xs, C + k * M);
+                            if (dd < best) {
+                                best = dd;
+                                bl = k;
+                            }
+                        }
+                        while (chi != 0u) {
+                            const int k = 32 + __builtin_ctz(chi);
+                            chi &= chi - 1u;
+                            const double dd = dist_fp64<M>(xs, C + k * M);
+                            if (dd < best) {
+                                best = dd;
+                                bl = k;
+                            }
+                        }
+                        lab = bl;
+                        dmin = (float)best;
+                    }
                 }
-                if (ctl != nullptr) nfallback += __popcll(__ballot(valid && !ok));
+                if (ctl != nullptr) nfallback += __popcll(__ballot(close));
             }
             if (MODE == kAssign && min_d2 != nullptr && valid && ok) {
                 const float *xg = X + i * M;
@@ -402,14 +625,17 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
         }
         if (kAcc) {
             const bool adds = valid && lab >= 0;
-            // slab row of object `lane` (object s + 32h sits in slab h), -1: none
-            const int my_off = adds ? ((lane >> 5) * K + lab) * M : -1;
+            // slab row of object `lane`, -1: none; stored where the lanes
+            // that add the object read it (entry 32h + s for the object of
+            // lane (h, .) in step s)
+            const int my_off = adds ? ((S == 2 ? (lane >> 5) : 0) * K + lab) * M : -1;
+            const int my_pos = S == 2 ? lane : (lane & 1) * 32 + (lane >> 1);
             if (adds) atomicAdd(cnts + lab, 1);
-            // all 32 broadcasts first, then the adds (each add waits for its
-            // broadcast; issued in between they would wait one by one)
-            // all 32 offsets first (8 broadcast reads), then the adds
+            // all 32 offsets first (8 broadcast reads), then the adds (each
+            // add waits for its broadcast; issued in between they would wait
+            // one by one)
             int o[32];
-            offs[lane] = my_off;
+            offs[my_pos] = my_off;
             __builtin_amdgcn_wave_barrier();
             {
                 const int4 *src = reinterpret_cast<const int4 *>(offs + 32 * h);
@@ -429,10 +655,12 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
         }
     };
 
-    // Main loop over the unguarded tiles, the next tile's operand loads in
-    // flight in the other register set; then the guarded tail tiles.
+    // Main loop over the unguarded tiles, the next tile's loads in flight in
+    // the other register set (accumulation values; operands too with one
+    // block); then the guarded tail tiles.
     // (The prefetch past a wave's last unguarded tile reloads tile nsafe - 1.)
-    f4v xb[2][4][2];
+    constexpr int kOpSets = kOneOpSet ? 1 : 2;
+    f4v xb[kOpSets][4][2];
     float xa[2][32];
     int64_t q = q0;
     auto next = [&](int64_t qq) { return qq < nsafe ? qq : nsafe - 1; };
@@ -441,17 +669,17 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
         if (kAcc) load_acc(q, xa[0], std::false_type{});
     }
     for (; q < nsafe; q += 2 * stride) {
-        step(q, xb[0], xa[0], xb[1], xa[1], next(q + stride), std::false_type{});
+        step(q, xb[0], xa[0], xb[kOpSets - 1], xa[1], next(q + stride), std::false_type{});
         if (q + stride >= nsafe) {
             q += stride;
             break;
         }
-        step(q + stride, xb[1], xa[1], xb[0], xa[0], next(q + 2 * stride), std::false_type{});
+        step(q + stride, xb[kOpSets - 1], xa[1], xb[0], xa[0], next(q + 2 * stride), std::false_type{});
     }
     for (; q < nt; q += stride) {
         if (kDist) load_ops_tail(q, xb[0]);
         if (kAcc) load_acc(q, xa[0], std::true_type{});
-        step(q, xb[0], xa[0], xb[1], xa[1], q, std::true_type{});
+        step(q, xb[0], xa[0], xb[kOpSets - 1], xa[1], q, std::true_type{});
     }
 
     if (ctl != nullptr && lane == 0 && nfallback > 0) atomicAdd(&ctl->fallbacks, nfallback);
@@ -459,11 +687,11 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
     if (kAcc) {
         __syncthreads();
         const double *all = reinterpret_cast<const double *>(smem);
-        const int32_t *allc = reinterpret_cast<const int32_t *>(all + (size_t)W * 2 * K * M);
+        const int32_t *allc = reinterpret_cast<const int32_t *>(all + (size_t)W * S * K * M);
         double *ps = part_sums + (int64_t)blockIdx.x * K * M;
         for (int e = threadIdx.x; e < K * M; e += blockDim.x) {
             double s = 0.0;
-            for (int r = 0; r < 2 * W; ++r) s = s + all[(size_t)r * K * M + e];
+            for (int r = 0; r < S * W; ++r) s = s + all[(size_t)r * K * M + e];
             ps[e] = s;
         }
         for (int k = threadIdx.x; k < K; k += blockDim.x) {
@@ -474,13 +702,13 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
     }
 }
 
-template <int M>
-hipError_t launch_m(const StepArgs &a, Mode mode, const AccumPlan &p, hipStream_t s)
+template <int M, int KB>
+hipError_t launch_mb(const StepArgs &a, Mode mode, const AccumPlan &p, hipStream_t s)
 {
     const dim3 grid(p.groups), block(p.waves * kWave);
 #define LANE_MFMA_LAUNCH(MD)                                                                   \
     do {                                                                                       \
-        auto kern = lane_mfma_kernel<M, MD>;                                                   \
+        auto kern = lane_mfma_kernel<M, MD, KB>;                                               \
         if (p.lds_bytes > (size_t)kMaxLds) return hipErrorInvalidConfiguration;                \
         hipExtLaunchKernelGGL(kern, grid, block, p.lds_bytes, s, a.ev_start, a.ev_stop, 0,     \
                               a.X, a.n, a.C, a.K, a.labels, a.labels_in, a.min_d2,            \
@@ -493,6 +721,16 @@ hipError_t launch_m(const StepArgs &a, Mode mode, const AccumPlan &p, hipStream_
     }
 #undef LANE_MFMA_LAUNCH
     return hipGetLastError();
+}
+
+template <int M>
+hipError_t launch_m(const StepArgs &a, Mode mode, const AccumPlan &p, hipStream_t s)
+{
+    switch (lane_blocks(a.K)) {
+    case 1: return launch_mb<M, 1>(a, mode, p, s);
+    case 2: return launch_mb<M, 2>(a, mode, p, s);
+    default: return launch_mb<M, 4>(a, mode, p, s);
+    }
 }
 
 using LaunchFn = hipError_t (*)(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
@@ -531,7 +769,11 @@ hipError_t LLOYD_PART_FN(launch_lane_mfma_part)(const StepArgs &a, Mode mode, co
 }
 
 #if LLOYD_PART == 0
-bool lane_mfma_fits(int M, int K) { return K <= kMaxKLane && M <= kMaxMLane; }
+bool lane_mfma_fits(int M, int K)
+{
+    return K <= kMaxKLane && M <= kMaxMLane &&
+           lane_lds_bytes(M, K, kWaves, kAssignAccum) <= (size_t)kMaxLds;
+}
 
 AccumPlan plan_lane_mfma(int64_t n, int M, int K, Mode mode)
 {
@@ -545,7 +787,7 @@ AccumPlan plan_lane_mfma(int64_t n, int M, int K, Mode mode)
     p.waves = W;
     p.groups = (int)groups;
     p.accum = 0;
-    p.lds_bytes = mode == kAssign ? 0 : lane_lds_bytes(M, K, W);
+    p.lds_bytes = lane_lds_bytes(M, K, W, mode);
     return p;
 }
 

@@ -2,13 +2,16 @@
 
 The centres must be bitwise reproducible (the congruence test of Algorithm 1
 steps 6-7 compares them bit for bit), so every fp64 addition has to happen in
-an order fixed by the problem shape. Two accumulation forms of the
-64-object-tile kernel (K > 16) let several lanes of one LDS fp64 add hit the
-same address -- one slab shared by the two objects of a step, and the
-workgroup slab that the waves add into in turn, one lane per object -- and so
-rely on the LDS applying those lanes in ascending lane order. (The small-K
-kernel never lets two lanes of one add meet.) These tests check that property
-on order-sensitive data instead of assuming it.
+an order fixed by the problem shape. Three accumulation forms let several
+lanes of one LDS fp64 add hit the same address -- in the small-K kernel with
+four 16-centre blocks (33 <= K <= 64) the one slab per wave that the two
+objects of a step share, in the 64-object-tile kernel (larger K, or more than
+32 features) a slab shared the same way and the workgroup slab that the waves
+add into in turn, one lane per object -- and so rely on the LDS applying those
+lanes in ascending lane order. (With one or two blocks the small-K kernel adds
+the halves of a tile to two slabs and never lets two lanes of one add meet.)
+These tests check that property on order-sensitive data instead of assuming
+it.
 
 With n = 64 objects the launch is one wave of one workgroup with one tile.
 The forms whose adds can collide then form a cluster's sums in ascending
@@ -73,13 +76,6 @@ def test_construction_is_order_sensitive():
     assert cnt[0] == 64 and all(C[0, j] == centre(X[:, j]) for j in range(4))
 
 
-# Shapes span the small-K kernel and every accumulation form of the tile
-# kernel (which one a shape takes depends on what fits in LDS: per-wave slabs
-# for small K*M, one shared slab per wave, or the workgroup slab for large
-# K*M).
-SHAPES = [(16, 25), (48, 25), (64, 25), (100, 25), (256, 25), (1024, 16), (512, 32), (200, 64)]
-
-
 def slab_orders():
     """Addition orders the code fixes for one tile of 64 objects: slab lists
     (objects in ascending order within a slab, the slabs added in order)."""
@@ -108,15 +104,17 @@ def expected_centres(X, labels, K, prev, slabs):
     return C
 
 
-# Shapes span the small-K kernel and every accumulation form of the tile
-# kernel (which one a shape takes depends on what fits in LDS: per-wave slabs
-# for small K*M, one shared slab per wave, or the workgroup slab for large
-# K*M). For the two 25-feature shapes of the named workloads the form is
-# known: K = 64 shares one slab between the two objects of a step, K = 256
-# adds into the workgroup slab with one lane per object; both must give the
-# ascending order.
-SHAPES = [(16, 25, None), (48, 25, None), (64, 25, "ascending"), (100, 25, None),
-          (256, 25, "ascending"), (1024, 16, None), (512, 32, None), (200, 64, None)]
+# Shapes span both forms of the small-K kernel and every accumulation form of
+# the tile kernel (which one a shape takes depends on what fits in LDS:
+# per-wave slabs for small K*M, one shared slab per wave, or the workgroup
+# slab for large K*M). For the 25-feature shapes of the named workloads the
+# form is known: K = 16 adds the halves of a tile to two slabs, K = 64 (small-K
+# kernel, four blocks) shares one slab between the two objects of a step in
+# ascending object order, K = 256 adds into the workgroup slab with one lane
+# per object; the last two must give the ascending order.
+SHAPES = [(16, 25, "halves"), (24, 25, "halves"), (48, 25, "ascending"), (64, 25, "ascending"),
+          (100, 25, None), (256, 25, "ascending"), (1024, 16, None), (512, 32, None),
+          (200, 64, None)]
 
 
 @pytest.mark.gpu

@@ -30,9 +30,11 @@ DEV = torch.device("cuda:0") if torch.cuda.is_available() else None
 U23 = 2.0 ** -23
 
 
-def lane_threshold(cmax, xsq):
-    """One object per lane, K <= 16 (keys carry 4 index bits)."""
-    E = 3.02 * 2.0 ** -16 + 104 * U23 + 1.01 * 2.0 ** -19
+def lane_threshold(cmax, xsq, K):
+    """One object per lane, K <= 64 (keys carry 4, 5 or 6 index bits for one,
+    two or four 16-centre blocks)."""
+    bits = 4 if K <= 16 else 5 if K <= 32 else 6
+    E = 3.02 * 2.0 ** -16 + 104 * U23 + 1.01 * 2.0 ** (bits - 23)
     return 2.02 * E * (3.02 * cmax + 1.0001 * xsq) + 1e-30
 
 
@@ -89,7 +91,7 @@ def _run_one_pass(X, C, path):
     return lab.cpu().numpy(), km.ctl_fallbacks(ws), km.ctl_reruns(ws)
 
 
-@pytest.mark.parametrize("K", [16, 9])
+@pytest.mark.parametrize("K", [16, 9, 24, 64])
 def test_lane_kernel_accepts_near_threshold(K):
     # features 0..6 and 24 are zero, so the lane kernel's |x|^2 (which adds
     # the squares of a few floats past each row, the next object's first
@@ -100,7 +102,8 @@ def test_lane_kernel_accepts_near_threshold(K):
     live[24] = 0
     rng = np.random.default_rng(K)
     C = (rng.uniform(-50, 50, (K, M)) * live).astype(np.float32)
-    X = near_threshold_objects(C, 6000, lane_threshold, K + 1, live)
+    thr = lambda cmax, xsq: lane_threshold(cmax, xsq, K)   # noqa: E731
+    X = near_threshold_objects(C, 6000, thr, K + 1, live)
     lab, fallbacks, _ = _run_one_pass(X, C, "mfma")
     olab = oracle.assign(X, C)
     print(f"[guard lane] K={K}: {len(X)} objects at 1.0-1.3 x the threshold, "

@@ -89,6 +89,9 @@ SHAPES = [
     (4097, 3, 2, "uniform", "farthest"),
     (4099, 25, 16, "blobs", "farthest"),
     (10_001, 7, 33, "uniform", "farthest"),
+    (12_345, 25, 24, "blobs", "farthest"),  # two 16-centre blocks in the small-K kernel
+    (7_777, 19, 32, "uniform", "farthest"),
+    (40_009, 25, 64, "blobs", "farthest"),  # four blocks, one fp64 slab per wave
     (50_003, 25, 16, "blobs", "farthest"),
     (20_011, 32, 64, "blobs", "farthest"),
     (20_013, 33, 8, "blobs", "farthest"),
@@ -134,7 +137,8 @@ def test_run_max_iter_one_and_alias():
 # ------------------------------------------------------------ single steps
 
 @pytest.mark.parametrize("n,M,K", [(1, 1, 1), (777, 2, 3), (65_537, 25, 16), (10_000, 64, 200),
-                                   (4_000, 16, 1024), (3_000, 25, 655)])
+                                   (4_000, 16, 1024), (3_000, 25, 655), (9_001, 12, 20),
+                                   (20_003, 25, 64)])
 @pytest.mark.parametrize("path", PATHS)
 def test_assign_parity(n, M, K, path):
     _say(f"[assign] n={n} M={M} K={K} path={path}")
@@ -198,9 +202,9 @@ def test_split_precision_rerun_parity(K, M):
     assert reruns > 0
 
 
-@pytest.mark.parametrize("K,M", [(16, 25), (9, 27), (12, 7)])
+@pytest.mark.parametrize("K,M", [(16, 25), (9, 27), (12, 7), (24, 25), (64, 25), (40, 13)])
 def test_lane_split_band_parity(K, M):
-    # The one-object-per-lane kernel (K <= 16) scores with split-precision
+    # The one-object-per-lane kernel (K <= 64) scores with split-precision
     # bf16 products and sends every call inside its guard band straight to
     # the fp64 re-decision: half of the objects lie within 1e-4 (relative) of
     # a bisector, so many of them must take that path, and labels, counts and
@@ -225,7 +229,7 @@ def test_lane_split_band_parity(K, M):
 
 
 @pytest.mark.parametrize("n,M,K", [(1, 2, 1), (1000, 3, 7), (65_537, 25, 16), (33_333, 64, 100),
-                                   (10_000, 10, 1024)])
+                                   (10_000, 10, 1024), (5_003, 25, 48), (4_321, 30, 30)])
 def test_update_parity(n, M, K):
     _say(f"[update] n={n} M={M} K={K}")
     rng = np.random.default_rng(n * 3 + K)
