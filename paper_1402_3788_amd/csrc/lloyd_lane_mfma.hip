@@ -58,7 +58,8 @@
 // only that each rounding is faithful (error below one unit in the last place,
 // 2^-23 relative), whatever the order or rounding direction, so the sums err by
 // at most 1.01 * 98 * 2^-23 of (|c|^2 + sum |a b|) <= (3|c|^2 + |x|^2). The
-// fp32 |c|^2 (M fused multiply-adds) errs by 25 * 2^-24 |c|^2 at M = 32.
+// fp32 |c|^2 (eight fused multiply-adds in each of the centre's four lanes,
+// then two additions across them) errs by at most 10 * 2^-23 |c|^2.
 // A packed key with b index bits moves its score by less than 2^(b-23) of
 // the score's magnitude, itself below (1 + E)(3|c|^2 + |x|^2). Together every
 // key is within E (3 max|c|^2 + |x|^2) of the exact score with
@@ -283,35 +284,111 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
     // -2 c_{16cb+o}, features 8g .. 8g+7 (zero past K and M), split into bf16
     // hi and lo, and the accumulator seeds |c_k|^2 of centres k = 16cb + 4g ..
     // 16cb + 4g + 3 (the largest finite float past K, so padding centres never
-    // win and their keys stay finite).
+    // win and their keys stay finite). The centre values are loaded first and
+    // the first tile's loads right after them, so that both are in flight
+    // together; |c|^2 is formed from the same registers (eight fused
+    // multiply-adds per lane, then the four lanes of a centre added pairwise).
     constexpr bool kALds = kDist && lane_a_in_lds(KB);
     uint32_t ah[KB][4], al[KB][4];
     f4v cseed[KB];
     float cmax = 0.f;
+    float craw[KB][8];
+    if (kDist) {
+#pragma unroll
+        for (int cb = 0; cb < KB; ++cb) {
+            const int ko = 16 * cb + o16;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int f = 8 * g + e;
+                craw[cb][e] = (ko < K && f < M) ? C[ko * M + f] : 0.f;
+            }
+        }
+    }
+    const int64_t nt = (n + kWave - 1) / kWave;                    // tiles
+    int64_t nsafe = (n - rows_after(M)) / kWave;                   // unguarded tiles
+    if (nsafe < 0) nsafe = 0;
+    const int64_t stride = (int64_t)gridDim.x * W;
+    const int64_t q0 = (int64_t)wave * gridDim.x + blockIdx.x;
+
+    // operand loads of tile q (unguarded: q < nsafe). Chunk starts are
+    // clamped into the row, so a lane group with fewer than eight features
+    // left reads some of them twice (harmless: A is zero there, and |x|^2 is
+    // an upper bound).
+    const int c0 = 8 * g < M ? 8 * g : 0;
+    const int c1 = 8 * g + 4 < M ? 8 * g + 4 : c0;
+    auto load_ops = [&](int64_t q, f4v (&xb)[4][2]) {
+        const float *tb = X + q * (kWave * M);                 // scalar
+        const int r0 = o16 * M;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            xb[b][0] = *reinterpret_cast<const f4u *>(tb + (r0 + 16 * b * M + c0));
+            xb[b][1] = *reinterpret_cast<const f4u *>(tb + (r0 + 16 * b * M + c1));
+        }
+    };
+    // guarded form for the last tiles: zero past n and past M
+    auto load_ops_tail = [&](int64_t q, f4v (&xb)[4][2]) {
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            const int64_t r = q * kWave + 16 * b + o16;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int f = 8 * g + e;
+                xb[b][e / 4][e % 4] = (r < n && f < M) ? X[r * M + f] : 0.f;
+            }
+        }
+    };
+    const int jr = j < M ? j : M - 1;
+
+    // Accumulation layout: in step s lane (h, j) adds feature j of object
+    // s + 32h of the tile into slab h (two slabs), or of object 2s + h (one
+    // slab: objects in ascending order, the two of a step meeting on an
+    // address only in the LDS's lane order).
+    // accumulation values of tile q (the guarded form reads zeros past n)
+    auto load_acc = [&](int64_t q, float (&xa)[32], auto tail) {
+        constexpr bool kTail = decltype(tail)::value;
+        const float *tb = X + q * (kWave * M);                 // scalar
+        const int c = (S == 2 ? 32 * h : h) * M + jr;
+        constexpr int kObjStride = S == 2 ? 1 : 2;
+#pragma unroll
+        for (int s = 0; s < 32; ++s) {
+            if (kTail) xa[s] = (q * kWave + (S == 2 ? 32 * h : h) + kObjStride * s < n)
+                                   ? tb[c + kObjStride * s * M] : 0.f;
+            else xa[s] = tb[c + kObjStride * s * M];
+        }
+    };
+
+    // the first tile's loads, in flight while the centre operands are formed
+    constexpr int kOpSets = kOneOpSet ? 1 : 2;
+    f4v xb[kOpSets][4][2];
+    float xa[2][32];
+    int64_t q = q0;
+    if (q < nsafe) {
+        if (kDist) load_ops(q, xb[0]);
+        if (kAcc) load_acc(q, xa[0], std::false_type{});
+    }
+
     // the A table in LDS: [hi | lo | seeds][KB][64 lanes], 16 bytes each
     uint4 *atab = reinterpret_cast<uint4 *>(smem + (kAcc ? lane_acc_bytes(M, K, W) : 0));
     if (kDist) {
 #pragma unroll
         for (int cb = 0; cb < KB; ++cb) {
             float a[8];
-            const int ko = 16 * cb + o16;
+            float nrm = 0.f;
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                const int f = 8 * g + e;
-                a[e] = (ko < K && f < M) ? -2.0f * C[ko * M + f] : 0.f;
+                a[e] = -2.0f * craw[cb][e];
+                nrm = __builtin_fmaf(craw[cb][e], craw[cb][e], nrm);
             }
             split_bf16x8(a, ah[cb], al[cb]);
+            // |c_{16cb+o}|^2 in every lane (g, o): (p0 + p1) + (p2 + p3)
+            nrm = nrm + __shfl_xor(nrm, 16, kWave);
+            nrm = nrm + __shfl_xor(nrm, 32, kWave);
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int k = 16 * cb + 4 * g + r;
-                float nk = FLT_MAX;
-                if (k < K) {
-                    nk = 0.f;
-#pragma unroll
-                    for (int f = 0; f < M; ++f) nk = __builtin_fmaf(C[k * M + f], C[k * M + f], nk);
-                    cmax = fmaxf(cmax, nk);
-                }
-                cseed[cb][r] = nk;
+                const float nk = __shfl(nrm, 4 * g + r, kWave);
+                cseed[cb][r] = k < K ? nk : FLT_MAX;
+                if (k < K) cmax = fmaxf(cmax, nk);
             }
             if (kALds && wave == 0) {
                 atab[(0 * KB + cb) * kWave + lane] = make_uint4(ah[cb][0], ah[cb][1], ah[cb][2], ah[cb][3]);
@@ -351,60 +428,8 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
     constexpr uint32_t kIdxMask = (1u << kBits) - 1u;
     constexpr uint32_t kKeyMask = ~kIdxMask;
 
-    const int64_t nt = (n + kWave - 1) / kWave;                    // tiles
-    int64_t nsafe = (n - rows_after(M)) / kWave;                   // unguarded tiles
-    if (nsafe < 0) nsafe = 0;
-    const int64_t stride = (int64_t)gridDim.x * W;
-    const int64_t q0 = (int64_t)wave * gridDim.x + blockIdx.x;
-
-    // operand loads of tile q (unguarded: q < nsafe). Chunk starts are
-    // clamped into the row, so a lane group with fewer than eight features
-    // left reads some of them twice (harmless: A is zero there, and |x|^2 is
-    // an upper bound).
-    const int c0 = 8 * g < M ? 8 * g : 0;
-    const int c1 = 8 * g + 4 < M ? 8 * g + 4 : c0;
-    auto load_ops = [&](int64_t q, f4v (&xb)[4][2]) {
-        const float *tb = X + q * (kWave * M);                 // scalar
-        const int r0 = o16 * M;
-#pragma unroll
-        for (int b = 0; b < 4; ++b) {
-            xb[b][0] = *reinterpret_cast<const f4u *>(tb + (r0 + 16 * b * M + c0));
-            xb[b][1] = *reinterpret_cast<const f4u *>(tb + (r0 + 16 * b * M + c1));
-        }
-    };
-    // guarded form for the last tiles: zero past n and past M
-    auto load_ops_tail = [&](int64_t q, f4v (&xb)[4][2]) {
-#pragma unroll
-        for (int b = 0; b < 4; ++b) {
-            const int64_t r = q * kWave + 16 * b + o16;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int f = 8 * g + e;
-                xb[b][e / 4][e % 4] = (r < n && f < M) ? X[r * M + f] : 0.f;
-            }
-        }
-    };
-    const int jr = j < M ? j : M - 1;
-
     int nfallback = 0;
 
-    // Accumulation layout: in step s lane (h, j) adds feature j of object
-    // s + 32h of the tile into slab h (two slabs), or of object 2s + h (one
-    // slab: objects in ascending order, the two of a step meeting on an
-    // address only in the LDS's lane order).
-    // accumulation values of tile q (the guarded form reads zeros past n)
-    auto load_acc = [&](int64_t q, float (&xa)[32], auto tail) {
-        constexpr bool kTail = decltype(tail)::value;
-        const float *tb = X + q * (kWave * M);                 // scalar
-        const int c = (S == 2 ? 32 * h : h) * M + jr;
-        constexpr int kObjStride = S == 2 ? 1 : 2;
-#pragma unroll
-        for (int s = 0; s < 32; ++s) {
-            if (kTail) xa[s] = (q * kWave + (S == 2 ? 32 * h : h) + kObjStride * s < n)
-                                   ? tb[c + kObjStride * s * M] : 0.f;
-            else xa[s] = tb[c + kObjStride * s * M];
-        }
-    };
     // One tile (kTail: the guarded loads and validity tests): xb / xa hold its
     // operand and accumulation values (loaded one tile earlier); the loads of
     // tile qn go into nxt / xan (unguarded form only; with one operand set,
@@ -659,15 +684,7 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
     // the other register set (accumulation values; operands too with one
     // block); then the guarded tail tiles.
     // (The prefetch past a wave's last unguarded tile reloads tile nsafe - 1.)
-    constexpr int kOpSets = kOneOpSet ? 1 : 2;
-    f4v xb[kOpSets][4][2];
-    float xa[2][32];
-    int64_t q = q0;
     auto next = [&](int64_t qq) { return qq < nsafe ? qq : nsafe - 1; };
-    if (q < nsafe) {
-        if (kDist) load_ops(q, xb[0]);
-        if (kAcc) load_acc(q, xa[0], std::false_type{});
-    }
     for (; q < nsafe; q += 2 * stride) {
         step(q, xb[0], xa[0], xb[kOpSets - 1], xa[1], next(q + stride), std::false_type{});
         if (q + stride >= nsafe) {
