@@ -111,7 +111,7 @@ struct StepArgs {
     const int32_t *labels_in;  // in (mode 2)
     float *min_d2;             // optional out (mode 0)
     double *part_sums;         // [groups][K][M] (modes 1/2)
-    int32_t *part_counts;      // [groups][K]
+    int32_t *part_counts;      // [K][groups]
     float *centers_out;        // new centres (may alias C)
     int32_t *counts_out;       // [K]
     Ctl *ctl;                  // control block (modes 1/2)

@@ -423,12 +423,13 @@ __device__ inline void accumulate_commit(int lab, const AccFetch<M, P_> &f, int3
 
 // Workgroup partial of the wave-accumulation form: for every (cluster, feature)
 // the sum over waves w and slabs h (w, then h, ascending) written to
-// part_sums[K][M], and the counts to part_counts[K]. Call after a barrier.
+// part_sums[K][M], and the count of cluster k to counts_col[k * cstride] (the
+// workgroup's column of the [K][G] count table). Call after a barrier.
 // kShared: one slab per wave (see accumulate_tile).
 template <int M, int P_, bool kShared = false>
 __device__ inline void write_wave_partials(const double *slabs, int W, int K,
                                            double *__restrict__ part_sums,
-                                           int32_t *__restrict__ part_counts)
+                                           int32_t *__restrict__ counts_col, int cstride)
 {
     using A = WaveAcc<M, P_>;
     constexpr int MW = A::MW, P = kShared ? 1 : A::P;
@@ -439,7 +440,7 @@ __device__ inline void write_wave_partials(const double *slabs, int W, int K,
         double s = 0.0;
         for (size_t r = 0; r < rows; ++r) s = s + slabs[(r * K + k) * MW + j];
         if (j < M) part_sums[(int64_t)k * M + j] = s;
-        else part_counts[k] = (int32_t)s;
+        else counts_col[(int64_t)k * cstride] = (int32_t)s;
     }
 }
 

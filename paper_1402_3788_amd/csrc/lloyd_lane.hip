@@ -192,7 +192,7 @@ lloyd_lane_kernel(const float *__restrict__ X, int64_t n, const float *__restric
     if (MODE != kAssign) {
         __syncthreads();
         write_wave_partials<M, PA>(slabs_all, W, K, part_sums + (int64_t)blockIdx.x * K * M,
-                                   part_counts + (int64_t)blockIdx.x * K);
+                                   part_counts + blockIdx.x, gridDim.x);
     }
 }
 

@@ -714,7 +714,7 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
         for (int k = threadIdx.x; k < K; k += blockDim.x) {
             int32_t c = 0;
             for (int w = 0; w < W; ++w) c += allc[w * K + k];
-            part_counts[(int64_t)blockIdx.x * K + k] = c;
+            part_counts[(int64_t)k * gridDim.x + blockIdx.x] = c;
         }
     }
 }

@@ -648,7 +648,7 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
         __syncthreads();
         write_wave_partials<M, PA, kShared>(reinterpret_cast<const double *>(smem + L.slab), W, K,
                                part_sums + (int64_t)blockIdx.x * K * M,
-                               part_counts + (int64_t)blockIdx.x * K);
+                               part_counts + blockIdx.x, gridDim.x);
     } else if (kAcc == kAccRing) {
         __syncthreads();
         constexpr int RS = ring_row(M);
@@ -658,7 +658,7 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
             const int k = e / (M + 1), j = e % (M + 1);
             const double v = slab[k * RS + j];
             if (j < M) out[(int64_t)k * M + j] = v;
-            else part_counts[(int64_t)blockIdx.x * K + k] = (int32_t)v;
+            else part_counts[(int64_t)k * gridDim.x + blockIdx.x] = (int32_t)v;
         }
     }
 }
