@@ -90,16 +90,16 @@ def _parse():
 
 def kernel_key(M: int, K: int, path: str) -> str:
     """Which kernel runs the iteration (mirrors the library's path choice)."""
-    lane_fits = K <= 16 and M <= 32
+    lane_fits = K <= 64 and M <= 32
     if path == "direct":
         return "direct"
     if path == "tiles":
         return "tiles"
     if path == "mfma":
         return "lane-mfma" if lane_fits else "tiles"
-    if K > 16:
-        return "tiles"
-    return "lane-mfma" if (lane_fits and K >= 5) else "direct"
+    if lane_fits and K >= 5:
+        return "lane-mfma"
+    return "tiles" if K > 16 else "direct"
 
 
 def sources_sha256(key: str) -> str:

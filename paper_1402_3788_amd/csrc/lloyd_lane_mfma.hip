@@ -140,34 +140,22 @@ __host__ __device__ constexpr bool lane_a_in_lds(int KB) { return KB > 1; }
 // in X take the unguarded loads.
 [[maybe_unused]] __host__ __device__ inline int64_t rows_after(int M) { return (3 + M - 1) / M; }
 
-// Comparisons of packed keys. A key is a float whose low bits were replaced
-// by an index, so the compiler cannot prove it canonical and would quieten it
-// before every min / max; written out, each is one instruction. Keys of
+// Comparisons of packed keys (a key is a float whose low bits were replaced by
+// an index). Plain floating-point minimum, maximum and median instructions, in
+// compiler-visible form: the compiler then also keeps the wait states that a
+// matrix instruction still reading an operand register needs before the
+// register is overwritten (it cannot do so for inline assembly). Keys of
 // finite scores are finite; a score that overflowed sends its object to the
 // fp64 path (its |x|^2 bound is infinite), whatever these return for it.
-[[maybe_unused]] __device__ inline float key_min(float a, float b)
-{
-    float r;
-    asm("v_min_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
-    return r;
-}
-[[maybe_unused]] __device__ inline float key_max(float a, float b)
-{
-    float r;
-    asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
-    return r;
-}
+[[maybe_unused]] __device__ inline float key_min(float a, float b) { return __builtin_fminf(a, b); }
+[[maybe_unused]] __device__ inline float key_max(float a, float b) { return __builtin_fmaxf(a, b); }
 [[maybe_unused]] __device__ inline float key_min3(float a, float b, float c)
 {
-    float r;
-    asm("v_min3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
-    return r;
+    return __builtin_fminf(__builtin_fminf(a, b), c);
 }
 [[maybe_unused]] __device__ inline float key_med3(float a, float b, float c)
 {
-    float r;
-    asm("v_med3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
-    return r;
+    return __builtin_amdgcn_fmed3f(a, b, c);
 }
 
 // Best and second best of two (best, second) key pairs.
@@ -258,6 +246,11 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
     // registers of the current one once it is split (one register set), which
     // leaves room for the A operands of the other blocks.
     constexpr bool kOneOpSet = KB > 1;
+    // With four blocks a tile's distance work is long enough to cover a read
+    // that hits the cache: the accumulation values of a tile are loaded at the
+    // start of its own step, before the next tile's operand loads (so waiting
+    // for them does not wait for those), in one register set instead of two.
+    constexpr bool kLateAcc = KB == 4 && MODE == kAssignAccum;
     extern __shared__ __align__(16) unsigned char smem[];
     const int W = blockDim.x / kWave;
     // wave-uniform (scalar) wave index, so that tile addresses are scalar
@@ -360,11 +353,11 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
     // the first tile's loads, in flight while the centre operands are formed
     constexpr int kOpSets = kOneOpSet ? 1 : 2;
     f4v xb[kOpSets][4][2];
-    float xa[2][32];
+    float xa[kLateAcc ? 1 : 2][32];
     int64_t q = q0;
     if (q < nsafe) {
         if (kDist) load_ops(q, xb[0]);
-        if (kAcc) load_acc(q, xa[0], std::false_type{});
+        if (kAcc && !kLateAcc) load_acc(q, xa[0], std::false_type{});
     }
 
     // the A table in LDS: [hi | lo | seeds][KB][64 lanes], 16 bytes each
@@ -442,7 +435,8 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
         const bool valid = !kTail || i < n;
         if (!kTail) {
             if (kDist && !kOneOpSet) load_ops(qn, nxt);
-            if (kAcc) load_acc(qn, xan, std::false_type{});
+            if (kAcc && kLateAcc) load_acc(q, xa, std::false_type{});
+            else if (kAcc) load_acc(qn, xan, std::false_type{});
         }
         int lab = 0;
         if (kDist) {
@@ -686,17 +680,18 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
     // (The prefetch past a wave's last unguarded tile reloads tile nsafe - 1.)
     auto next = [&](int64_t qq) { return qq < nsafe ? qq : nsafe - 1; };
     for (; q < nsafe; q += 2 * stride) {
-        step(q, xb[0], xa[0], xb[kOpSets - 1], xa[1], next(q + stride), std::false_type{});
+        step(q, xb[0], xa[0], xb[kOpSets - 1], xa[kLateAcc ? 0 : 1], next(q + stride), std::false_type{});
         if (q + stride >= nsafe) {
             q += stride;
             break;
         }
-        step(q + stride, xb[kOpSets - 1], xa[1], xb[0], xa[0], next(q + 2 * stride), std::false_type{});
+        step(q + stride, xb[kOpSets - 1], xa[kLateAcc ? 0 : 1], xb[0], xa[0], next(q + 2 * stride),
+             std::false_type{});
     }
     for (; q < nt; q += stride) {
         if (kDist) load_ops_tail(q, xb[0]);
         if (kAcc) load_acc(q, xa[0], std::true_type{});
-        step(q, xb[0], xa[0], xb[kOpSets - 1], xa[1], q, std::true_type{});
+        step(q, xb[0], xa[0], xb[kOpSets - 1], xa[kLateAcc ? 0 : 1], q, std::true_type{});
     }
 
     if (ctl != nullptr && lane == 0 && nfallback > 0) atomicAdd(&ctl->fallbacks, nfallback);

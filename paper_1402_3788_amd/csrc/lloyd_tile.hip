@@ -466,19 +466,24 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
                 float k1[kCols], k2[kCols];
                 int kt0 = 0;
                 auto scan_key = [&](int tt, const f4v (&d)[kCols]) {
+                    // the four index values of the lane's centre rows, shared
+                    // by the four columns; one and-or per key, and per column
+                    // two (med3, min3) pairs and a min3 for the running second
+                    // best
                     const uint32_t i0 = (uint32_t)((tt - kt0) * 16 + 4 * g);
+                    const uint32_t iv[4] = {i0, i0 + 1, i0 + 2, i0 + 3};
 #pragma unroll
-                    for (int c = 0; c < kCols; ++c)
+                    for (int c = 0; c < kCols; ++c) {
+                        float sk[4];
 #pragma unroll
-                        for (int r = 0; r < 4; r += 2) {
-                            const float s1 = __uint_as_float(
-                                (__float_as_uint(d[c][r]) & kmask) | (i0 + r));
-                            const float s2 = __uint_as_float(
-                                (__float_as_uint(d[c][r + 1]) & kmask) | (i0 + r + 1));
-                            const float n2 = fminf(k2[c], __builtin_amdgcn_fmed3f(k1[c], s1, s2));
-                            k1[c] = fminf(fminf(k1[c], s1), s2);
-                            k2[c] = n2;
-                        }
+                        for (int r = 0; r < 4; ++r)
+                            sk[r] = __uint_as_float((__float_as_uint(d[c][r]) & kmask) | iv[r]);
+                        const float ma = __builtin_amdgcn_fmed3f(k1[c], sk[0], sk[1]);
+                        const float b1 = fminf(fminf(k1[c], sk[0]), sk[1]);
+                        const float mb = __builtin_amdgcn_fmed3f(b1, sk[2], sk[3]);
+                        k1[c] = fminf(fminf(b1, sk[2]), sk[3]);
+                        k2[c] = fminf(fminf(k2[c], ma), mb);
+                    }
                 };
                 OpsH oA, oB;
                 for (; kt0 < KT; kt0 += gblocks) {

@@ -179,3 +179,65 @@ def test_skewed_clusters_reproducible(K, M):
     C = runs[0][0].cpu().numpy().astype(np.float64)
     scale = np.maximum(np.abs(oC).max(axis=1, keepdims=True), 1e-30)
     assert (np.abs(C - oC) <= 1e-5 * scale).all()
+
+
+# The assign + accumulate launch of the small-K kernel (K <= 64, M <= 32)
+# forms its sums the way the update launch does: with one or two 16-centre
+# blocks the halves of a tile go to two slabs (no two lanes of one add meet),
+# with four blocks the two objects of a step share one slab, in ascending
+# object order only if the LDS applies the lanes of an add in ascending lane
+# order. Checked through kmeans_run, whose labels come from the same launch.
+RUN_SHAPES = [(16, 25, "halves"), (12, 7, "halves"), (16, 32, "halves"),
+              (24, 25, "halves"), (32, 16, "halves"), (48, 25, "ascending"),
+              (64, 25, "ascending"), (64, 32, "ascending")]
+
+
+def labelled_tile(M: int, seed: int, alternate: bool):
+    """64 order-sensitive objects whose nearest initial centre is 0 for all
+    (alternate=False) or 0 for even and 1 for odd objects: feature 0 stays in
+    [-1, 1] (+10^6 for the odd objects when alternating; the squared distances
+    to centres 0 and 1 then differ by about 10^12, far above the fp64 spacing
+    at the objects' norms), the +-2^40 values sit in the other features of
+    the first and last object (and, when alternating, of objects 1 and 62)."""
+    X = order_sensitive(M, seed)
+    X[0, 0], X[63, 0] = 0.5, -0.5
+    if alternate:
+        # each cluster gets a +2^40 and a -2^40 object, so its sums cancel to
+        # values whose low bits depend on the order
+        X[1, 1:], X[62, 1:] = X[0, 1:], X[63, 1:]
+        X[1::2, 0] += 1.0e6
+    return X
+
+
+def far_centres(K: int, M: int) -> np.ndarray:
+    C = np.zeros((K, M), np.float32)
+    C[1, 0] = 1.0e6
+    for k in range(2, K):
+        C[k, 0] = -1e15 * k           # never the nearest
+    return C
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("K,M,want", RUN_SHAPES)
+def test_assign_accumulate_follows_lane_order(K, M, want):
+    """One fixed-count iteration of kmeans_run (assignment and the sums of
+    Eq. (1) in one launch) on a one-tile problem: the new centres equal those of
+    the addition order the code fixes, on every seed and labelling."""
+    print(f"[order-run] K={K} M={M}", flush=True)
+    init = far_centres(K, M)
+    orders = slab_orders()
+    for seed in range(8):
+        for alternate in (False, True):
+            X = labelled_tile(M, 5000 * K + 10 * M + seed, alternate)
+            labels = (np.arange(64) % 2 if alternate else np.zeros(64)).astype(np.int32)
+            assert np.array_equal(oracle.assign(X, init), labels)
+            lab, C, cnt, it = km.kmeans_run(torch.from_numpy(X).to(DEV), K,
+                                            torch.from_numpy(init).to(DEV), 1, fixed_iters=True)
+            assert it == 1 and np.array_equal(lab.cpu().numpy(), labels)
+            assert np.array_equal(cnt.cpu().numpy(), np.bincount(labels, minlength=K))
+            got = C.cpu().numpy().view(np.uint32)
+            want_c = expected_centres(X, labels, K, init, orders[want]).view(np.uint32)
+            other = [nm for nm, sl in orders.items()
+                     if np.array_equal(got, expected_centres(X, labels, K, init, sl).view(np.uint32))]
+            assert np.array_equal(got, want_c), f"seed {seed}: centres match {other}, not {want}"
+    print(f"[order-run] K={K} M={M}: sums formed in the order {want}", flush=True)
