@@ -28,11 +28,15 @@
 //      rounds of row swaps (v_permlane32_swap, then v_permlane16_swap) leave
 //      lane l with the two best keys of object l; a label is accepted when the
 //      two differ by more than twice the proven error bound thr/2. Otherwise
-//      (a close call) the keys are formed again, every centre whose key is
-//      within thr of the best becomes a candidate (no other centre can be the
-//      nearest), and the object is decided among its candidates with fp64
-//      distances in the reference operation order (lowest index on ties), so
-//      every label is the exact-arithmetic argmin;
+//      (a close call) the keys of the object's column are formed again from
+//      the same split operands, every centre whose key is within thr of the
+//      best becomes a candidate (no other centre can be the nearest), and the
+//      object is decided among its candidates with fp64 distances in the
+//      reference operation order (lowest index on ties): one close object at
+//      a time, its features made wave-uniform, lane k computing the distance
+//      to centre k from an LDS copy of the centres, so that no memory read
+//      of the close path waits behind the next tile's loads. Every label is
+//      the exact-arithmetic argmin;
 //   5. accumulation (the numerator and denominator of Eq. (1)): lane l
 //      writes the slab row offset of object l to the wave's offset table;
 //      lanes (h, .) read the offsets of their 32 objects back with broadcast
@@ -120,19 +124,25 @@ __host__ __device__ constexpr int lane_slabs(int KB) { return KB == 4 ? 1 : 2; }
 __host__ __device__ constexpr bool lane_a_in_lds(int KB) { return KB > 1; }
 
 // LDS of a workgroup: with accumulation [W][S][K][M] fp64 slabs, [W][K] int32
-// counts and [W][64] int32 slab offsets of the objects of the current tile;
-// with distances and more than one block, the A table [3][KB][64] x 16 bytes.
+// counts and [W][64] int32 slab offsets of the objects of the current tile
+// (rounded up to 16 bytes); with distances, the A table [3][KB][64] x 16 bytes
+// when there is more than one block, then the centres [K][M] in fp32 (read by
+// the fp64 re-decisions of close calls).
 [[maybe_unused]] __host__ __device__ inline size_t lane_acc_bytes(int M, int K, int W)
 {
     const int S = lane_slabs(lane_blocks(K));
-    return (size_t)W * S * K * M * 8 + (size_t)W * K * 4 + (size_t)W * kWave * 4;
+    return ((size_t)W * S * K * M * 8 + (size_t)W * K * 4 + (size_t)W * kWave * 4 + 15) & ~size_t(15);
+}
+[[maybe_unused]] __host__ __device__ inline size_t lane_tab_bytes(int K, Mode mode)
+{
+    const int KB = lane_blocks(K);
+    return (mode != kAccumLabels && lane_a_in_lds(KB)) ? (size_t)3 * KB * kWave * 16 : 0;
 }
 [[maybe_unused]] __host__ __device__ inline size_t lane_lds_bytes(int M, int K, int W, Mode mode)
 {
-    const int KB = lane_blocks(K);
     const size_t acc = mode == kAssign ? 0 : lane_acc_bytes(M, K, W);
-    const size_t tab = (mode != kAccumLabels && lane_a_in_lds(KB)) ? (size_t)3 * KB * kWave * 16 : 0;
-    return acc + tab;
+    const size_t ctab = mode != kAccumLabels ? (size_t)(lane_blocks(K) == 1 ? W : 1) * K * M * 4 : 0;
+    return acc + lane_tab_bytes(K, mode) + ctab;
 }
 
 // Object rows after the last row of a tile that the operand loads may touch
@@ -360,8 +370,12 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
         if (kAcc && !kLateAcc) load_acc(q, xa[0], std::false_type{});
     }
 
-    // the A table in LDS: [hi | lo | seeds][KB][64 lanes], 16 bytes each
+    // the A table in LDS: [hi | lo | seeds][KB][64 lanes], 16 bytes each; then
+    // the centres, [K][M] fp32
     uint4 *atab = reinterpret_cast<uint4 *>(smem + (kAcc ? lane_acc_bytes(M, K, W) : 0));
+    float *ctab_w = reinterpret_cast<float *>(smem + (kAcc ? lane_acc_bytes(M, K, W) : 0) +
+                                              lane_tab_bytes(K, (Mode)MODE)) +
+                    (kALds ? 0 : wave * K * M);
     if (kDist) {
 #pragma unroll
         for (int cb = 0; cb < KB; ++cb) {
@@ -383,6 +397,12 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
                 cseed[cb][r] = k < K ? nk : FLT_MAX;
                 if (k < K) cmax = fmaxf(cmax, nk);
             }
+            if (!kALds || wave == 0) {
+                const int ko = 16 * cb + o16;
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    if (ko < K && 8 * g + e < M) ctab_w[ko * M + 8 * g + e] = craw[cb][e];
+            }
             if (kALds && wave == 0) {
                 atab[(0 * KB + cb) * kWave + lane] = make_uint4(ah[cb][0], ah[cb][1], ah[cb][2], ah[cb][3]);
                 atab[(1 * KB + cb) * kWave + lane] = make_uint4(al[cb][0], al[cb][1], al[cb][2], al[cb][3]);
@@ -393,7 +413,10 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
         }
         cmax = fmaxf(cmax, __shfl_xor(cmax, 16, kWave));
         cmax = fmaxf(cmax, __shfl_xor(cmax, 32, kWave));
+        // the tables are read by other lanes (and, for the shared ones, other
+        // waves) from here on
         if (kALds) __syncthreads();
+        else __builtin_amdgcn_wave_barrier();
     }
     // block cb's operands and seeds: registers, or the LDS table
     auto a_ops = [&](int cb, uint32_t (&h4)[4], uint32_t (&l4)[4], f4v &seed) {
@@ -509,7 +532,8 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
             const bool ok = !force64 && ((K == 1) || (b2 - b1 > thr));
             float dmin = 0.f;
             const bool close = valid && !ok;
-            if (__ballot(close) != 0) {
+            const uint64_t cmask = __ballot(close);
+            if (cmask != 0ull) {
                 if (force64) {
                     if (valid) {
                         double bd;
@@ -520,108 +544,127 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
                     // Close calls: only centres whose key is within thr of the
                     // best key can be the nearest (a key errs by at most half
                     // of thr, so any other centre's exact score exceeds the
-                    // best centre's). The keys are formed again exactly as
-                    // above, each lane marks its candidates for the object of
-                    // each column, the four lanes of an object combine their
-                    // marks, and the object's lane decides among its
-                    // candidates with fp64 distances in ascending index order
-                    // (lowest index on ties).
+                    // best centre's). The object's features are loaded first
+                    // (in flight during the rest); then, for each column that
+                    // holds a close call, the keys are formed again exactly as
+                    // above from the same split operands, each lane marks its
+                    // candidates for the object of the column, and the four
+                    // lanes of an object combine their marks; the object's
+                    // lane decides among its candidates with fp64 distances in
+                    // ascending index order (lowest index on ties), the
+                    // centres read from the workgroup's LDS copy.
                     const float lim_own = close ? b1 + thr : -INFINITY;
+                    // the limits of the four lanes o16 + 16b (b = 0..3) in
+                    // every lane: a 32-lane swap leaves rows r and r + 2 in
+                    // the lanes of rows r and r + 2 (r = 0, 1), two 16-lane
+                    // swaps then rows 0 and 1, and rows 2 and 3
+                    float lim4[4];
+                    {
+                        float lo = lim_own, hi = lim_own;
+                        swap32(lo, hi);
+                        float r0 = lo, r1 = lo, r2 = hi, r3 = hi;
+                        swap16(r0, r1);
+                        swap16(r2, r3);
+                        lim4[0] = r0;
+                        lim4[1] = r1;
+                        lim4[2] = r2;
+                        lim4[3] = r3;
+                    }
                     uint32_t clo = 0u, chi = 0u;
-                    // one column at a time; with one operand register set
-                    // (which holds the next tile by now) the column's
-                    // operands are read again, in a loop kept rolled so that
-                    // only one column's values are live
-                    auto column = [&](int b, const float (&v)[8]) {
-                        uint32_t rh[4], rl[4];
-                        split_bf16x8(v, rh, rl);
-                        const float lim = __shfl(lim_own, 16 * b + o16, kWave);
+#pragma unroll
+                    for (int b = 0; b < 4; ++b) {
+                        if (((cmask >> (16 * b)) & 0xffffull) == 0ull) continue;   // uniform
+                        const float lim = lim4[b];
                         uint32_t mlo = 0u, mhi = 0u;
 #pragma unroll
                         for (int cb = 0; cb < KB; ++cb) {
                             uint32_t h4[4], l4[4];
                             f4v d;
                             a_ops(cb, h4, l4, d);
-                            d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf8(l4), as_bf8(rh), d, 0, 0, 0);
-                            d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf8(h4), as_bf8(rl), d, 0, 0, 0);
-                            d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf8(h4), as_bf8(rh), d, 0, 0, 0);
+                            d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf8(l4), as_bf8(bh[b]), d, 0, 0, 0);
+                            d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf8(h4), as_bf8(bl[b]), d, 0, 0, 0);
+                            d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf8(h4), as_bf8(bh[b]), d, 0, 0, 0);
 #pragma unroll
                             for (int r = 0; r < 4; ++r) {
                                 const uint32_t idx = i0 + (uint32_t)(16 * cb + r);
                                 const float key =
                                     __uint_as_float((__float_as_uint(d[r]) & kKeyMask) | idx);
-                                const uint32_t bit = key <= lim ? 1u << (idx & 31u) : 0u;
+                                // bit idx - i0 of the word (an immediate), shifted by
+                                // i0 below
+                                const uint32_t bit = key <= lim ? 1u << (16 * (cb & 1) + r) : 0u;
                                 if (cb < 2) mlo |= bit;
                                 else mhi |= bit;
                             }
                         }
+                        mlo <<= i0;
+                        mhi <<= i0;
                         // lane l16 + 16b keeps the marks of its own object
                         mlo = or_rows(mlo);
                         if (KB == 4) mhi = or_rows(mhi);
                         clo = g == b ? mlo : clo;
                         chi = g == b ? mhi : chi;
-                    };
-                    if (kOneOpSet) {
-#pragma unroll 1
-                        for (int b = 0; b < 4; ++b) {
-                            float v[8];
-                            if (kTail) {
-                                const int64_t r = q * kWave + 16 * b + o16;
-#pragma unroll
-                                for (int e = 0; e < 8; ++e) {
-                                    const int f = 8 * g + e;
-                                    v[e] = (r < n && f < M) ? X[r * M + f] : 0.f;
-                                }
-                            } else {
-                                const float *rb = X + q * (kWave * M) + (o16 * M + 16 * b * M);
-                                const f4v u0 = *reinterpret_cast<const f4u *>(rb + c0);
-                                const f4v u1 = *reinterpret_cast<const f4u *>(rb + c1);
-#pragma unroll
-                                for (int e = 0; e < 4; ++e) {
-                                    v[e] = u0[e];
-                                    v[4 + e] = u1[e];
-                                }
-                            }
-                            column(b, v);
-                        }
-                    } else {
-#pragma unroll
-                        for (int b = 0; b < 4; ++b) {
-                            float v[8];
-#pragma unroll
-                            for (int e = 0; e < 8; ++e) v[e] = xb[b][e / 4][e % 4];
-                            column(b, v);
-                        }
                     }
                     if (K < 32) clo &= (1u << K) - 1u;      // padding centres never count
                     if (K > 32 && K < 64) chi &= (1u << (K - 32)) - 1u;
-                    if (close) {
-                        const float *xs = X + i * M;
-                        double best = INFINITY;
-                        int bl = 0;
-                        while (clo != 0u) {
-                            const int k = __builtin_ctz(clo);
-                            clo &= clo - 1u;
-                            const double dd = dist_fp64<M>(xs, C + k * M);
-                            if (dd < best) {
-                                best = dd;
-                                bl = k;
+                    // The fp64 decisions, one close object at a time: its
+                    // features are made wave-uniform (scalars), lane k
+                    // computes the distance to centre k if that is one of the
+                    // object's candidates (the fp64 sum in the reference
+                    // order), and a butterfly over the lanes keeps the
+                    // smallest distance, the lowest index on ties. A distance
+                    // that is not below infinity (overflow, NaN) never wins,
+                    // and with no finite distance the label is 0: what the
+                    // ascending scan with a strict comparison gives.
+                    uint64_t rem = cmask;
+                    while (rem != 0ull) {
+                        const int l = (int)__builtin_ctzll(rem);     // uniform
+                        rem &= rem - 1ull;
+                        float xr[M];
+                        if constexpr (kAcc) {
+                            // the tile's accumulation registers hold the
+                            // object's features (feature f of object l in lane
+                            // 32h + f, register s): the register is picked by
+                            // selects and read out lane by lane, so that no
+                            // memory read waits behind the next tile's loads
+                            const int sl = S == 2 ? (l & 31) : (l >> 1);
+                            const int hl = S == 2 ? (l >> 5) : (l & 1);
+                            float v = xa[0];
+#pragma unroll
+                            for (int u = 1; u < 32; ++u) v = sl == u ? xa[u] : v;
+#pragma unroll
+                            for (int f = 0; f < M; ++f)
+                                xr[f] = __int_as_float(
+                                    __builtin_amdgcn_readlane(__float_as_int(v), 32 * hl + f));
+                        } else {
+                            const float *xs = X + (q * kWave + l) * M;   // uniform address
+#pragma unroll
+                            for (int f = 0; f < M; ++f) xr[f] = xs[f];
+                        }
+                        const uint64_t cand =
+                            ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)chi, l) << 32) |
+                            (uint32_t)__builtin_amdgcn_readlane((int)clo, l);
+                        double dk = INFINITY;
+                        if ((cand >> lane) & 1ull) {
+                            const double dd = dist_fp64<M>(xr, ctab_w + lane * M);
+                            dk = dd < INFINITY ? dd : INFINITY;
+                        }
+                        int kk = lane;
+#pragma unroll
+                        for (int m = 1; m < kWave; m <<= 1) {
+                            const double od = __shfl_xor(dk, m, kWave);
+                            const int ok2 = __shfl_xor(kk, m, kWave);
+                            if (od < dk || (od == dk && ok2 < kk)) {
+                                dk = od;
+                                kk = ok2;
                             }
                         }
-                        while (chi != 0u) {
-                            const int k = 32 + __builtin_ctz(chi);
-                            chi &= chi - 1u;
-                            const double dd = dist_fp64<M>(xs, C + k * M);
-                            if (dd < best) {
-                                best = dd;
-                                bl = k;
-                            }
+                        if (lane == l) {
+                            lab = kk;
+                            dmin = (float)dk;
                         }
-                        lab = bl;
-                        dmin = (float)best;
                     }
                 }
-                if (ctl != nullptr) nfallback += __popcll(__ballot(close));
+                if (ctl != nullptr) nfallback += __popcll(cmask);
             }
             if (MODE == kAssign && min_d2 != nullptr && valid && ok) {
                 const float *xg = X + i * M;
