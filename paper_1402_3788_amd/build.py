@@ -18,14 +18,17 @@ LIB = os.path.join(HERE, "libkmeans_mi355x.so")
 # compiler's iterative scheduler aiming at occupancy (measured per launch at
 # n = 2e6, M = 25, K = 16: 38.2 us against 39.1 with the default scheduler and
 # 38.9 with the instruction-level-parallelism one; the same as the default at
-# K = 64 on 2e7 objects; the tile kernel is slower with any of them).
-UNIT_FLAGS = {"lloyd_lane_mfma.hip": ["-mllvm", "-amdgpu-sched-strategy=iterative-maxocc"]}
+# K = 64 on 2e7 objects; the tile kernel is slower with any of them); the L1
+# assignment kernel for instruction-level parallelism (an L1 iteration at
+# K = 16: 110.4 us against 113.3 with the default scheduler).
+UNIT_FLAGS = {"lloyd_lane_mfma.hip": ["-mllvm", "-amdgpu-sched-strategy=iterative-maxocc"],
+              "lloyd_l1.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp"]}
 # (source, extra flags, object name); the kernel files are compiled once per
 # part of the feature-count range so the template instantiations build in parallel
 PARTS = 4
 SOURCES = ([("kmeans_api.hip", [], "kmeans_api.o"), ("lloyd_ctl.hip", [], "lloyd_ctl.o"),
             ("lloyd_centres.hip", [], "lloyd_centres.o"), ("farthest.hip", [], "farthest.o"),
-            ("diameter.hip", [], "diameter.o"), ("lloyd_l1.hip", [], "lloyd_l1.o")]
+            ("diameter.hip", [], "diameter.o"), ("lloyd_l1.hip", UNIT_FLAGS["lloyd_l1.hip"], "lloyd_l1.o")]
            + [(f, [f"-DLLOYD_PART={p}", *UNIT_FLAGS.get(f, [])], f.replace(".hip", f"_part{p}.o"))
               for f in ("lloyd_tile.hip", "lloyd_lane.hip", "lloyd_lane_mfma.hip")
               for p in range(PARTS)])
