@@ -590,8 +590,12 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
                                 const float key =
                                     __uint_as_float((__float_as_uint(d[r]) & kKeyMask) | idx);
                                 // bit idx - i0 of the word (an immediate), shifted by
-                                // i0 below
-                                const uint32_t bit = key <= lim ? 1u << (16 * (cb & 1) + r) : 0u;
+                                // i0 below; a centre is ruled out only by a key
+                                // above the limit, so a NaN key (a score that
+                                // overflowed, or values read past the object's
+                                // features that hold an infinity or a NaN) or a NaN
+                                // limit keeps every such centre a candidate
+                                const uint32_t bit = !(key > lim) ? 1u << (16 * (cb & 1) + r) : 0u;
                                 if (cb < 2) mlo |= bit;
                                 else mhi |= bit;
                             }

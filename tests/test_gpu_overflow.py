@@ -1,0 +1,63 @@
+"""Objects whose fp32 scores overflow, and non-finite objects.
+
+An object with a coordinate near the largest fp32 value has fp32 scores
+|c|^2 - 2 x.c that overflow to infinity for some centres, while its fp64
+distances (Eq. (2), the oracle's arithmetic) stay finite. Its |x|^2 bound is
+infinite, so every kernel sends it to the fp64 decision; that decision must
+then consider every centre an exact argmin could pick, including the ones
+whose overflowed score left no usable key. Near 3e38 the squared coordinate
+dominates the fp64 sum, so the distances to most centres round to the same
+value and the label is the lowest index among them (the oracle's strict
+comparison in ascending order): a centre left out of the decision shows up
+as a different label. Objects holding NaN or an infinity have no finite
+distance; the oracle labels them 0, and so must the kernels.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_1402_3788_amd as km
+
+pytestmark = pytest.mark.gpu
+
+DEV = torch.device("cuda:0") if torch.cuda.is_available() else None
+
+# (K, path): the direct form, the small-K kernel with one and four blocks, tiles
+CASES = [(4, "direct"), (16, None), (40, None), (64, None), (300, "tiles")]
+
+
+def objects(K: int, seed: int):
+    rng = np.random.default_rng(seed)
+    n, M = 4099, 25
+    C = rng.uniform(0.6, 2.0, (K, M)).astype(np.float32)
+    X = rng.normal(0.0, 1.0, (n, M)).astype(np.float32)
+    big = [(5, 3, 3.0e38), (64, 7, -3.0e38), (100, 0, 3.3e38), (2000, 24, 1.5e38),
+           (2001, 12, -2.9e38), (4098, 1, 3.0e38)]
+    for i, j, v in big:
+        X[i, j] = v
+    X[777, 5:9] = 2.5e38                   # several overflowing coordinates
+    X[7, 2] = np.nan
+    X[8, 4] = np.inf
+    X[9, 1] = -np.inf
+    X[10, :] = np.nan
+    return X, C, [b[0] for b in big] + [777, 7, 8, 9, 10]
+
+
+@pytest.mark.parametrize("K,path", CASES)
+def test_overflowing_and_nonfinite_objects_follow_the_oracle(K, path):
+    print(f"[overflow] K={K} path={path}", flush=True)
+    for seed in range(3):
+        X, C, special = objects(K, 100 * K + seed)
+        want = oracle.assign(X, C)
+        Xg, Cg = torch.from_numpy(X).to(DEV), torch.from_numpy(C).to(DEV)
+        got = km.kmeans_assign(Xg, Cg, path=path).cpu().numpy()
+        bad = np.flatnonzero(got != want)
+        assert bad.size == 0, (f"seed {seed}: {bad.size} labels differ, e.g. objects {bad[:8].tolist()} "
+                               f"(special objects {special}): got {got[bad[:8]].tolist()}, "
+                               f"oracle {want[bad[:8]].tolist()}")
+        # the fused assign + accumulate launch takes the same decisions
+        lab, _, cnt, it = km.kmeans_run(Xg, K, Cg, 1, fixed_iters=True, path=path)
+        assert it == 1
+        assert np.array_equal(lab.cpu().numpy(), want)
+        assert np.array_equal(cnt.cpu().numpy(), np.bincount(want, minlength=K))
