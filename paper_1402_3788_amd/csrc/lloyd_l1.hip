@@ -106,7 +106,10 @@ lloyd_l1_kernel(const float *__restrict__ X, int64_t n, int M, const float *__re
             }
         }
         float best = b1;
-        const bool close = force64 || (b2 != INFINITY && !(b2 - b1 > tau * (b1 + b2)));
+        // every fp32 distance overflowed or is NaN (b1 never set): the fp64
+        // distances may still tell the centres apart
+        const bool close = force64 || !(b1 < INFINITY) ||
+                           (b2 != INFINITY && !(b2 - b1 > tau * (b1 + b2)));
         if (close && i < n) {
             // too close to call in fp32: every centre again in fp64
             double bd = INFINITY;

@@ -61,3 +61,29 @@ def test_overflowing_and_nonfinite_objects_follow_the_oracle(K, path):
         assert it == 1
         assert np.array_equal(lab.cpu().numpy(), want)
         assert np.array_equal(cnt.cpu().numpy(), np.bincount(want, minlength=K))
+
+
+def test_l1_overflowing_and_nonfinite_objects_follow_the_oracle():
+    """The L1 assignment: objects whose fp32 L1 distances to every centre
+    overflow (two coordinates near 3e38) while the fp64 distances still differ
+    (the centres are spread by 1e31 along the first coordinate, so the fp64
+    sums tell them apart and the farthest-out centre is the nearest), and
+    objects holding NaN or an infinity."""
+    rng = np.random.default_rng(11)
+    n, M, K = 4099, 25, 16
+    C = rng.uniform(-1.0, 1.0, (K, M)).astype(np.float32)
+    C[:, 0] = (np.arange(K) * 1.0e31).astype(np.float32)
+    X = rng.normal(0.0, 1.0, (n, M)).astype(np.float32)
+    X[:, 0] += C[rng.integers(0, K, n), 0]
+    for i in (3, 500, 4097):
+        X[i, 0], X[i, 1] = 3.0e38, 3.0e38
+    X[7, 2], X[8, 4], X[9, 1] = np.nan, np.inf, -np.inf
+    want = oracle.assign(X, C, metric="l1")
+    assert want[3] == K - 1                 # the premise: fp64 tells the centres apart
+    Xg, Cg = torch.from_numpy(X).to(DEV), torch.from_numpy(C).to(DEV)
+    got = km.kmeans_assign(Xg, Cg, metric="l1").cpu().numpy()
+    bad = np.flatnonzero(got != want)
+    assert bad.size == 0, f"objects {bad[:8].tolist()}: got {got[bad[:8]].tolist()}, oracle {want[bad[:8]].tolist()}"
+    lab, _, cnt, it = km.kmeans_run(Xg, K, Cg, 1, fixed_iters=True, metric="l1")
+    assert it == 1 and np.array_equal(lab.cpu().numpy(), want)
+    assert np.array_equal(cnt.cpu().numpy(), np.bincount(want, minlength=K))
