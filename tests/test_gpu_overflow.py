@@ -87,3 +87,27 @@ def test_l1_overflowing_and_nonfinite_objects_follow_the_oracle():
     lab, _, cnt, it = km.kmeans_run(Xg, K, Cg, 1, fixed_iters=True, metric="l1")
     assert it == 1 and np.array_equal(lab.cpu().numpy(), want)
     assert np.array_equal(cnt.cpu().numpy(), np.bincount(want, minlength=K))
+
+
+@pytest.mark.parametrize("case", ["nan", "inf", "nan_first", "huge"])
+def test_farthest_init_with_nonfinite_objects_follows_the_oracle(case):
+    """Farthest-point initial centres (Algorithm 1 step 1) on objects with a
+    NaN, an infinity (a NaN distance never lowers an object's nearest-centre
+    distance, an infinite one makes the object the farthest), a first object
+    of NaNs, and coordinates near the fp32 maximum: the same indices as the
+    oracle's traversal."""
+    rng = np.random.default_rng(5)
+    n, M, K = 3001, 25, 16
+    X = rng.normal(0.0, 1.0, (n, M)).astype(np.float32)
+    if case == "nan":
+        X[17, 3] = np.nan
+    elif case == "inf":
+        X[17, 3] = np.inf
+    elif case == "nan_first":
+        X[0, :] = np.nan
+    else:
+        X[100, 2], X[200, 5] = 3.0e38, -3.0e38
+    want = np.asarray(oracle.init_farthest(X, K)).ravel()
+    got, _ = km.kmeans_init_farthest(torch.from_numpy(X).to(DEV), K)
+    got = got.cpu().numpy().ravel() if hasattr(got, "cpu") else np.asarray(got).ravel()
+    assert np.array_equal(got[:K], want[:K])
