@@ -181,7 +181,9 @@ size_t kmeans_diameter_workspace_bytes(int64_t n, int32_t M);
  *   pair    = (k, l), the lexicographically smallest pair reaching it
  *             (DEVICE int32 [2]);
  *   centroid (may be NULL) = the centre of gravity, as kmeans_centroid.
- * With n = 1 there is no pair: *d2 = 0 and pair = (0, 0). The diameter is
+ * With n = 1 there is no pair: *d2 = 0 and pair = (0, 0). If X holds a NaN
+ * or an infinity the diameter is not defined: *d2 = NaN and pair = (-1, -1)
+ * (kmeans_init_farthest_from refuses such seeds). The diameter is
  * sqrt(*d2). The pairs are screened with split-precision bf16 matrix
  * products under a proven error bound and the close ones re-evaluated in
  * fp64, so the result is exact; the cost is two passes over all n(n-1)/2

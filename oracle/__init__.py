@@ -221,7 +221,8 @@ def centroid(X):
 def diameter(X):
     """Eq. (3), squared (Algorithm 2 step 1): (d2, k, l) with d2 the largest
     squared distance over pairs k < l (fp64) and (k, l) the lexicographically
-    smallest pair reaching it; (0.0, 0, 0) when n == 1. O(n^2 M)."""
+    smallest pair reaching it; (0.0, 0, 0) when n == 1; (nan, -1, -1) when a
+    coordinate is NaN or infinite (the diameter is not defined). O(n^2 M)."""
     X = _f32(X)
     n, M = X.shape
     d2 = ctypes.c_double(0.0)

@@ -344,6 +344,16 @@ int oracle_diameter(const float *X, int64_t n, int32_t M, double *d2, int32_t *k
 {
     if (!X || !d2 || !k_out || !l_out || n < 1 || M < 1)
         return ORACLE_EINVAL;
+    /* A coordinate that is NaN or infinite leaves the diameter undefined (the
+     * paper defines it for real vectors): NaN and the pair (-1, -1). */
+    for (int64_t e = 0; e < n * (int64_t)M; ++e) {
+        if (!isfinite(X[e])) {
+            *d2 = NAN;
+            *k_out = -1;
+            *l_out = -1;
+            return 0;
+        }
+    }
     double best = 0.0;
     int64_t bk = 0, bl = n > 1 ? 1 : 0;
     int have = 0;

@@ -29,7 +29,8 @@ struct DiameterArgs {
     int M;
     float *centroid_ws;       // [M] centre of gravity (written by launch_centroid)
     uint4 *ah, *al, *bh, *bl; // [npad][4 ks] split operands
-    uint32_t *counters;       // [0] largest |y|^2 (fp32 bits), [1] key of the pass-1 maximum
+    uint32_t *counters;       // [0] largest |y|^2 (fp32 bits), [1] key of the pass-1 maximum,
+                              // [2] nonzero if X holds a NaN or an infinity
     DiamBest *slots;          // [row_blocks * chunks]
     double *d2;               // out: squared diameter
     int32_t *pair;            // out: [2] the pair

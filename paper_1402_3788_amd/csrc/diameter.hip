@@ -57,6 +57,7 @@
 #include "lloyd_device.h"
 #include "diameter.h"
 
+#include <cfloat>
 #include <climits>
 
 namespace lloyd {
@@ -119,7 +120,8 @@ __global__ void centroid_final_kernel(const double *__restrict__ part, int G, in
         if (centroid_ws) centroid_ws[j] = c;
         if (centroid_out) centroid_out[j] = c;
     }
-    if (counters && threadIdx.x < 2) counters[threadIdx.x] = 0;   // max norm, key of d~*
+    // max norm, key of d~*, non-finite coordinate seen
+    if (counters && threadIdx.x < 3) counters[threadIdx.x] = 0;
 }
 
 // ---------------------------------------------------------------------------
@@ -137,11 +139,17 @@ diam_prep_kernel(const float *__restrict__ X, int64_t n, int64_t npad, int M,
     float y[P];
     float nrm = 0.f;
     const bool real = i < n;
+    bool finite = true;
 #pragma unroll
     for (int f = 0; f < P; ++f) {
-        y[f] = (real && f < M) ? X[i * M + f] - C[f] : 0.f;
+        const float x = (real && f < M) ? X[i * M + f] : 0.f;
+        finite = finite && fabsf(x) < INFINITY;
+        y[f] = (real && f < M) ? x - C[f] : 0.f;
         nrm = nrm + y[f] * y[f];
     }
+    // a NaN or an infinite coordinate leaves the diameter undefined: the
+    // passes return at once and the result is NaN with the pair (-1, -1)
+    if (__ballot(!finite) != 0ull && threadIdx.x % kWave == 0) atomicOr(&counters[2], 1u);
     if (i < npad) {
 #pragma unroll
         for (int g = 0; g < 4 * KS; ++g) {
@@ -186,7 +194,10 @@ __device__ inline bool diam_better(double d, int k, int l, double bd, int bk, in
     return d > bd || (d == bd && (k < bk || (k == bk && l < bl_)));
 }
 
-// Threshold of pass 2: d~* - 2B, rounded down to fp32.
+// Threshold of pass 2: d~* - 2B, rounded down to fp32; minus infinity (every
+// pair re-evaluated in fp64) when the largest norm is so large that an fp32
+// pair value may overflow (a value is at most 4 max n_i), where the bound no
+// longer holds.
 template <int KS>
 __device__ inline float diam_threshold(const uint32_t *counters, int M)
 {
@@ -196,6 +207,7 @@ __device__ inline float diam_threshold(const uint32_t *counters, int M)
     auto phi = [&](int m) { return 2.0 * m * u / (1.0 - 2.0 * m * u); };
     const double E = 4.01 * u + 4.03 * 1.52587890625e-05 + 1.01 * gamma(M) + 2.02 * phi(3 * P + 2);
     const double maxn = (double)__uint_as_float(counters[0]);
+    if (!(4.0 * maxn < (double)FLT_MAX)) return -INFINITY;
     const double B = 1.25 * 2.02 * E * maxn;
     const double thr = (double)key_float(counters[1]) - 2.0 * B;
     float t = (float)thr;
@@ -236,6 +248,7 @@ diam_pass_body(const uint4 *__restrict__ ah, const uint4 *__restrict__ al,
     __shared__ float wmax[kDiamWaves];
     __shared__ DiamBest wbest[kDiamWaves];
 
+    if (counters[2] != 0u) return;                    // non-finite input (uniform)
     const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
     const int64_t I0 = (int64_t)blockIdx.x * kRowBlock;
     const int64_t J0 = (int64_t)blockIdx.y * kChunk;
@@ -365,7 +378,7 @@ diam_pass_body(const uint4 *__restrict__ ah, const uint4 *__restrict__ al,
                                  fmaxf(acc[rb][cc][2], acc[rb][cc][3]));
             if constexpr (!kExact) {
                 vmax = fmaxf(vmax, smax);
-            } else if (__builtin_amdgcn_ballot_w64(smax >= thr) != 0) {
+            } else if (__builtin_amdgcn_ballot_w64(!(smax < thr)) != 0) {
                 // rare: some pair of this wave's half step reaches the threshold
                 const int64_t c0 = s * 64 + 32 * half;
 #pragma unroll
@@ -376,7 +389,9 @@ diam_pass_body(const uint4 *__restrict__ ah, const uint4 *__restrict__ al,
                         for (int r = 0; r < 4; ++r) {
                             const int64_t i = r0 + 16 * rb + 4 * (lane / 16) + r;
                             const int64_t j = c0 + 16 * cc + lane % 16;
-                            if (acc[rb][cc][r] >= thr && i < j && j < n) {
+                            // (a NaN value, possible only when thr is minus
+                            // infinity, is re-evaluated too)
+                            if (!(acc[rb][cc][r] < thr) && i < j && j < n) {
                                 const double d = diam_exact_d2(X, M, i, j);
                                 if (diam_better(d, (int)i, (int)j, bd, bk, bl_)) {
                                     bd = d;
@@ -436,11 +451,20 @@ diam_pass_kernel(const uint4 *__restrict__ ah, const uint4 *__restrict__ al,
 }
 
 // The lexicographic best of all item slots. With n = 1 there is no pair:
-// (0, 0, 0).
+// (0, 0, 0); with a non-finite coordinate in X: (NaN, -1, -1).
 __global__ void __launch_bounds__(1024)
 diam_final_kernel(const DiamBest *__restrict__ slots, int64_t nslots, int64_t n,
-                  double *__restrict__ d2_out, int32_t *__restrict__ pair_out)
+                  const uint32_t *__restrict__ counters, double *__restrict__ d2_out,
+                  int32_t *__restrict__ pair_out)
 {
+    if (counters[2] != 0u) {
+        if (threadIdx.x == 0) {
+            *d2_out = __builtin_nan("");
+            pair_out[0] = -1;
+            pair_out[1] = -1;
+        }
+        return;
+    }
     __shared__ DiamBest wb[1024 / kWave];
     double bd = -1.0;
     int bk = INT_MAX, bl_ = INT_MAX;
@@ -495,7 +519,7 @@ hipError_t diam_launch_ks(const DiameterArgs &a, const DiameterPlan &pl, hipStre
                        nsteps, a.X, a.M, a.counters, a.slots);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(diam_final_kernel, dim3(1), dim3(1024), 0, s, a.slots,
-                       (int64_t)pl.row_blocks * pl.chunks, a.n, a.d2, a.pair);
+                       (int64_t)pl.row_blocks * pl.chunks, a.n, a.counters, a.d2, a.pair);
     return hipGetLastError();
 }
 

@@ -106,3 +106,31 @@ def test_diameter_full_size_properties():
     i, j = rng.integers(0, X.shape[0], (2, 1_000_000))
     assert (((X64[i] - X64[j]) ** 2).sum(1) <= d2 * (1 + 1e-12)).all()
     check_centroid(c, X)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("bad", [float("nan"), float("inf"), float("-inf")])
+def test_nonfinite_coordinates_give_no_diameter(bad):
+    """A NaN or an infinite coordinate: the diameter is not defined, the GPU
+    reports (NaN, -1, -1) as the oracle does, and a farthest-point traversal
+    seeded with that pair is refused. Finite data that overflows fp32 squares
+    (coordinates near 3e38) still gives the oracle's pair."""
+    print(f"[diam-nonfinite] {bad}", flush=True)
+    rng = np.random.default_rng(21)
+    X = rng.normal(0.0, 1.0, (3000, 25)).astype(np.float32)
+    X[1234, 7] = bad
+    d2w, kw, lw = oracle.diameter(X)
+    assert np.isnan(d2w) and (kw, lw) == (-1, -1)
+    Xg = torch.from_numpy(X).to(DEV)
+    ws = torch.empty(km.kmeans_diameter_workspace_bytes(*X.shape), dtype=torch.uint8, device=DEV)
+    d2, pair, _ = km.kmeans_diameter(Xg, ws=ws)
+    assert np.isnan(d2.item()) and pair.cpu().tolist() == [-1, -1]
+    with pytest.raises(km.KmeansError):
+        km.kmeans_init_farthest(Xg, 4, seeds=pair)
+    # the same workspace then serves finite data (the flag is reset per call);
+    # squares near 1e77 overflow fp32, so every pair is re-evaluated in fp64
+    X[1234, 7] = 0.5
+    X[10, 3], X[2999, 3] = 3.0e38, -3.0e38
+    d2w, kw, lw = oracle.diameter(X)
+    d2, pair, _ = km.kmeans_diameter(torch.from_numpy(X).to(DEV), ws=ws)
+    assert pair.cpu().tolist() == [kw, lw] == [10, 2999] and d2.item() == d2w

@@ -109,3 +109,20 @@ def test_centroid_of_a_translated_grid():
     g = np.arange(-4, 5, dtype=np.float32)
     X = np.stack(np.meshgrid(g, g, g), -1).reshape(-1, 3) + np.float32(7.0)
     assert np.array_equal(oracle.centroid(X), np.full(3, 7.0, np.float32))
+
+
+def test_nonfinite_coordinates_leave_the_diameter_undefined():
+    """A NaN or an infinite coordinate anywhere: (nan, -1, -1), whatever the
+    other objects (the reading for data outside the real vectors the paper
+    defines the diameter on); finite data, however large, keeps its pair."""
+    rng = np.random.default_rng(3)
+    for bad in (np.nan, np.inf, -np.inf):
+        for where in ((0, 0), (5, 2), (19, 3)):
+            X = rng.normal(0.0, 1.0, (20, 4)).astype(np.float32)
+            X[where] = bad
+            d2, k, l = oracle.diameter(X)
+            assert np.isnan(d2) and (k, l) == (-1, -1)
+    X = rng.normal(0.0, 1.0, (20, 4)).astype(np.float32)
+    X[3, 1], X[11, 1] = 3.0e38, -3.0e38
+    d2, k, l = oracle.diameter(X)
+    assert (k, l) == (3, 11) and d2 > 3.5e77
