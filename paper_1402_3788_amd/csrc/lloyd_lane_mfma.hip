@@ -126,8 +126,9 @@ __host__ __device__ constexpr bool lane_a_in_lds(int KB) { return KB > 1; }
 // LDS of a workgroup: with accumulation [W][S][K][M] fp64 slabs, [W][K] int32
 // counts and [W][64] int32 slab offsets of the objects of the current tile
 // (rounded up to 16 bytes); with distances, the A table [3][KB][64] x 16 bytes
-// when there is more than one block, then the centres [K][M] in fp32 (read by
-// the fp64 re-decisions of close calls).
+// when there is more than one block, then the centres [K][M] in fp32 (one copy
+// per wave with one block, which needs no workgroup barrier, else one for the
+// workgroup; read by the fp64 decisions of close calls).
 [[maybe_unused]] __host__ __device__ inline size_t lane_acc_bytes(int M, int K, int W)
 {
     const int S = lane_slabs(lane_blocks(K));
@@ -371,7 +372,7 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
     }
 
     // the A table in LDS: [hi | lo | seeds][KB][64 lanes], 16 bytes each; then
-    // the centres, [K][M] fp32
+    // the centres, [K][M] fp32 (the wave's own copy with one block)
     uint4 *atab = reinterpret_cast<uint4 *>(smem + (kAcc ? lane_acc_bytes(M, K, W) : 0));
     float *ctab_w = reinterpret_cast<float *>(smem + (kAcc ? lane_acc_bytes(M, K, W) : 0) +
                                               lane_tab_bytes(K, (Mode)MODE)) +
@@ -544,15 +545,12 @@ lane_mfma_kernel(const float *__restrict__ X, int64_t n, const float *__restrict
                     // Close calls: only centres whose key is within thr of the
                     // best key can be the nearest (a key errs by at most half
                     // of thr, so any other centre's exact score exceeds the
-                    // best centre's). The object's features are loaded first
-                    // (in flight during the rest); then, for each column that
-                    // holds a close call, the keys are formed again exactly as
-                    // above from the same split operands, each lane marks its
-                    // candidates for the object of the column, and the four
-                    // lanes of an object combine their marks; the object's
-                    // lane decides among its candidates with fp64 distances in
-                    // ascending index order (lowest index on ties), the
-                    // centres read from the workgroup's LDS copy.
+                    // best centre's). For each column that holds a close call
+                    // the keys are formed again exactly as above from the same
+                    // split operands, each lane marks its candidates for the
+                    // object of the column, and the four lanes of an object
+                    // combine their marks; then the objects are decided one at
+                    // a time with fp64 distances (below).
                     const float lim_own = close ? b1 + thr : -INFINITY;
                     // the limits of the four lanes o16 + 16b (b = 0..3) in
                     // every lane: a 32-lane swap leaves rows r and r + 2 in
