@@ -317,7 +317,6 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
             // column l / 16, i.e. object l.
             float b1[kCols], b2[kCols];
             int lb[kCols];
-            float xsq[kCols];
             auto reset = [&]() {
 #pragma unroll
                 for (int c = 0; c < kCols; ++c) {
@@ -349,17 +348,24 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
                 }
                 mb1 = b1[0];
                 mb2 = b2[0];
-                mx = xsq[0];
                 ml = lb[0];
 #pragma unroll
                 for (int c = 1; c < kCols; ++c) {
                     const bool mine = g == c;
                     mb1 = mine ? b1[c] : mb1;
                     mb2 = mine ? b2[c] : mb2;
-                    mx = mine ? xsq[c] : mx;
                     ml = mine ? lb[c] : ml;
                 }
             };
+            // |x|^2 of the lane's own object (row `lane` of the tile), features
+            // in order; it enters only the guard bands, whose margins cover its
+            // fp32 rounding
+            mx = 0.f;
+#pragma unroll
+            for (int j = 0; j < M; ++j) {
+                const float v = tile[lane * M + j];
+                mx = __builtin_fmaf(v, v, mx);
+            }
             // Both passes keep two accumulator sets and two operand sets: the
             // matrix cores compute one centre block while the vector ALU scans
             // the previous one and the next block's operands arrive.
@@ -392,15 +398,13 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
             // Past M the A operands are zero, so the B values there only need
             // to be finite: with M >= 16 the tile's zero slack covers the last
             // row's reads past M and the rows are read straight through (the
-            // next object's features), else the reads are clamped to the row;
-            // |x|^2 masks them out.
+            // next object's features), else the reads are clamped to the row.
             {
                 constexpr bool kClampReads = M < 16;
                 uint32_t bh[kCols][KC][4], bl[kCols][KC][4];
 #pragma unroll
                 for (int c = 0; c < kCols; ++c) {
                     const float *row = tile + (16 * c + l16) * M;
-                    float acc = 0.f;
 #pragma unroll
                     for (int qc = 0; qc < KC; ++qc) {
                         float v[8];
@@ -408,14 +412,9 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
                         for (int e = 0; e < 8; ++e) {
                             const int f = 32 * qc + 8 * g + e;
                             v[e] = kClampReads ? row[f < M ? f : M - 1] : row[f];
-                            // in range for every lane group: no mask needed
-                            const bool always = 32 * qc + 24 + e < M;
-                            const float m = (always || f < M) ? v[e] : 0.f;
-                            acc = __builtin_fmaf(m, m, acc);
                         }
                         split_bf16x8(v, bh[c][qc], bl[c][qc]);
                     }
-                    xsq[c] = sum_rows<32>(sum_rows<16>(acc));
                 }
                 struct OpsH {
                     uint32_t ah[KC][4], al[KC][4];
@@ -505,9 +504,6 @@ lloyd_tile_kernel(const float *__restrict__ X, int64_t n, const float *__restric
                 mb1 = g1;
                 mb2 = g2;
                 ml = gl;
-                mx = xsq[0];
-#pragma unroll
-                for (int c = 1; c < kCols; ++c) mx = g == c ? xsq[c] : mx;
             }
             // Error of a pass-1 score against the exact score |c|^2 - 2 x.c:
             // with a = ah + al + ea, b = bh + bl + eb (|ea| <= 2^-16 |a|, |al|
