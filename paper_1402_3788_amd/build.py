@@ -20,7 +20,7 @@ LIB = os.path.join(HERE, "libkmeans_mi355x.so")
 # 38.9 with the instruction-level-parallelism one; the same as the default at
 # K = 64 on 2e7 objects; the tile kernel is slower with any of them); the L1
 # assignment kernel for instruction-level parallelism (an L1 iteration at
-# K = 16: 110.4 us against 113.3 with the default scheduler).
+# K = 16: 99.7 us against 103.4 with the default scheduler).
 UNIT_FLAGS = {"lloyd_lane_mfma.hip": ["-mllvm", "-amdgpu-sched-strategy=iterative-maxocc"],
               "lloyd_l1.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp"]}
 # (source, extra flags, object name); the kernel files are compiled once per

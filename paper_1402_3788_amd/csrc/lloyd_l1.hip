@@ -5,11 +5,11 @@
 // Euclidean path.
 //
 // One object per lane, on the vector ALU (the L1 distance is no contraction,
-// so there is nothing for the matrix cores). The centres sit in LDS padded to
-// MB = 4, 8, 16, 32 or 64 features with zeros and are read with uniform
-// (broadcast) 16-byte reads; each lane holds its object's features in
-// registers, zero past M, read from its wave's LDS tile slot. Padding adds
-// |0 - 0| = 0 exactly, so the fp32 sum is the sum over the M real features.
+// so there is nothing for the matrix cores). The kernel is compiled for each
+// feature count M. The centres sit in LDS, each padded with zeros to a
+// multiple of 4 features, and are read with uniform (broadcast) 16-byte
+// reads. Each lane holds its object's M features in registers, read from its
+// wave's LDS tile slot. Only the M real features enter a distance.
 //
 // fp32 error: each term |fl(x_j - c_j)| is within u of |x_j - c_j| and the
 // recursive sum of M non-negative terms adds gamma_{M-1}, so every computed
@@ -22,6 +22,8 @@
 
 #include <math.h>
 
+#include <utility>
+
 namespace lloyd {
 
 namespace {
@@ -31,14 +33,16 @@ constexpr size_t kL1MaxLds = 150 * 1024;
 
 typedef float f4v __attribute__((ext_vector_type(4)));
 
-int l1_padded(int M) { return M <= 4 ? 4 : M <= 8 ? 8 : M <= 16 ? 16 : M <= 32 ? 32 : 64; }
+// features per centre row in LDS: M rounded up to a multiple of 4
+__host__ __device__ constexpr int l1_row(int M) { return (M + 3) / 4 * 4; }
 
-template <int MB>
+template <int M>
 __global__ void __launch_bounds__(kL1MaxWaves * kWave)
-lloyd_l1_kernel(const float *__restrict__ X, int64_t n, int M, const float *__restrict__ C,
-                int K, int32_t *__restrict__ labels, float *__restrict__ min_d,
-                Ctl *__restrict__ ctl, int t, int fixed, int force64)
+lloyd_l1_kernel(const float *__restrict__ X, int64_t n, const float *__restrict__ C, int K,
+                int32_t *__restrict__ labels, float *__restrict__ min_d, Ctl *__restrict__ ctl,
+                int t, int fixed, int force64)
 {
+    constexpr int MB = l1_row(M);
     if (stop_before(ctl, t, fixed)) return;
     extern __shared__ __align__(16) float l1_lds[];
     const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave, W = blockDim.x / kWave;
@@ -75,13 +79,11 @@ lloyd_l1_kernel(const float *__restrict__ X, int64_t n, int M, const float *__re
         __builtin_amdgcn_wave_barrier();
         const int64_t i = q * kWave + lane;
 
-        // every lane reads every feature (the index clamped to the row, the
-        // value zeroed past M), so the features stay in registers, branch-free
-        float x[MB];
+        // the object's features stay in registers
+        float x[M];
 #pragma unroll
-        for (int j = 0; j < MB; ++j) {
-            const float v = slot[lane * M + (j < M ? j : M - 1)];
-            x[j] = j < M ? v : 0.f;
+        for (int j = 0; j < M; ++j) {
+            x[j] = slot[lane * M + j];
             asm volatile("" : "+v"(x[j]));            // keep it in a register: no re-read per centre
         }
 
@@ -92,10 +94,9 @@ lloyd_l1_kernel(const float *__restrict__ X, int64_t n, int M, const float *__re
 #pragma unroll
             for (int j4 = 0; j4 < MB / 4; ++j4) {
                 const f4v c = cen[k * (MB / 4) + j4];
-                d = d + fabsf(x[4 * j4 + 0] - c[0]);
-                d = d + fabsf(x[4 * j4 + 1] - c[1]);
-                d = d + fabsf(x[4 * j4 + 2] - c[2]);
-                d = d + fabsf(x[4 * j4 + 3] - c[3]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (4 * j4 + e < M) d = d + fabsf(x[4 * j4 + e] - c[e]);
             }
             if (d < b1) {
                 b2 = b1;
@@ -143,17 +144,27 @@ lloyd_l1_kernel(const float *__restrict__ X, int64_t n, int M, const float *__re
     }
 }
 
-template <int MB>
-hipError_t l1_launch_mb(const StepArgs &a, const L1Plan &pl, hipStream_t s)
+template <int M>
+hipError_t l1_launch_m(const StepArgs &a, const L1Plan &pl, hipStream_t s)
 {
-    auto kern = lloyd_l1_kernel<MB>;
+    auto kern = lloyd_l1_kernel<M>;
     static const size_t st = static_lds_bytes(reinterpret_cast<const void *>(kern));
     if (st > (size_t)kMaxLds || st + pl.lds_bytes > (size_t)kMaxLds)
         return hipErrorInvalidConfiguration;
     hipExtLaunchKernelGGL(kern, dim3(pl.groups), dim3(pl.waves * kWave), pl.lds_bytes, s,
-                          a.ev_start, a.ev_stop, 0, a.X, a.n, a.M, a.C, a.K, a.labels, a.min_d2,
-                          a.ctl, a.t, a.fixed, a.force64);
+                          a.ev_start, a.ev_stop, 0, a.X, a.n, a.C, a.K, a.labels, a.min_d2, a.ctl,
+                          a.t, a.fixed, a.force64);
     return hipGetLastError();
+}
+
+// the instance for M = a.M (1 .. kMaxM)
+template <int... Ms>
+hipError_t l1_dispatch(std::integer_sequence<int, Ms...>, const StepArgs &a, const L1Plan &pl,
+                       hipStream_t s)
+{
+    hipError_t r = hipErrorInvalidValue;
+    (void)((a.M == Ms + 1 ? (r = l1_launch_m<Ms + 1>(a, pl, s), true) : false) || ...);
+    return r;
 }
 
 }  // namespace
@@ -161,7 +172,7 @@ hipError_t l1_launch_mb(const StepArgs &a, const L1Plan &pl, hipStream_t s)
 L1Plan plan_l1(int64_t n, int M, int K)
 {
     L1Plan pl{};
-    const size_t cen = (size_t)K * l1_padded(M) * sizeof(float);
+    const size_t cen = (size_t)K * l1_row(M) * sizeof(float);
     const size_t slot = (size_t)kWave * M * sizeof(float);
     int W = cen + slot > kL1MaxLds ? 0 : (int)((kL1MaxLds - cen) / slot);
     if (W > kL1MaxWaves) W = kL1MaxWaves;
@@ -180,14 +191,8 @@ L1Plan plan_l1(int64_t n, int M, int K)
 hipError_t launch_l1(const StepArgs &a, const L1Plan &pl, hipStream_t s)
 {
     if (pl.waves < 1 || pl.groups < 1) return hipErrorInvalidConfiguration;
-    switch (l1_padded(a.M)) {
-    case 4: return l1_launch_mb<4>(a, pl, s);
-    case 8: return l1_launch_mb<8>(a, pl, s);
-    case 16: return l1_launch_mb<16>(a, pl, s);
-    case 32: return l1_launch_mb<32>(a, pl, s);
-    case 64: return l1_launch_mb<64>(a, pl, s);
-    }
-    return hipErrorInvalidValue;
+    if (a.M < 1 || a.M > kMaxM) return hipErrorInvalidValue;
+    return l1_dispatch(std::make_integer_sequence<int, kMaxM>{}, a, pl, s);
 }
 
 }  // namespace lloyd
