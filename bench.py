@@ -389,9 +389,11 @@ def main():
         result["diameter"] = time_diameter(torch, km, Xg)
 
     if not args.no_l1:
-        # the other metric: an L1 assign launch, then the accumulate-from-labels
-        # and centres launches of the Euclidean path (three launches per step)
+        # the other metric: the L1 assignment fused with the accumulation
+        # where its per-wave slabs leave enough waves (else an L1 assign launch
+        # and an accumulate-from-labels launch), then the centres launch
         T = 200
+        ws = km.workspace(n, M, K, dev, km.KMEANS_FIXED_ITERS | km.KMEANS_METRIC_L1)
         km.kmeans_run(Xg, K, Cg, 5, fixed_iters=True, metric="l1", out=out, ws=ws)
         torch.cuda.synchronize()
         _, _, _, _, tml = km.kmeans_run(Xg, K, Cg, T, fixed_iters=True, metric="l1", timing=True,

@@ -81,8 +81,9 @@ extern "C" {
  * steps 2/4 and the sums of Eq. (1)), then the centres and the congruence test
  * (Eq. (1), steps 6-7). HIP events are recorded on `stream` before the first
  * and after the last launch of the call (step_ms). The assigning launch of
- * every sample_every-th iteration (for the L1 metric the assign launch, else
- * the fused assign + accumulate launch) is made with hipExtLaunchKernel and a
+ * every sample_every-th iteration (for the L1 metric with K > 32 the L1 assign
+ * launch, else the fused assign + accumulate launch) is made with
+ * hipExtLaunchKernel and a
  * pair of events that its dispatch stamps at its start and end (assign_ms: the
  * kernel's own duration, nothing between launches). In early-stop mode step_ms
  * also contains the host's convergence polls; timing is meant for

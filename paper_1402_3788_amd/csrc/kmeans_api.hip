@@ -99,13 +99,19 @@ RunCache &run_cache()
 // counts G*K], with G the persistent workgroups of the accumulating launch.
 struct Layout {
     AccumPlan plan;
+    bool l1_fused;   // L1 runs assign and accumulate in one launch (plan is its plan)
     size_t sums_off, counts_off, total;
 };
 
 Layout layout(int64_t n, int32_t M, int32_t K, uint32_t flags)
 {
     Layout L{};
-    L.plan = plan_for(select_path(M, K, flags), n, M, K, kAssignAccum);
+    if (flags & KMEANS_METRIC_L1) {
+        const AccumPlan f = plan_lane_l1(n, M, K);
+        L.l1_fused = f.waves > 0;
+        if (L.l1_fused) L.plan = f;
+    }
+    if (!L.l1_fused) L.plan = plan_for(select_path(M, K, flags), n, M, K, kAssignAccum);
     const size_t km = (size_t)K * M;
     L.sums_off = align_up(sizeof(Ctl), 256);
     L.counts_off = align_up(L.sums_off + (size_t)L.plan.groups * km * sizeof(double), 256);
@@ -227,8 +233,8 @@ int run_impl(const float *X, int64_t n, int32_t M, int32_t K, const float *init_
     int rc = KMEANS_OK;
     const int fixed = (flags & KMEANS_FIXED_ITERS) ? 1 : 0;
     const bool l1 = (flags & KMEANS_METRIC_L1) != 0;
-    const L1Plan p1 = l1 ? plan_l1(n, M, K) : L1Plan{};
-    if (l1 && p1.waves < 1) return KMEANS_EUNSUPPORTED;
+    const L1Plan p1 = l1 && !L.l1_fused ? plan_l1(n, M, K) : L1Plan{};
+    if (l1 && !L.l1_fused && p1.waves < 1) return KMEANS_EUNSUPPORTED;
     const int every = timing == nullptr ? 0 : (timing->sample_every > 0 ? timing->sample_every : 16);
     // events: one before the first launch, one after the last, and a pair
     // stamped with the start and end of each sampled assigning launch
@@ -295,7 +301,11 @@ int run_impl(const float *X, int64_t n, int32_t M, int32_t K, const float *init_
                 a.ev_start = cache.ev[nev++];
                 a.ev_stop = cache.ev[nev++];
             }
-            if (l1) {
+            if (l1 && L.l1_fused) {
+                // L1 assignment fused with the sums of Eq. (1)
+                rc = hip_status(launch_lane_l1(a, L.plan, s));
+                a.ev_start = a.ev_stop = nullptr;
+            } else if (l1) {
                 // L1: assign, then the sums of Eq. (1) from those labels
                 rc = hip_status(launch_l1(a, p1, s));
                 a.ev_start = a.ev_stop = nullptr;

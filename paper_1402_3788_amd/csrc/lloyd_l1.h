@@ -16,4 +16,12 @@ L1Plan plan_l1(int64_t n, int M, int K);
 // a.ctl / a.t / a.fixed as the other assigning launches.
 hipError_t launch_l1(const StepArgs &a, const L1Plan &plan, hipStream_t s);
 
+// The L1 assignment fused with the accumulation of Eq. (1) in the direct-form
+// lane kernel (lloyd_lane.hip), for shapes where its per-wave fp64 slabs leave
+// enough waves per workgroup; waves = 0 in the plan when it is not used.
+// The partials go where the other accumulating launches put theirs, for
+// launch_centres with plan.groups.
+AccumPlan plan_lane_l1(int64_t n, int M, int K);
+hipError_t launch_lane_l1(const StepArgs &a, const AccumPlan &plan, hipStream_t s);
+
 }  // namespace lloyd

@@ -2,7 +2,9 @@
 // allows in place of Eq. (2): label = argmin_k sum_j |x_j - c_kj|, lowest k on
 // ties. Only the assignment changes; the sums of Eq. (1) and the centres are
 // formed by the accumulate-from-labels and centres launches shared with the
-// Euclidean path.
+// Euclidean path. This kernel serves the assign-only call and the iterations
+// with K > 32; below that an iteration assigns and accumulates in one launch
+// of the direct-form lane kernel (lloyd_lane.hip).
 //
 // One object per lane, on the vector ALU (the L1 distance is no contraction,
 // so there is nothing for the matrix cores). The kernel is compiled for each

@@ -25,6 +25,10 @@ hipError_t launch_lane_part_0(const StepArgs &, Mode, const AccumPlan &, hipStre
 hipError_t launch_lane_part_1(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
 hipError_t launch_lane_part_2(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
 hipError_t launch_lane_part_3(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
+hipError_t launch_lane_l1_part_0(const StepArgs &, const AccumPlan &, hipStream_t);
+hipError_t launch_lane_l1_part_1(const StepArgs &, const AccumPlan &, hipStream_t);
+hipError_t launch_lane_l1_part_2(const StepArgs &, const AccumPlan &, hipStream_t);
+hipError_t launch_lane_l1_part_3(const StepArgs &, const AccumPlan &, hipStream_t);
 hipError_t launch_lane_mfma_part_0(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
 hipError_t launch_lane_mfma_part_1(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
 hipError_t launch_lane_mfma_part_2(const StepArgs &, Mode, const AccumPlan &, hipStream_t);
