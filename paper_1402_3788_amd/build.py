@@ -20,9 +20,13 @@ LIB = os.path.join(HERE, "libkmeans_mi355x.so")
 # 38.9 with the instruction-level-parallelism one; the same as the default at
 # K = 64 on 2e7 objects; the tile kernel is slower with any of them); the L1
 # assignment kernel for instruction-level parallelism (an L1 iteration at
-# K = 16: 99.7 us against 103.4 with the default scheduler).
+# K = 16: 99.7 us against 103.4 with the default scheduler); the direct-form
+# lane kernel likewise (at n = 2e6, M = 25, K = 16: a fused L1 iteration
+# 66.2-66.6 us against 69.3-69.4, a direct-form Euclidean iteration 64.2-64.3
+# against 65.7-65.9).
 UNIT_FLAGS = {"lloyd_lane_mfma.hip": ["-mllvm", "-amdgpu-sched-strategy=iterative-maxocc"],
-              "lloyd_l1.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp"]}
+              "lloyd_l1.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp"],
+              "lloyd_lane.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp"]}
 # (source, extra flags, object name); the kernel files are compiled once per
 # part of the feature-count range so the template instantiations build in parallel
 PARTS = 4
